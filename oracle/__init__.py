@@ -1,0 +1,111 @@
+"""CPU oracle for the Coop sliding-window eviction search.
+
+TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the
+benchmark's CPU-baseline leg import this package; the GPU library never
+does, and the two share no code.  See coop_oracle.h for what is computed
+(section 3.1 Eq. (1) and section 3.3 of the Coop paper).
+
+All arrays are numpy: size/cost/seg_offsets/req_sizes/req_offsets uint64,
+kind uint8.  Results are uint64 arrays of shape (Q, 3) holding
+(start, end, cost); an infeasible request reads (2**64-1, 2**64-1, 2**64-1).
+"""
+import ctypes
+import os
+
+import numpy as np
+
+from . import build as _build
+
+INFEASIBLE = np.uint64(0xFFFFFFFFFFFFFFFF)
+
+_ERRORS = {-1: "invalid arguments", -4: "a run total overflows 64 bits",
+           -5: "input too large for brute force"}
+
+_lib = None
+
+
+class OracleError(RuntimeError):
+    def __init__(self, code: int):
+        super().__init__(f"oracle returned {code}: {_ERRORS.get(code, 'unknown error')}")
+        self.code = code
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_build.LIBRARY):
+            _build.build()
+        lib = ctypes.CDLL(_build.LIBRARY)
+        p64 = ctypes.POINTER(ctypes.c_uint64)
+        p8 = ctypes.POINTER(ctypes.c_uint8)
+        common = [p64, p64, p8, ctypes.c_uint64, p64, ctypes.c_uint64, p64, p64,
+                  ctypes.c_uint64, p64]
+        lib.coop_oracle_window_search.argtypes = common + [ctypes.c_int]
+        lib.coop_oracle_brute_windows.argtypes = common
+        lib.coop_oracle_brute_eq1.argtypes = common
+        for f in (lib.coop_oracle_window_search, lib.coop_oracle_brute_windows,
+                  lib.coop_oracle_brute_eq1):
+            f.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def _u64(a):
+    return np.ascontiguousarray(a, dtype=np.uint64)
+
+
+def _ptr(a, ctype):
+    return a.ctypes.data_as(ctypes.POINTER(ctype))
+
+
+def _args(size, cost, kind, seg_offsets, req_sizes, req_offsets):
+    size, cost, seg_offsets = _u64(size), _u64(cost), _u64(seg_offsets)
+    req_sizes, req_offsets = _u64(req_sizes), _u64(req_offsets)
+    kind = np.ascontiguousarray(kind, dtype=np.uint8)
+    if not (len(size) == len(cost) == len(kind)):
+        raise ValueError("size, cost and kind must have the same length")
+    if len(seg_offsets) != len(req_offsets) or len(seg_offsets) < 1:
+        raise ValueError("seg_offsets and req_offsets must both have num_segments + 1 entries")
+    keep = (size, cost, kind, seg_offsets, req_sizes, req_offsets)
+    cargs = [_ptr(size, ctypes.c_uint64), _ptr(cost, ctypes.c_uint64),
+             _ptr(kind, ctypes.c_uint8), len(size), _ptr(seg_offsets, ctypes.c_uint64),
+             len(seg_offsets) - 1, _ptr(req_sizes, ctypes.c_uint64),
+             _ptr(req_offsets, ctypes.c_uint64), len(req_sizes)]
+    return keep, cargs
+
+
+def window_search(size, cost, kind, seg_offsets, req_sizes, req_offsets, threads=1):
+    """Linear two-pointer sweep; returns uint64 (Q, 3) = (start, end, cost)."""
+    keep, cargs = _args(size, cost, kind, seg_offsets, req_sizes, req_offsets)
+    out = np.empty((len(keep[4]), 3), dtype=np.uint64)
+    rc = _load().coop_oracle_window_search(*cargs, _ptr(out, ctypes.c_uint64), int(threads))
+    if rc != 0:
+        raise OracleError(rc)
+    return out
+
+
+def brute_windows(size, cost, kind, seg_offsets, req_sizes, req_offsets):
+    """Every window enumerated; returns uint64 (Q, 3).  Snapshots <= 512 blocks."""
+    keep, cargs = _args(size, cost, kind, seg_offsets, req_sizes, req_offsets)
+    out = np.empty((len(keep[4]), 3), dtype=np.uint64)
+    rc = _load().coop_oracle_brute_windows(*cargs, _ptr(out, ctypes.c_uint64))
+    if rc != 0:
+        raise OracleError(rc)
+    return out
+
+
+def brute_eq1(size, cost, kind, seg_offsets, req_sizes, req_offsets):
+    """Eq. (1) over every evictable subset; returns uint64 (Q,) minimal cost."""
+    keep, cargs = _args(size, cost, kind, seg_offsets, req_sizes, req_offsets)
+    out = np.empty(len(keep[4]), dtype=np.uint64)
+    rc = _load().coop_oracle_brute_eq1(*cargs, _ptr(out, ctypes.c_uint64))
+    if rc != 0:
+        raise OracleError(rc)
+    return out
+
+
+def search_single(size, cost, kind, requests, threads=1):
+    """Convenience wrapper: one snapshot, a list of request sizes."""
+    requests = _u64(requests)
+    return window_search(size, cost, kind, [0, len(size)], requests, [0, len(requests)],
+                         threads=threads)

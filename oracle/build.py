@@ -1,0 +1,28 @@
+"""Compiles the CPU oracle (coop_oracle.c) into oracle/libcoop_oracle.so with gcc.
+
+Test infrastructure: the library it builds is used only by the tests, the
+smoke check and the benchmark's CPU-baseline leg.
+"""
+import os
+import subprocess
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SOURCE = os.path.join(HERE, "coop_oracle.c")
+LIBRARY = os.path.join(HERE, "libcoop_oracle.so")
+
+
+def build(verbose: bool = False) -> str:
+    """Always recompiles; returns the path of the shared library."""
+    tmp = LIBRARY + ".tmp"
+    cmd = ["gcc", "-std=c11", "-O2", "-Wall", "-Wextra", "-Werror", "-fPIC", "-shared",
+           "-pthread", "-o", tmp, SOURCE]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, LIBRARY)
+    return LIBRARY
+
+
+if __name__ == "__main__":
+    print(build(verbose="-v" in sys.argv))

@@ -1,0 +1,311 @@
+/*
+ * coop_oracle.c -- plain, slow, obviously correct CPU reference for the Coop
+ * sliding-window eviction search (section 3.1 Eq. (1), section 3.3).
+ *
+ * TEST INFRASTRUCTURE ONLY: called by the tests, the smoke check and the
+ * benchmark's CPU-baseline leg.  It shares nothing with the GPU library.
+ *
+ * Everything is unsigned 64-bit integer arithmetic; no rounding is involved,
+ * so any correct implementation must agree with this one bit for bit.
+ */
+#include "coop_oracle.h"
+
+#include <pthread.h>
+#include <stdatomic.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define NONE UINT64_MAX
+
+/* Kinds (section 3.3 and the Fig. 1 caption): free chunk, evictable tensor,
+ * unevictable tensor.  Any kind value of 2 or more is unevictable. */
+#define KIND_FREE 0
+#define KIND_EVICTABLE 1
+
+static int is_pinned(uint8_t k) { return k >= 2; }
+
+/* Cost of evicting one block: a free chunk is a zero-heuristic entry
+ * (section 3.3), a pinned block is never part of a window. */
+static uint64_t eviction_cost(uint8_t k, uint64_t c) {
+    return k == KIND_EVICTABLE ? c : 0;
+}
+
+/* Lexicographic order on (cost, bytes, start). */
+static int key_less(uint64_t c1, uint64_t b1, uint64_t s1,
+                    uint64_t c2, uint64_t b2, uint64_t s2) {
+    if (c1 != c2) return c1 < c2;
+    if (b1 != b2) return b1 < b2;
+    return s1 < s2;
+}
+
+/* Checks the CSR offsets of one batch dimension. */
+static int offsets_ok(const uint64_t *off, uint64_t n, uint64_t total) {
+    if (!off || off[0] != 0 || off[n] != total) return 0;
+    for (uint64_t b = 0; b < n; ++b)
+        if (off[b + 1] < off[b]) return 0;
+    return 1;
+}
+
+static int batch_ok(const uint64_t *size, const uint64_t *cost, const uint8_t *kind,
+                    uint64_t num_blocks, const uint64_t *seg_offsets,
+                    uint64_t num_segments, const uint64_t *req_sizes,
+                    const uint64_t *req_offsets, uint64_t num_requests,
+                    const void *out) {
+    if (num_blocks && (!size || !cost || !kind)) return 0;
+    if (num_requests && (!req_sizes || !out)) return 0;
+    if (num_segments == 0) return num_blocks == 0 && num_requests == 0;
+    return offsets_ok(seg_offsets, num_segments, num_blocks) &&
+           offsets_ok(req_offsets, num_segments, num_requests);
+}
+
+/* The precondition every implementation relies on: within each run (a
+ * maximal stretch of unpinned blocks) the byte total and the effective-cost
+ * total fit in 64 bits.  Then every window sum fits as well. */
+static int runs_fit(const uint64_t *size, const uint64_t *cost, const uint8_t *kind,
+                    uint64_t n) {
+    uint64_t bytes = 0, c = 0;
+    for (uint64_t k = 0; k < n; ++k) {
+        if (is_pinned(kind[k])) { bytes = 0; c = 0; continue; }
+        if (__builtin_add_overflow(bytes, size[k], &bytes)) return 0;
+        if (__builtin_add_overflow(c, eviction_cost(kind[k], cost[k]), &c)) return 0;
+    }
+    return 1;
+}
+
+/* ---------------------------------------------------------------------------
+ * Linear sweep (section 3.3).  The list is cut into runs at pinned blocks.
+ * Inside a run two indices, st and e, bound the window [st, e).  For each
+ * start st the end e is pushed right until the window holds at least S
+ * bytes; that is the shortest window beginning at st, and any longer one
+ * costs no less and holds no fewer bytes, so it is the only candidate for
+ * st.  Moving st one block right never moves the shortest end left, so e
+ * only ever advances and one pass over the run suffices.
+ * ------------------------------------------------------------------------- */
+static void sweep_one(const uint64_t *size, const uint64_t *cost, const uint8_t *kind,
+                      uint64_t n, uint64_t S, uint64_t res[3]) {
+    res[0] = res[1] = res[2] = NONE;
+    if (S == 0) { res[0] = res[1] = res[2] = 0; return; }
+
+    int found = 0;
+    uint64_t best_c = 0, best_b = 0, best_s = 0, best_e = 0;
+    uint64_t i = 0;
+    while (i < n) {
+        if (is_pinned(kind[i])) { ++i; continue; }
+        uint64_t r = i;                       /* the run is [i, r) */
+        while (r < n && !is_pinned(kind[r])) ++r;
+
+        uint64_t e = i, bytes = 0, c = 0;     /* window [st, e) */
+        for (uint64_t st = i; st < r; ++st) {
+            while (e < r && bytes < S) {
+                bytes += size[e];
+                c += eviction_cost(kind[e], cost[e]);
+                ++e;
+            }
+            if (bytes < S) break;             /* no later start can reach S */
+            if (!found || key_less(c, bytes, st, best_c, best_b, best_s)) {
+                found = 1;
+                best_c = c; best_b = bytes; best_s = st; best_e = e;
+            }
+            bytes -= size[st];
+            c -= eviction_cost(kind[st], cost[st]);
+        }
+        i = r;
+    }
+    if (found) { res[0] = best_s; res[1] = best_e; res[2] = best_c; }
+}
+
+/* Request q belongs to the snapshot b with req_offsets[b] <= q < req_offsets[b+1]. */
+static uint64_t owner_segment(const uint64_t *req_offsets, uint64_t num_segments,
+                              uint64_t q) {
+    uint64_t lo = 0, hi = num_segments;       /* answer in [lo, hi) */
+    while (hi - lo > 1) {
+        uint64_t mid = lo + (hi - lo) / 2;
+        if (req_offsets[mid] <= q) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+struct sweep_job {
+    const uint64_t *size, *cost;
+    const uint8_t *kind;
+    const uint64_t *seg_offsets, *req_sizes, *req_offsets;
+    uint64_t num_segments, num_requests;
+    uint64_t *out;
+    _Atomic uint64_t next;
+};
+
+#define SWEEP_CHUNK 16
+
+static void *sweep_worker(void *arg) {
+    struct sweep_job *job = (struct sweep_job *)arg;
+    for (;;) {
+        uint64_t q0 = atomic_fetch_add(&job->next, SWEEP_CHUNK);
+        if (q0 >= job->num_requests) break;
+        uint64_t q1 = q0 + SWEEP_CHUNK < job->num_requests ? q0 + SWEEP_CHUNK
+                                                           : job->num_requests;
+        for (uint64_t q = q0; q < q1; ++q) {
+            uint64_t b = owner_segment(job->req_offsets, job->num_segments, q);
+            uint64_t s0 = job->seg_offsets[b], n = job->seg_offsets[b + 1] - s0;
+            sweep_one(job->size + s0, job->cost + s0, job->kind + s0, n,
+                      job->req_sizes[q], job->out + 3 * q);
+        }
+    }
+    return NULL;
+}
+
+int coop_oracle_window_search(const uint64_t *size, const uint64_t *cost,
+                              const uint8_t *kind, uint64_t num_blocks,
+                              const uint64_t *seg_offsets, uint64_t num_segments,
+                              const uint64_t *req_sizes, const uint64_t *req_offsets,
+                              uint64_t num_requests, uint64_t *out, int num_threads) {
+    if (!batch_ok(size, cost, kind, num_blocks, seg_offsets, num_segments, req_sizes,
+                  req_offsets, num_requests, out))
+        return COOP_ORACLE_ERR_INVALID;
+    if (num_requests == 0) return COOP_ORACLE_OK;
+    for (uint64_t b = 0; b < num_segments; ++b) {
+        uint64_t s0 = seg_offsets[b];
+        if (!runs_fit(size + s0, cost + s0, kind + s0, seg_offsets[b + 1] - s0))
+            return COOP_ORACLE_ERR_OVERFLOW;
+    }
+
+    struct sweep_job job;
+    job.size = size; job.cost = cost; job.kind = kind;
+    job.seg_offsets = seg_offsets; job.req_sizes = req_sizes;
+    job.req_offsets = req_offsets; job.num_segments = num_segments;
+    job.num_requests = num_requests; job.out = out;
+    atomic_init(&job.next, 0);
+
+    if (num_threads <= 1) {
+        sweep_worker(&job);
+        return COOP_ORACLE_OK;
+    }
+    pthread_t *tid = (pthread_t *)calloc((size_t)num_threads, sizeof(pthread_t));
+    if (!tid) return COOP_ORACLE_ERR_INVALID;
+    int started = 0;
+    for (int t = 0; t < num_threads; ++t) {
+        if (pthread_create(&tid[t], NULL, sweep_worker, &job) != 0) break;
+        ++started;
+    }
+    if (started == 0) sweep_worker(&job);
+    for (int t = 0; t < started; ++t) pthread_join(tid[t], NULL);
+    free(tid);
+    return COOP_ORACLE_OK;
+}
+
+/* ---------------------------------------------------------------------------
+ * Brute force over windows: every [i, j) with no pinned block inside and at
+ * least S bytes is a candidate; each sum is recomputed from scratch.  The
+ * minimum of (cost, bytes, i, j) is the answer.
+ * ------------------------------------------------------------------------- */
+#define BRUTE_WINDOWS_MAX_N 512
+
+static void brute_windows_one(const uint64_t *size, const uint64_t *cost,
+                              const uint8_t *kind, uint64_t n, uint64_t S,
+                              uint64_t res[3]) {
+    res[0] = res[1] = res[2] = NONE;
+    if (S == 0) { res[0] = res[1] = res[2] = 0; return; }
+    int found = 0;
+    uint64_t bc = 0, bb = 0, bi = 0, bj = 0;
+    for (uint64_t i = 0; i < n; ++i) {
+        for (uint64_t j = i + 1; j <= n; ++j) {
+            int blocked = 0;
+            uint64_t bytes = 0, c = 0;
+            for (uint64_t k = i; k < j; ++k) {
+                if (is_pinned(kind[k])) { blocked = 1; break; }
+                bytes += size[k];
+                c += eviction_cost(kind[k], cost[k]);
+            }
+            if (blocked || bytes < S) continue;
+            int better = !found || c < bc || (c == bc && bytes < bb) ||
+                         (c == bc && bytes == bb && i < bi) ||
+                         (c == bc && bytes == bb && i == bi && j < bj);
+            if (better) { found = 1; bc = c; bb = bytes; bi = i; bj = j; }
+        }
+    }
+    if (found) { res[0] = bi; res[1] = bj; res[2] = bc; }
+}
+
+int coop_oracle_brute_windows(const uint64_t *size, const uint64_t *cost,
+                              const uint8_t *kind, uint64_t num_blocks,
+                              const uint64_t *seg_offsets, uint64_t num_segments,
+                              const uint64_t *req_sizes, const uint64_t *req_offsets,
+                              uint64_t num_requests, uint64_t *out) {
+    if (!batch_ok(size, cost, kind, num_blocks, seg_offsets, num_segments, req_sizes,
+                  req_offsets, num_requests, out))
+        return COOP_ORACLE_ERR_INVALID;
+    for (uint64_t b = 0; b < num_segments; ++b) {
+        uint64_t s0 = seg_offsets[b], n = seg_offsets[b + 1] - s0;
+        if (n > BRUTE_WINDOWS_MAX_N) return COOP_ORACLE_ERR_TOO_LARGE;
+        if (!runs_fit(size + s0, cost + s0, kind + s0, n)) return COOP_ORACLE_ERR_OVERFLOW;
+    }
+    for (uint64_t b = 0; b < num_segments; ++b) {
+        uint64_t s0 = seg_offsets[b], n = seg_offsets[b + 1] - s0;
+        for (uint64_t q = req_offsets[b]; q < req_offsets[b + 1]; ++q)
+            brute_windows_one(size + s0, cost + s0, kind + s0, n, req_sizes[q],
+                              out + 3 * q);
+    }
+    return COOP_ORACLE_OK;
+}
+
+/* ---------------------------------------------------------------------------
+ * Eq. (1) by exhaustion (section 3.3 names this 2^N enumeration as the naive
+ * approach).  For a subset E of the evictable blocks, M(E, L) is the largest
+ * byte total of adjacent available blocks, where a block is available when
+ * it is a free chunk or belongs to E.  The answer is min over E with
+ * M(E, L) >= S of the summed cost of E.
+ * ------------------------------------------------------------------------- */
+#define BRUTE_EQ1_MAX_EVICTABLE 20
+
+static uint64_t brute_eq1_one(const uint64_t *size, const uint64_t *cost,
+                              const uint8_t *kind, uint64_t n, uint64_t S,
+                              const uint64_t *evictable, unsigned m) {
+    uint64_t best = NONE;
+    for (uint64_t mask = 0; mask < (1ull << m); ++mask) {
+        uint64_t c = 0;
+        for (unsigned t = 0; t < m; ++t)
+            if (mask >> t & 1) c += cost[evictable[t]];
+        /* Largest contiguous available memory after evicting the subset. */
+        uint64_t largest = 0, run = 0;
+        unsigned t = 0;
+        for (uint64_t k = 0; k < n; ++k) {
+            int available;
+            if (kind[k] == KIND_FREE) {
+                available = 1;
+            } else if (kind[k] == KIND_EVICTABLE) {
+                while (t < m && evictable[t] < k) ++t;
+                available = (t < m && evictable[t] == k) ? (int)(mask >> t & 1) : 0;
+            } else {
+                available = 0;
+            }
+            run = available ? run + size[k] : 0;
+            if (run > largest) largest = run;
+        }
+        if (largest >= S && c < best) best = c;
+    }
+    return best;
+}
+
+int coop_oracle_brute_eq1(const uint64_t *size, const uint64_t *cost,
+                          const uint8_t *kind, uint64_t num_blocks,
+                          const uint64_t *seg_offsets, uint64_t num_segments,
+                          const uint64_t *req_sizes, const uint64_t *req_offsets,
+                          uint64_t num_requests, uint64_t *out_cost) {
+    if (!batch_ok(size, cost, kind, num_blocks, seg_offsets, num_segments, req_sizes,
+                  req_offsets, num_requests, out_cost))
+        return COOP_ORACLE_ERR_INVALID;
+    uint64_t evictable[BRUTE_EQ1_MAX_EVICTABLE];
+    for (uint64_t b = 0; b < num_segments; ++b) {
+        uint64_t s0 = seg_offsets[b], n = seg_offsets[b + 1] - s0;
+        unsigned m = 0;
+        for (uint64_t k = 0; k < n; ++k) {
+            if (kind[s0 + k] != KIND_EVICTABLE) continue;
+            if (m == BRUTE_EQ1_MAX_EVICTABLE) return COOP_ORACLE_ERR_TOO_LARGE;
+            evictable[m++] = k;
+        }
+        if (!runs_fit(size + s0, cost + s0, kind + s0, n)) return COOP_ORACLE_ERR_OVERFLOW;
+        for (uint64_t q = req_offsets[b]; q < req_offsets[b + 1]; ++q)
+            out_cost[q] = brute_eq1_one(size + s0, cost + s0, kind + s0, n,
+                                        req_sizes[q], evictable, m);
+    }
+    return COOP_ORACLE_OK;
+}

@@ -1,0 +1,89 @@
+/*
+ * coop_oracle.h -- CPU oracle for the Coop sliding-window eviction search.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This library is the correctness reference that
+ * the GPU path is compared against.  It is called by the test suite, by the
+ * smoke check and by the benchmark's CPU-baseline leg, and by nothing else.
+ * It shares no code, header, table or helper with the GPU library: it defines
+ * its own constants and reads plain host arrays.
+ *
+ * What it computes (Coop, "Memory is not a Commodity", section 3.1 Eq. (1)
+ * and section 3.3):
+ *
+ *   A pool snapshot is an address-sorted list of N blocks.  Block k has a
+ *   byte size size[k], a kind (0 = free chunk, 1 = evictable tensor,
+ *   any value >= 2 = unevictable/pinned tensor) and a cost cost[k].  Free
+ *   chunks count as zero-cost entries (section 3.3: free chunks are tensors
+ *   whose heuristic is zero); the stored cost of free and pinned blocks is
+ *   ignored.  Pinned blocks can never be evicted (Fig. 1 caption).
+ *
+ *   For a request of S bytes the result is the window [start, end), a run of
+ *   adjacent blocks containing no pinned block, whose byte total is >= S and
+ *   whose summed evictable cost is minimal.  Ties are broken by the smaller
+ *   byte total, then the lower start (the paper does not fix a tie-break;
+ *   this one makes the answer unique).  S == 0 yields the empty window
+ *   {0, 0, 0}.  No qualifying window yields {~0, ~0, ~0}.
+ *
+ * Batch layout (all host memory, caller-owned):
+ *   size[num_blocks], cost[num_blocks], kind[num_blocks]: blocks of all
+ *     snapshots, concatenated.
+ *   seg_offsets[num_segments + 1]: snapshot b is blocks
+ *     [seg_offsets[b], seg_offsets[b+1]); seg_offsets[0] == 0, non-decreasing,
+ *     seg_offsets[num_segments] == num_blocks.
+ *   req_sizes[num_requests], req_offsets[num_segments + 1]: the requests of
+ *     snapshot b are [req_offsets[b], req_offsets[b+1]), same rules, last
+ *     entry == num_requests.
+ *   out[3 * num_requests]: (start, end, cost) per request, start/end local to
+ *     the request's snapshot.
+ *
+ * Return codes: 0 ok, -1 invalid arguments, -4 a run's size or effective-cost
+ * total does not fit in 64 bits (the precondition the GPU path relies on),
+ * -5 input too large for a brute-force enumerator.
+ */
+#ifndef COOP_ORACLE_H
+#define COOP_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define COOP_ORACLE_OK 0
+#define COOP_ORACLE_ERR_INVALID (-1)
+#define COOP_ORACLE_ERR_OVERFLOW (-4)
+#define COOP_ORACLE_ERR_TOO_LARGE (-5)
+
+/* Linear two-pointer sweep per run (section 3.3), one request at a time,
+ * requests spread over num_threads POSIX threads (<= 0 means 1). */
+int coop_oracle_window_search(const uint64_t *size, const uint64_t *cost,
+                              const uint8_t *kind, uint64_t num_blocks,
+                              const uint64_t *seg_offsets, uint64_t num_segments,
+                              const uint64_t *req_sizes, const uint64_t *req_offsets,
+                              uint64_t num_requests, uint64_t *out, int num_threads);
+
+/* Brute force over every window [i, j) of every snapshot, keyed by
+ * (cost, bytes, i, j).  O(N^3) per request; snapshots must have <= 512
+ * blocks.  Same arguments and output as coop_oracle_window_search. */
+int coop_oracle_brute_windows(const uint64_t *size, const uint64_t *cost,
+                              const uint8_t *kind, uint64_t num_blocks,
+                              const uint64_t *seg_offsets, uint64_t num_segments,
+                              const uint64_t *req_sizes, const uint64_t *req_offsets,
+                              uint64_t num_requests, uint64_t *out);
+
+/* Eq. (1) taken literally: enumerate every subset of the evictable blocks of
+ * the snapshot, evict it, measure the largest contiguous run of available
+ * bytes (free chunks plus evicted blocks), and keep the cheapest subset whose
+ * run reaches S.  Writes the minimal cost per request to out_cost, or ~0 when
+ * no subset qualifies.  At most 20 evictable blocks per snapshot. */
+int coop_oracle_brute_eq1(const uint64_t *size, const uint64_t *cost,
+                          const uint8_t *kind, uint64_t num_blocks,
+                          const uint64_t *seg_offsets, uint64_t num_segments,
+                          const uint64_t *req_sizes, const uint64_t *req_offsets,
+                          uint64_t num_requests, uint64_t *out_cost);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* COOP_ORACLE_H */

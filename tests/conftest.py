@@ -1,0 +1,56 @@
+import os
+import sys
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+GOLDEN = os.path.join(ROOT, "tests", "golden")
+INF = np.uint64(0xFFFFFFFFFFFFFFFF)
+
+
+def pytest_configure(config):
+    config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU")
+    config.addinivalue_line("markers", "slow: takes more than a few seconds on the CPU")
+
+
+def parse_golden(path):
+    """Parses tests/golden/window_examples.txt into a list of
+    (name, size, cost, kind, [(S, expected (start, end, cost) or None)])."""
+    kinds = {"F": 0, "E": 1, "P": 2}
+    examples, cur, unit = [], None, 1
+
+    def val(tok):
+        return int(tok[:-1]) * unit if tok.endswith("u") else int(tok)
+
+    with open(path) as f:
+        for raw in f:
+            line = raw.split("#", 1)[0].strip()
+            if not line:
+                continue
+            tok = line.split()
+            if tok[0] == "example":
+                cur = {"name": tok[1], "size": [], "cost": [], "kind": [], "req": []}
+                examples.append(cur)
+                unit = 1
+            elif tok[0] == "unit":
+                unit = int(tok[1])
+            elif tok[0] == "block":
+                cur["kind"].append(kinds[tok[1]])
+                cur["size"].append(val(tok[2]))
+                cur["cost"].append(int(tok[3]))
+            elif tok[0] == "S":
+                assert tok[2] == "->"
+                exp = None if tok[3] == "infeasible" else tuple(int(t) for t in tok[3:6])
+                cur["req"].append((val(tok[1]), exp))
+            else:
+                raise ValueError(f"bad golden line: {raw!r}")
+    return examples
+
+
+@pytest.fixture(scope="session")
+def golden_examples():
+    return parse_golden(os.path.join(GOLDEN, "window_examples.txt"))

@@ -1,0 +1,70 @@
+"""The seeded generator draws what the input recipe says, deterministically."""
+import numpy as np
+import pytest
+
+import workloads
+from workloads import EVICTABLE, FREE, GRAIN, PINNED
+
+
+def _common(p):
+    assert p.size.dtype == np.uint64 and p.cost.dtype == np.uint64
+    assert p.kind.dtype == np.uint8
+    assert p.seg_offsets[0] == 0 and p.seg_offsets[-1] == p.num_blocks
+    assert p.req_offsets[0] == 0 and p.req_offsets[-1] == p.num_requests
+    assert np.all(np.diff(p.seg_offsets.astype(np.int64)) >= 0)
+    assert np.all(p.size % GRAIN == 0) and np.all(p.size >= GRAIN)
+    assert np.all(p.cost[p.kind != EVICTABLE] == 0)
+    assert set(np.unique(p.kind).tolist()) <= {FREE, EVICTABLE, PINNED}
+
+
+def test_deterministic():
+    a = workloads.make_config(1, 7, num_segments=16)
+    b = workloads.make_config(1, 7, num_segments=16)
+    c = workloads.make_config(1, 8, num_segments=16)
+    assert a.digest() == b.digest() != c.digest()
+
+
+@pytest.mark.parametrize("k", [0, 1, 2])
+def test_iid_workloads(k):
+    spec = workloads.CONFIGS[k]
+    p = workloads.make_config(k, 0, num_segments=min(spec.num_segments, 64))
+    _common(p)
+    assert np.all(np.diff(p.seg_offsets.astype(np.int64)) == spec.blocks[0])
+    assert np.all(np.diff(p.req_offsets.astype(np.int64)) == spec.requests_per_segment)
+    frac = np.bincount(p.kind, minlength=3) / p.num_blocks
+    tol = 4 * np.sqrt(0.25 / p.num_blocks)      # four binomial standard deviations
+    assert abs(frac[FREE] - spec.p_free) < tol and abs(frac[PINNED] - spec.p_pinned) < tol
+    assert p.size.max() <= spec.size_hi
+    ev = p.cost[p.kind == EVICTABLE]
+    assert ev.min() >= spec.cost_lo and ev.max() <= spec.cost_hi
+    assert p.req_sizes.min() >= spec.req_lo and p.req_sizes.max() <= spec.req_hi
+    # log-uniform sizes: the median sits near the geometric mean of the range
+    gm = np.sqrt(spec.size_lo * spec.size_hi)
+    assert 0.7 * gm < np.median(p.size.astype(np.float64)) < 1.4 * gm
+
+
+def test_ragged_clustered_workload():
+    spec = workloads.CONFIGS[3]
+    p = workloads.make_config(3, 0, num_segments=256)
+    _common(p)
+    nb = np.diff(p.seg_offsets.astype(np.int64))
+    assert nb.min() >= spec.blocks[0] and nb.max() <= spec.blocks[1]
+    frac_pinned = (p.kind == PINNED).mean()
+    assert 0.25 < frac_pinned < 0.35
+    assert p.size.max() <= spec.size_hi
+    # pinned blocks come in clusters: mean pinned-run length near 1/0.3
+    pin = (p.kind == PINNED).astype(np.int8)
+    starts = np.sum((pin[1:] == 1) & (pin[:-1] == 0))
+    assert 2.8 < pin.sum() / max(starts, 1) < 3.9
+
+
+def test_huge_pool_shape():
+    p = workloads.make_config(4, 0, blocks=(1 << 16, 1 << 16), requests_per_segment=32)
+    _common(p)
+    assert p.num_segments == 1 and p.num_requests == 32
+
+
+def test_from_lists():
+    p = workloads.from_lists([([512, 1024], [0, 5], [0, 1]), ([], [], [])], [[1, 2], [3]])
+    assert p.seg_offsets.tolist() == [0, 2, 2]
+    assert p.req_offsets.tolist() == [0, 2, 3]

@@ -1,0 +1,6 @@
+"""Seeded synthetic inputs for the Coop window search (no search arithmetic here)."""
+from .pools import (CONFIGS, EVICTABLE, FREE, GRAIN, PINNED, PoolSpec, Pools, from_lists,
+                    generate, make_config)
+
+__all__ = ["CONFIGS", "EVICTABLE", "FREE", "GRAIN", "PINNED", "PoolSpec", "Pools",
+           "from_lists", "generate", "make_config"]
