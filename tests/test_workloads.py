@@ -38,9 +38,11 @@ def test_iid_workloads(k):
     ev = p.cost[p.kind == EVICTABLE]
     assert ev.min() >= spec.cost_lo and ev.max() <= spec.cost_hi
     assert p.req_sizes.min() >= spec.req_lo and p.req_sizes.max() <= spec.req_hi
-    # log-uniform sizes: the median sits near the geometric mean of the range
-    gm = np.sqrt(spec.size_lo * spec.size_hi)
-    assert 0.7 * gm < np.median(p.size.astype(np.float64)) < 1.4 * gm
+    # log-uniform sizes: the median of log(size) sits at the middle of the
+    # log range (tolerance: four standard errors of a sample median)
+    mid = 0.5 * (np.log(spec.size_lo) + np.log(spec.size_hi))
+    se = 0.5 * (np.log(spec.size_hi) - np.log(spec.size_lo)) / np.sqrt(p.num_blocks)
+    assert abs(np.median(np.log(p.size.astype(np.float64))) - mid) < 4 * se + 0.01
 
 
 def test_ragged_clustered_workload():
