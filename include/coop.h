@@ -1,0 +1,117 @@
+/*
+ * coop.h -- C ABI of the MI355X (gfx950) batched sliding-window eviction
+ * search of Coop ("Memory is not a Commodity", section 3.3).
+ *
+ * The problem (section 3.1 Eq. (1), restated for windows in section 3.3):
+ * a pool snapshot is the address-sorted list of the blocks of a memory pool.
+ * Each block is a free chunk (cost 0), an evictable tensor with an eviction
+ * cost, or a pinned (unevictable) tensor.  For a request of S bytes, find the
+ * window [start, end) of adjacent blocks that contains no pinned block, holds
+ * at least S bytes in total, and has the smallest summed cost of its
+ * evictable blocks.  Ties are broken by the smaller byte total, then by the
+ * lower start, which makes the answer unique.  S == 0 gives the empty window
+ * {0, 0, 0}; a request no window satisfies gives {~0, ~0, ~0}.
+ *
+ * The library is stateless apart from a per-process call counter, allocates
+ * nothing, never synchronises the stream, and may be called from several
+ * host threads (with distinct workspaces).  It needs no HIP header: streams
+ * are passed as void* (a hipStream_t; NULL is the default stream).
+ */
+#ifndef COOP_H
+#define COOP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Block kinds stored in the kind[] array.  Every value >= COOP_PINNED is
+ * pinned: it can never be part of a window (Fig. 1 caption: parameters and
+ * buffers are unevictable).  A free chunk is a zero-cost entry whatever its
+ * stored cost (section 3.3). */
+typedef enum {
+    COOP_FREE = 0,
+    COOP_EVICTABLE = 1,
+    COOP_PINNED = 2
+} coop_kind_t;
+
+/* One result: the window [start, end), indices local to the request's
+ * snapshot, and its summed eviction cost.  Infeasible: all three ~0. */
+typedef struct {
+    uint64_t start;
+    uint64_t end;
+    uint64_t cost;
+} coop_window_t;
+
+typedef enum {
+    COOP_OK = 0,
+    COOP_ERR_INVALID = -1,   /* null pointer with a nonzero count, bad sizes */
+    COOP_ERR_WORKSPACE = -2, /* workspace missing or smaller than required */
+    COOP_ERR_HIP = -3        /* a HIP launch failed; the HIP error is cleared */
+} coop_status_t;
+
+/* Version of this ABI; bumped on any incompatible change. */
+#define COOP_ABI_VERSION 1
+int coop_abi_version(void);
+
+/* Human-readable text for a status code (static storage, never NULL). */
+const char *coop_status_string(int status);
+
+/* Bytes of device workspace coop_window_search needs for a batch of these
+ * dimensions.  Depends only on the three counts.  Returns COOP_ERR_INVALID
+ * if bytes_out is NULL or the batch is too large to launch. */
+coop_status_t coop_window_search_workspace_size(uint64_t num_blocks,
+                                                uint64_t num_segments,
+                                                uint64_t num_requests,
+                                                size_t *bytes_out);
+
+/*
+ * coop_window_search -- enqueue the search for every request of a batch.
+ *
+ * Blocks (device memory, structure of arrays, num_blocks entries each; the
+ * snapshots are concatenated):
+ *   size[k]  block size in bytes;
+ *   cost[k]  eviction cost, used only when kind[k] == COOP_EVICTABLE;
+ *   kind[k]  coop_kind_t (any value >= 2 is pinned).
+ * Snapshots (device): seg_offsets[num_segments + 1]; snapshot b is blocks
+ *   [seg_offsets[b], seg_offsets[b+1]).  seg_offsets[0] == 0, the entries
+ *   never decrease, seg_offsets[num_segments] == num_blocks.  Empty
+ *   snapshots are allowed.
+ * Requests (device): req_sizes[num_requests] in bytes;
+ *   req_offsets[num_segments + 1] with the same rules (last entry ==
+ *   num_requests); the requests of snapshot b are
+ *   [req_offsets[b], req_offsets[b+1]).
+ * out (device): num_requests results, in request order.
+ * workspace (device): at least coop_window_search_workspace_size() bytes,
+ *   256-byte aligned, owned by the caller; its contents need not be
+ *   initialised and are meaningless afterwards.  Two calls in flight at the
+ *   same time must not share a workspace.
+ * stream: hipStream_t the work is enqueued on; out is valid once the
+ *   stream has reached this point.
+ *
+ * Preconditions that live in device memory are not checked: the offset
+ * rules above, and that within every run (a maximal stretch of unpinned
+ * blocks) the byte total and the total cost of evictable blocks fit in
+ * 64 bits.  When they fail the results are unspecified (but every memory
+ * access stays inside the arrays described by the counts).
+ *
+ * Returns COOP_OK once the work is enqueued (and immediately, enqueuing
+ * nothing, when num_requests == 0); COOP_ERR_INVALID for a NULL pointer
+ * whose array is non-empty, requests without snapshots, or a batch too large
+ * to launch; COOP_ERR_WORKSPACE for a missing or too small workspace;
+ * COOP_ERR_HIP when the launch fails.
+ */
+coop_status_t coop_window_search(const uint64_t *size, const uint64_t *cost,
+                                 const uint8_t *kind, uint64_t num_blocks,
+                                 const uint64_t *seg_offsets, uint64_t num_segments,
+                                 const uint64_t *req_sizes, const uint64_t *req_offsets,
+                                 uint64_t num_requests, coop_window_t *out,
+                                 void *workspace, size_t workspace_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* COOP_H */

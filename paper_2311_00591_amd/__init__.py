@@ -1,0 +1,170 @@
+"""MI355X (gfx950) batched sliding-window eviction search of Coop.
+
+Thin ctypes binding over libcoop.so (include/coop.h): argument marshalling
+only; every step of the search runs in the HIP kernels.  PyTorch supplies the
+device memory and the stream.  There is no CPU fallback: without the built
+library or a GPU the calls raise.
+
+Unsigned 64-bit arrays travel in torch.int64 (or torch.uint64) storage; the
+bit patterns are what the library reads.  Results come back as int64 (Q, 3)
+tensors holding (start, end, cost); an infeasible request reads (-1, -1, -1),
+the two's-complement view of the all-ones sentinel.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIBRARY = os.path.join(_PKG, "libcoop.so")
+
+COOP_FREE, COOP_EVICTABLE, COOP_PINNED = 0, 1, 2
+INFEASIBLE = -1  # int64 view of the all-ones sentinel
+
+_STATUS = {0: "ok", -1: "invalid argument", -2: "workspace missing or too small",
+           -3: "HIP launch failed"}
+
+_lib = None
+
+
+class CoopError(RuntimeError):
+    def __init__(self, status: int, text: str):
+        super().__init__(f"coop status {status}: {text}")
+        self.status = status
+
+
+def load_library():
+    """Loads libcoop.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIBRARY):
+        raise ImportError(f"{LIBRARY} is missing: build it with __graft_entry__.build() "
+                          "(or python -m paper_2311_00591_amd._build)")
+    lib = ctypes.CDLL(LIBRARY)
+    u64, vp, sz = ctypes.c_uint64, ctypes.c_void_p, ctypes.c_size_t
+    lib.coop_abi_version.argtypes = []
+    lib.coop_abi_version.restype = ctypes.c_int
+    lib.coop_status_string.argtypes = [ctypes.c_int]
+    lib.coop_status_string.restype = ctypes.c_char_p
+    lib.coop_window_search_workspace_size.argtypes = [u64, u64, u64, ctypes.POINTER(sz)]
+    lib.coop_window_search_workspace_size.restype = ctypes.c_int
+    lib.coop_window_search.argtypes = [vp, vp, vp, u64, vp, u64, vp, vp, u64, vp, vp, sz, vp]
+    lib.coop_window_search.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != 0:
+        text = load_library().coop_status_string(status).decode()
+        raise CoopError(status, text)
+
+
+def workspace_size(num_blocks: int, num_segments: int, num_requests: int) -> int:
+    """Device workspace bytes coop_window_search needs for these counts."""
+    out = ctypes.c_size_t(0)
+    _check(load_library().coop_window_search_workspace_size(
+        int(num_blocks), int(num_segments), int(num_requests), ctypes.byref(out)))
+    return out.value
+
+
+def _u64_tensor(t: torch.Tensor, name: str, device) -> torch.Tensor:
+    if t.dtype not in (torch.int64, torch.uint64):
+        raise TypeError(f"{name} must be int64/uint64 storage, got {t.dtype}")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return t.data_ptr() if t is not None and t.numel() > 0 else None
+
+
+class WindowSearch:
+    """A prepared call for fixed device tensors: validates and marshals once,
+    so that repeated launches (benchmarks, serving loops) cost one ctypes
+    call each.  The tensors must stay alive and unchanged in shape."""
+
+    def __init__(self, size, cost, kind, seg_offsets, req_sizes, req_offsets,
+                 out: Optional[torch.Tensor] = None,
+                 workspace: Optional[torch.Tensor] = None):
+        device = size.device
+        if device.type != "cuda":
+            raise ValueError("coop window search runs on the GPU; tensors are on "
+                             f"{device} (there is no CPU fallback)")
+        lib = load_library()
+        self.size = _u64_tensor(size, "size", device)
+        self.cost = _u64_tensor(cost, "cost", device)
+        if kind.dtype != torch.uint8 or kind.device != device or not kind.is_contiguous():
+            raise TypeError("kind must be a contiguous uint8 tensor on the same device")
+        self.kind = kind
+        self.seg_offsets = _u64_tensor(seg_offsets, "seg_offsets", device)
+        self.req_sizes = _u64_tensor(req_sizes, "req_sizes", device)
+        self.req_offsets = _u64_tensor(req_offsets, "req_offsets", device)
+        n, b1, q = size.numel(), seg_offsets.numel(), req_sizes.numel()
+        if cost.numel() != n or kind.numel() != n:
+            raise ValueError("size, cost and kind must have the same length")
+        if b1 < 1 or req_offsets.numel() != b1:
+            raise ValueError("seg_offsets and req_offsets need num_segments + 1 entries")
+        self.num_blocks, self.num_segments, self.num_requests = n, b1 - 1, q
+        if out is None:
+            out = torch.empty((q, 3), dtype=torch.int64, device=device)
+        if out.shape != (q, 3) or out.dtype != torch.int64 or not out.is_contiguous():
+            raise ValueError("out must be a contiguous int64 (Q, 3) tensor")
+        self.out = out
+        need = workspace_size(n, b1 - 1, q)
+        if workspace is None:
+            workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+        if workspace.numel() * workspace.element_size() < need:
+            raise ValueError(f"workspace holds {workspace.numel()} bytes, needs {need}")
+        self.workspace = workspace
+        self.workspace_bytes = workspace.numel() * workspace.element_size()
+        self._fn = lib.coop_window_search
+        self._args = (_ptr(self.size), _ptr(self.cost), _ptr(self.kind), n,
+                      _ptr(self.seg_offsets), b1 - 1, _ptr(self.req_sizes),
+                      _ptr(self.req_offsets), q, _ptr(self.out), _ptr(self.workspace),
+                      self.workspace_bytes)
+
+    def launch(self, stream: Optional[int] = None) -> None:
+        """Enqueues the search on `stream` (default: torch's current stream)."""
+        if stream is None:
+            stream = torch.cuda.current_stream(self.size.device).cuda_stream
+        _check(self._fn(*self._args, stream))
+
+    def __call__(self, stream: Optional[int] = None) -> torch.Tensor:
+        self.launch(stream)
+        return self.out
+
+
+def window_search(size, cost, kind, seg_offsets, req_sizes, req_offsets, *,
+                  out: Optional[torch.Tensor] = None,
+                  workspace: Optional[torch.Tensor] = None,
+                  stream: Optional[int] = None) -> torch.Tensor:
+    """One batched search on device tensors; returns int64 (Q, 3)
+    (start, end, cost).  Asynchronous on `stream` like any torch op."""
+    ws = WindowSearch(size, cost, kind, seg_offsets, req_sizes, req_offsets, out, workspace)
+    return ws(stream)
+
+
+def to_device(pools, device="cuda"):
+    """Moves a host batch (numpy arrays, e.g. workloads.Pools) to the GPU as
+    the tensors window_search takes."""
+    import numpy as np
+
+    def u64(a):
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.uint64).view(np.int64)).to(device)
+
+    return (u64(pools.size), u64(pools.cost),
+            torch.from_numpy(np.ascontiguousarray(pools.kind, dtype=np.uint8)).to(device),
+            u64(pools.seg_offsets), u64(pools.req_sizes), u64(pools.req_offsets))
+
+
+__all__ = ["COOP_EVICTABLE", "COOP_FREE", "COOP_PINNED", "CoopError", "INFEASIBLE",
+           "LIBRARY", "WindowSearch", "load_library", "to_device", "window_search",
+           "workspace_size"]

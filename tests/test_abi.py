@@ -1,0 +1,94 @@
+"""The C ABI library loads, exports what include/coop.h declares, and
+validates host-visible arguments without touching a GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2311_00591_amd as coop
+from conftest import ROOT
+
+HEADER = os.path.join(ROOT, "include", "coop.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(coop_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    names = _declared_functions()
+    assert {"coop_window_search", "coop_window_search_workspace_size",
+            "coop_status_string", "coop_abi_version"} <= set(names)
+    lib = coop.load_library()
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_abi_version_matches_header():
+    m = re.search(r"#define COOP_ABI_VERSION (\d+)", open(HEADER).read())
+    assert coop.load_library().coop_abi_version() == int(m.group(1))
+
+
+def test_status_strings():
+    lib = coop.load_library()
+    for s in (0, -1, -2, -3, 7):
+        assert lib.coop_status_string(s)
+
+
+def test_workspace_size_depends_on_counts_only():
+    a = coop.workspace_size(4096 * 1024, 1024, 1024)
+    assert a == coop.workspace_size(4096 * 1024, 1024, 1024) > 0
+    assert coop.workspace_size(1 << 24, 1, 4096) >= coop.workspace_size(1 << 20, 1, 4096)
+    # partial storage is bounded: 2^22 keys of 32 bytes plus one counter per snapshot
+    assert coop.workspace_size(1 << 30, 1, 1 << 20) <= (1 << 22) * 32 + 8 + 256
+    lib = coop.load_library()
+    assert lib.coop_window_search_workspace_size(1, 1, 1, None) == -1
+    out = ctypes.c_size_t()
+    assert lib.coop_window_search_workspace_size(1, 1 << 40, 1, ctypes.byref(out)) == -1
+
+
+def _call(**kw):
+    args = dict(size=8, cost=8, kind=8, n=4, seg=8, B=1, req=8, roff=8, Q=1, out=8,
+                ws=8, wsb=1 << 30, stream=None)
+    args.update(kw)
+    return coop.load_library().coop_window_search(
+        args["size"], args["cost"], args["kind"], args["n"], args["seg"], args["B"],
+        args["req"], args["roff"], args["Q"], args["out"], args["ws"], args["wsb"],
+        args["stream"])
+
+
+def test_validation_rejects_bad_host_arguments():
+    # Non-null but never dereferenced: validation fails before any launch.
+    assert _call(Q=0) == 0
+    assert _call(Q=0, size=None, seg=None) == 0
+    assert _call(B=0) == -1
+    assert _call(size=None) == -1
+    assert _call(kind=None) == -1
+    assert _call(seg=None) == -1
+    assert _call(req=None) == -1
+    assert _call(roff=None) == -1
+    assert _call(out=None) == -1
+    assert _call(ws=None) == -2
+    assert _call(wsb=1) == -2
+    assert _call(B=1 << 40) == -1
+
+
+def test_no_cpu_fallback():
+    import torch
+    t = torch.zeros(4, dtype=torch.int64)
+    with pytest.raises(ValueError, match="GPU"):
+        coop.window_search(t, t, torch.zeros(4, dtype=torch.uint8), torch.tensor([0, 4]),
+                           torch.tensor([1]), torch.tensor([0, 1]))
+
+
+def test_gpu_path_shares_nothing_with_the_oracle():
+    gpu_src = open(os.path.join(ROOT, "paper_2311_00591_amd", "csrc",
+                                "coop_window_search.hip")).read()
+    oracle_src = open(os.path.join(ROOT, "oracle", "coop_oracle.c")).read()
+    assert "coop_oracle" not in gpu_src and "oracle" not in gpu_src.lower()
+    assert '#include "coop.h"' not in oracle_src
+    pkg = open(os.path.join(ROOT, "paper_2311_00591_amd", "__init__.py")).read()
+    assert "import oracle" not in pkg and "from oracle" not in pkg

@@ -1,0 +1,214 @@
+"""GPU results equal the CPU oracle's, bit for bit, through the C ABI.
+
+Every comparison is element by element on (start, end, cost); costs are
+integers, so there is no tolerance.  The standard workloads run at their
+full sizes in the same launch configuration the benchmark times, plus
+adversarial pools aimed at the tile edges, the halo, the streaming pass for
+runs longer than the staged region, the cross-workgroup combine and the
+strided tile assignment.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from checks import check_results
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+TILE = 4096
+U64MAX = (1 << 64) - 1
+
+
+def _threads():
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def gpu_search(pools, workspace_fill=None):
+    import paper_2311_00591_amd as coop
+    dev = coop.to_device(pools, "cuda")
+    ws = None
+    if workspace_fill is not None:
+        need = coop.workspace_size(pools.num_blocks, pools.num_segments, pools.num_requests)
+        ws = torch.full((max(need, 1),), workspace_fill, dtype=torch.uint8, device="cuda")
+    out = coop.window_search(*dev, workspace=ws)
+    torch.cuda.synchronize()
+    return out.cpu().numpy().view(np.uint64)
+
+
+def assert_parity(pools, got, label):
+    want = oracle.window_search(*pools.arrays(), threads=_threads())
+    bad = np.flatnonzero((got != want).any(axis=1))
+    if len(bad):
+        q = int(bad[0])
+        raise AssertionError(f"{label}: {len(bad)} of {len(want)} requests differ; first q={q} "
+                             f"S={int(pools.req_sizes[q])} gpu={got[q].tolist()} "
+                             f"oracle={want[q].tolist()}")
+
+
+def _announce(label):
+    print(f"[gpu case] {label}", flush=True)
+    sys.stdout.flush()
+
+
+@pytest.mark.parametrize("k", [0, 1, 2, 3, 4])
+def test_standard_workload_full_size(k):
+    _announce(f"workload {k} full size seed 0")
+    pools = workloads.make_config(k, 0)
+    got = gpu_search(pools)
+    assert_parity(pools, got, f"workload {k}")
+    if k != 4:
+        check_results(pools, got)
+    else:
+        check_results(pools, got, sample=range(0, pools.num_requests, 37))
+
+
+@pytest.mark.parametrize("k,seed,overrides", [
+    (0, 1, {}), (0, 2, {}),
+    (1, 1, {"num_segments": 256}), (1, 2, {"num_segments": 256}),
+    (2, 1, {"num_segments": 16}), (2, 2, {"num_segments": 16}),
+    (3, 1, {"num_segments": 512}), (3, 2, {"num_segments": 512}),
+    (4, 1, {"blocks": (1 << 21, 1 << 21), "requests_per_segment": 256}),
+    (4, 2, {"blocks": (1 << 21, 1 << 21), "requests_per_segment": 256}),
+])
+def test_standard_workload_other_seeds(k, seed, overrides):
+    _announce(f"workload {k} seed {seed} {overrides}")
+    pools = workloads.make_config(k, seed, **overrides)
+    assert_parity(pools, gpu_search(pools), f"workload {k} seed {seed}")
+
+
+def _pools(snaps, reqs):
+    return workloads.from_lists(snaps, reqs)
+
+
+def test_tile_edges_and_ragged_tails():
+    """Snapshots of lengths around multiples of the tile, pinned blocks at
+    and around every tile edge, requests from tiny to whole-run."""
+    _announce("tile edges")
+    rng = np.random.default_rng(11)
+    snaps, reqs = [], []
+    for n in [1, 2, 63, 64, 65, TILE - 1, TILE, TILE + 1, 2 * TILE - 1, 2 * TILE,
+              2 * TILE + 3, 3 * TILE + 777]:
+        size = (rng.integers(1, 64, size=n) * 512).astype(np.uint64)
+        kind = rng.choice([0, 1, 1, 1, 1, 1, 1, 2], size=n).astype(np.uint8)
+        for e in range(TILE, n + 2, TILE):
+            for d in (-2, -1, 0, 1):
+                if 0 <= e + d < n and rng.random() < 0.5:
+                    kind[e + d] = 2
+        cost = rng.integers(0, 1000, size=n).astype(np.uint64)
+        snaps.append((size, cost, kind))
+        reqs.append([0, 1, 512, 4096, 65536, 1 << 20, 1 << 22, 1 << 24, U64MAX])
+    pools = _pools(snaps, reqs)
+    assert_parity(pools, gpu_search(pools), "tile edges")
+
+
+def test_runs_longer_than_the_staged_region():
+    """One pin-free run far longer than tile + halo: windows of thousands of
+    blocks cross many tiles and are finished by the streaming pass."""
+    _announce("long runs")
+    rng = np.random.default_rng(12)
+    n = 40 * TILE + 123
+    size = (rng.integers(1, 16, size=n) * 512).astype(np.uint64)
+    kind = np.where(rng.random(n) < 0.2, 0, 1).astype(np.uint8)
+    cost = rng.integers(1, 10**6, size=n).astype(np.uint64)
+    mean = int(size.mean())
+    reqs = [mean * w for w in (1, 100, 1500, 5000, 20000, 39 * TILE)] + [int(size.sum())]
+    # a second snapshot: the same run cut by one pinned block in the middle
+    kind2 = kind.copy()
+    kind2[n // 2] = 2
+    pools = _pools([(size, cost, kind), (size, cost, kind2)], [reqs, reqs])
+    assert_parity(pools, gpu_search(pools), "long runs")
+
+
+def test_degenerate_snapshots():
+    _announce("degenerate snapshots")
+    z = np.zeros(0, dtype=np.uint64)
+    pinned = (np.full(5000, 512, np.uint64), np.zeros(5000, np.uint64),
+              np.full(5000, 2, np.uint8))
+    zero_size = (np.array([0, 0, 512, 0, 1024], np.uint64), np.array([3, 0, 5, 1, 2], np.uint64),
+                 np.array([1, 1, 1, 0, 1], np.uint8))
+    stored = (np.array([512, 512, 512], np.uint64), np.array([99, 98, 97], np.uint64),
+              np.array([0, 3, 255], np.uint8))
+    extreme = (np.array([1, 1], np.uint64), np.array([1 << 63, (1 << 63) - 1], np.uint64),
+               np.array([1, 1], np.uint8))
+    snaps = [(z, z, np.zeros(0, np.uint8)), pinned, zero_size, stored, extreme,
+             (z, z, np.zeros(0, np.uint8))]
+    reqs = [[0, 1, U64MAX], [0, 1, 512], [0, 1, 512, 1024, 1536, 2048], [1, 512, 513],
+            [1, 2, 3, U64MAX], []]
+    pools = _pools(snaps, reqs)
+    got = gpu_search(pools)
+    assert_parity(pools, got, "degenerate")
+    assert got[3 + 3 + 6 + 3 + 1].tolist() == [0, 2, U64MAX]  # extreme snapshot, S = 2
+
+
+def test_ties_across_tiles():
+    """Identical blocks everywhere: every window of the same length ties on
+    cost and bytes, so the lowest start must win across workgroups."""
+    _announce("ties")
+    n = 9 * TILE + 5
+    size = np.full(n, 1024, np.uint64)
+    cost = np.full(n, 7, np.uint64)
+    kind = np.ones(n, np.uint8)
+    kind[::997] = 2
+    pools = _pools([(size, cost, kind)], [[1, 1024, 5000, 1024 * 500, 1024 * 996, 1024 * 997]])
+    assert_parity(pools, gpu_search(pools), "ties")
+
+
+def test_many_requests_cap_workgroups_per_snapshot():
+    """With ~1M requests the partial budget allows only 4 workgroups per
+    snapshot, so a 20-tile snapshot is swept by workgroups striding over
+    tiles."""
+    _announce("strided tiles")
+    rng = np.random.default_rng(13)
+    n_big = 20 * TILE
+    size = (rng.integers(1, 64, size=n_big) * 512).astype(np.uint64)
+    kind = rng.choice([0, 1, 1, 1, 1, 2], size=n_big).astype(np.uint8)
+    cost = rng.integers(0, 10**9, size=n_big).astype(np.uint64)
+    snaps = [(size, cost, kind)]
+    reqs = [[int(x) for x in rng.integers(1, 1 << 26, size=6)]]
+    one = (np.array([512], np.uint64), np.array([1], np.uint64), np.array([1], np.uint8))
+    nsmall = (1 << 20) // 8
+    for _ in range(nsmall):
+        snaps.append(one)
+        reqs.append([1, 512, 513, 0, 7, 100, 600, 1])
+    pools = _pools(snaps, reqs)
+    import paper_2311_00591_amd as coop
+    assert coop.workspace_size(pools.num_blocks, pools.num_segments,
+                               pools.num_requests) <= (1 << 22) * 32 + 8 * (nsmall + 1) + 256
+    assert_parity(pools, gpu_search(pools), "strided tiles")
+
+
+def test_workspace_contents_do_not_matter_and_calls_repeat():
+    _announce("workspace garbage / repeat")
+    pools = workloads.make_config(2, 3, num_segments=6, blocks=(30000, 30000),
+                                  requests_per_segment=7)
+    a = gpu_search(pools, workspace_fill=0xFF)
+    b = gpu_search(pools, workspace_fill=0x00)
+    c = gpu_search(pools, workspace_fill=0x5A)
+    assert np.array_equal(a, b) and np.array_equal(b, c)
+    assert_parity(pools, a, "workspace garbage")
+
+
+def test_same_workspace_back_to_back():
+    """Repeated launches sharing one workspace on one stream (the per-call
+    counters must not leak between calls)."""
+    _announce("back to back")
+    import paper_2311_00591_amd as coop
+    pools = workloads.make_config(2, 4, num_segments=4, blocks=(20000, 20000),
+                                  requests_per_segment=3)
+    ws = coop.WindowSearch(*coop.to_device(pools, "cuda"))
+    outs = []
+    for _ in range(5):
+        outs.append(ws().clone())
+    torch.cuda.synchronize()
+    want = oracle.window_search(*pools.arrays())
+    for o in outs:
+        assert np.array_equal(o.cpu().numpy().view(np.uint64), want)
