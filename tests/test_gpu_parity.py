@@ -212,3 +212,35 @@ def test_same_workspace_back_to_back():
     want = oracle.window_search(*pools.arrays())
     for o in outs:
         assert np.array_equal(o.cpu().numpy().view(np.uint64), want)
+
+
+def test_huge_sizes_take_the_plain_prefix_path():
+    """Tiles whose byte total reaches 2^51 cannot pack the run id into the
+    key; they keep plain 64-bit prefixes and bisect each start."""
+    _announce("huge sizes (plain prefixes)")
+    rng = np.random.default_rng(14)
+    n = 3 * TILE + 500
+    size = (rng.integers(1, 1 << 12, size=n).astype(np.uint64) << np.uint64(38))
+    kind = rng.choice([0, 1, 1, 1], size=n).astype(np.uint8)
+    kind[::400] = 2  # runs of < 400 blocks keep run totals below 2^64
+    cost = rng.integers(0, 1 << 40, size=n).astype(np.uint64)
+    reqs = [1, 1 << 40, 1 << 50, 1 << 52, 1 << 55, 1 << 58, U64MAX]
+    pools = _pools([(size, cost, kind)], [reqs])
+    assert int(size[kind < 2].astype(object).sum()) >= 1 << 51
+    assert_parity(pools, gpu_search(pools), "huge sizes")
+
+
+def test_halo_that_would_overflow_the_key_field():
+    """A small tile whose last run continues into blocks so large that the
+    halo's byte prefix would reach 2^51: the halo is dropped and those windows
+    go through the streaming pass."""
+    _announce("halo overflow")
+    n = TILE + 300
+    size = np.full(n, 512, np.uint64)
+    size[TILE:] = np.uint64(1) << np.uint64(46)  # 64 of them reach 2^52
+    cost = np.arange(n, dtype=np.uint64) % np.uint64(97)
+    kind = np.ones(n, np.uint8)
+    kind[:TILE - 40:37] = 2
+    reqs = [1, 512 * 30, 1 << 46, (1 << 46) + 1, 1 << 50, 1 << 52, 1 << 55]
+    pools = _pools([(size, cost, kind)], [reqs])
+    assert_parity(pools, gpu_search(pools), "halo overflow")
