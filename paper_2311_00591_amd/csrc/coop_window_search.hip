@@ -77,9 +77,16 @@ static_assert(kTile == kThreads * kItems, "tile = threads x items");
 constexpr uint32_t kHaloCap = 256;  // also the chunk length of the streaming pass
 static_assert(kHaloCap <= kThreads, "one halo block per thread");
 constexpr uint32_t kStage = kTile + kHaloCap;
-constexpr uint32_t kXN = kStage + 16;  // keys of blocks [0, kStage] plus swizzle slack
+constexpr uint32_t kSent = 24;  // +infinity keys after the staged region (>= merge slice + 2)
+constexpr uint32_t kXN = kStage + 32;  // keys of blocks [0, kStage], sentinels, swizzle slack
 constexpr uint32_t kValBits = 51;
 constexpr uint64_t kValMask = (1ull << kValBits) - 1;
+// Blocks below 2^38 bytes keep any staged byte prefix (at most kStage < 2^13
+// blocks) below the 51-bit field of a key.
+constexpr uint64_t kBigBlock = 1ull << 38;
+static_assert(kStage < (1u << (kValBits - 38)), "staged prefixes must fit the key field");
+// A key above every real key and target that stays finite after adding S'.
+constexpr uint64_t kSentinel = ~0ull - kValMask;
 constexpr uint64_t kNone = ~0ull;
 constexpr uint64_t kPartialBudget = 1ull << 22;  // partial keys (32 B each)
 constexpr uint32_t kEpochShift = 24;             // counter = epoch << 24 | tickets
@@ -100,19 +107,13 @@ __device__ __forceinline__ bool key_less(const Key& a, const Key& b) {
 
 // Segmented-scan element over blocks where a pinned block closes its run:
 // `flag` says a pinned block occurred, q/c are the size and cost sums after
-// the last one, `cnt` counts pinned blocks, `all` is the byte total of every
-// unpinned block (saturating), an upper bound on every run prefix.
+// the last one, `cnt` counts pinned blocks.
 struct Seg {
     uint32_t flag, cnt;
-    uint64_t q, c, all;
+    uint64_t q, c;
 };
 
-__device__ __forceinline__ Seg seg_identity() { return Seg{0u, 0u, 0ull, 0ull, 0ull}; }
-
-__device__ __forceinline__ uint64_t add_sat(uint64_t a, uint64_t b) {
-    const uint64_t r = a + b;
-    return r < a ? kNone : r;
-}
+__device__ __forceinline__ Seg seg_identity() { return Seg{0u, 0u, 0ull, 0ull}; }
 
 // a precedes b.
 __device__ __forceinline__ Seg seg_combine(const Seg& a, const Seg& b) {
@@ -121,7 +122,6 @@ __device__ __forceinline__ Seg seg_combine(const Seg& a, const Seg& b) {
     r.cnt = a.cnt + b.cnt;
     r.q = b.flag ? b.q : a.q + b.q;
     r.c = b.flag ? b.c : a.c + b.c;
-    r.all = add_sat(a.all, b.all);
     return r;
 }
 
@@ -149,7 +149,6 @@ __device__ __forceinline__ Seg shfl_up_seg(const Seg& s, unsigned d) {
     r.cnt = __shfl_up(s.cnt, d, 64);
     r.q = shfl_up_u64(s.q, d);
     r.c = shfl_up_u64(s.c, d);
-    r.all = shfl_up_u64(s.all, d);
     return r;
 }
 
@@ -159,7 +158,6 @@ __device__ __forceinline__ Seg shfl_seg(const Seg& s, int src) {
     r.cnt = __shfl(s.cnt, src, 64);
     r.q = shfl_u64(s.q, src);
     r.c = shfl_u64(s.c, src);
-    r.all = shfl_u64(s.all, src);
     return r;
 }
 
@@ -185,8 +183,8 @@ struct Params {
     uint64_t num_virtual;  // floor(num_blocks / kTile) + num_segments
     uint64_t pc;
     uint64_t epoch;
-    uint32_t rot_bits;     // the grid is 2^rot_bits workgroups
-    uint32_t pad;
+    uint32_t rot_bits;     // the grid is 2^rot_bits workgroups (x) by slices (y)
+    uint32_t slices;       // request slices: workgroup y takes requests y, y + slices, ...
     double inv_slope;      // guess of b per virtual id, for the snapshot lookup
 };
 
@@ -366,25 +364,29 @@ __device__ __forceinline__ coop_window_t to_window(const Key& k, uint64_t S) {
     return coop_window_t{k.start, k.end, k.cost};
 }
 
-// Stages the blocks [pos, pos + m) after the tile (halo), cut at the first
-// pinned block: keys at stage indices [kTile, kTile + fp] (the last one is
-// the boundary after the staged blocks), continuing the prefixes cq/cc of
-// run `run`.  Returns fp, the number of staged blocks, and in `vend` the
-// byte prefix at the boundary.  In packed mode the keys carry the run id;
-// otherwise aux holds it.  Five barriers.
+// Stages the blocks [pos, pos + m) after the tile (halo): keys at stage
+// indices [kTile, kTile + fp] (the last one is the boundary after the staged
+// blocks), continuing the prefixes cq/cc of run `run`.  The halo stops at the
+// first pinned block, or, in packed mode, before the first block of 2^38 bytes
+// or more (its prefix might not fit the key field); `cut` reports the second
+// case, in which the run goes on past the halo.  In packed mode the keys carry
+// the run id; otherwise aux holds it.  Returns fp.  Five barriers.
 __device__ uint32_t stage_halo(const Params& P, Smem& sm, uint64_t pos, uint32_t m, uint64_t cq,
-                               uint64_t cc, uint32_t run, bool packed, uint64_t& vend) {
+                               uint64_t cc, uint32_t run, bool packed, bool& cut) {
     const uint32_t tid = threadIdx.x;
-    bool pinned = true;
+    uint32_t stop = 2 * m;  // 2*index for a pinned block, 2*index+1 for an oversized one
     uint64_t sz = 0, ct = 0;
     if (tid < m) {
         const uint8_t kd = P.kind[pos + tid];
-        pinned = kd >= COOP_PINNED;
         sz = P.size[pos + tid];
         ct = P.cost[pos + tid];
         ct = kd == COOP_EVICTABLE ? ct : 0;
+        if (kd >= COOP_PINNED) stop = 2 * tid;
+        else if (packed && sz >= kBigBlock) stop = 2 * tid + 1;
     }
-    const uint32_t fp = block_min_u32(pinned ? tid : m, sm);
+    const uint32_t first = block_min_u32(stop, sm);
+    const uint32_t fp = first >> 1;
+    cut = fp < m && (first & 1u);
     const bool valid = tid < fp;
     Seg x = seg_identity();
     x.q = valid ? sz : 0;
@@ -402,9 +404,14 @@ __device__ uint32_t stage_halo(const Params& P, Smem& sm, uint64_t pos, uint32_t
         sm.xc[sw(kTile + fp)] = cc + tot.c;
         if (!packed) sm.aux[sw(kTile + fp)] = static_cast<uint16_t>(run);
     }
-    vend = cq + tot.q;
     __syncthreads();
     return fp;
+}
+
+// +infinity keys after the staged region [0, end]: the merge path reads past
+// the end of both sequences without bounds checks.  The caller synchronises.
+__device__ __forceinline__ void write_sentinels(Smem& sm, uint32_t end) {
+    if (threadIdx.x < kSent) sm.x[sw(end + 1 + threadIdx.x)] = kSentinel;
 }
 
 // Finishes the pending starts [cur, nt): they all lie in the tile's last
@@ -486,7 +493,9 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
     const uint64_t nb = s1 - s0;
     const uint64_t tiles = nb ? (nb + kTile - 1) >> kTileLog2 : 1;
     const uint64_t p = v - sn.first;  // wraps (and exits) if the offsets are malformed
-    if (p >= tiles || R == 0) return;
+    // request slice: this workgroup answers requests y, y + slices, ... of the snapshot
+    const uint32_t y = blockIdx.y;
+    if (p >= tiles || R == 0 || y >= R) return;
     // At most pc workgroups per snapshot: each takes `stride` consecutive tiles.
     const uint64_t stride = tiles <= P.pc ? 1 : (tiles + P.pc - 1) / P.pc;
     if (stride != 1 && p % stride != 0) return;
@@ -512,8 +521,8 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
             uint64_t sz[kItems], ct[kItems];
             uint8_t kd[kItems];
             load_items(P, t0, nt, sz, ct, kd);
-            uint64_t acc = 0, cacc = 0, all = 0;
-            uint32_t runs = 0, flag = 0, lflags = 0;
+            uint64_t acc = 0, cacc = 0;
+            uint32_t runs = 0, flag = 0, lflags = 0, big = 0;
             uint32_t xr[kItems];  // run id (pinned blocks before the block) within the thread
 #pragma unroll
             for (uint32_t j = 0; j < kItems; ++j) {
@@ -531,11 +540,11 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
                 } else {
                     acc += s_j;
                     cacc += c_j;
-                    all = add_sat(all, s_j);
+                    big |= s_j >= kBigBlock ? 1u : 0u;
                 }
             }
             Seg tot;
-            const Seg carry = block_exclusive_scan(Seg{flag, runs, acc, cacc, all}, sm, tot);
+            const Seg carry = block_exclusive_scan(Seg{flag, runs, acc, cacc}, sm, tot);
 #pragma unroll
             for (uint32_t j = 0; j < kItems; ++j) {
                 const bool own = (lflags >> j) & 1u;
@@ -546,8 +555,8 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
             const uint64_t lastq = flag ? acc : carry.q + acc;  // prefix after the last block
             const uint64_t lastc = flag ? cacc : carry.c + cacc;
             const uint32_t lastr = carry.cnt + runs;
-            // every run prefix is at most the byte total of the tile's unpinned blocks
-            packed = tot.all < kValMask;
+            // with every block below 2^38 bytes, every prefix fits the key field
+            packed = !__syncthreads_or(big);
 #pragma unroll
             for (uint32_t j = 0; j < kItems; ++j) {
                 const uint32_t s = sw(i0 + j);
@@ -580,29 +589,19 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
                 const uint64_t pos = t0 + kTile;
                 const uint64_t left = s1 - pos;
                 const uint32_t m = static_cast<uint32_t>(left < kHaloCap ? left : kHaloCap);
-                uint64_t vend;
-                const uint32_t fp = stage_halo(P, sm, pos, m, xb & vmask, xcb, runb, packed, vend);
-                if (packed && vend >= kValMask) {
-                    // the halo's byte prefix would leave the field: keep only the tile;
-                    // the run goes on (fp >= 1 here), so its windows may leave the tile
-                    __syncthreads();
-                    if (tid == 0) {
-                        sm.x[sw(kTile)] = xb;
-                        sm.xc[sw(kTile)] = xcb;
-                    }
-                    __syncthreads();
-                    end = kTile;
-                    open = true;
-                } else {
-                    end = kTile + fp;
-                    open = fp == m && left > m;  // neither a pinned block nor the snapshot end
-                }
+                bool cut;
+                const uint32_t fp = stage_halo(P, sm, pos, m, xb & vmask, xcb, runb, packed, cut);
+                end = kTile + fp;
+                // open: the run goes on past the staged blocks
+                open = cut || (fp == m && left > m);
             }
         }
         const uint32_t endrun = runb;  // the run reaching the end of the staged region
+        write_sentinels(sm, end);
+        __syncthreads();
 
-        // ---- 3. every request of the snapshot
-        for (uint64_t r = 0; r < R; ++r) {
+        // ---- 3. the snapshot's requests of this slice
+        for (uint64_t r = y; r < R; r += P.slices) {
             const uint64_t q = q0 + r;
             const uint64_t S = P.req_size[q];
             Key best = key_none();
@@ -628,19 +627,21 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
                         lo = before ? mid + 1 : lo;
                         hi = before ? hi : mid;
                     }
+                    // Past the ends the sentinels compare above every target, so all
+                    // remaining starts take "no end in the region" (e = end).  Starts
+                    // past nA are phantoms: their entries are never read.
                     uint32_t a = lo, bq = d - lo;
-                    uint64_t ta = a < nA ? sm.x[sw(a)] + Sc : kNone;
-                    uint64_t kb = bq < nB ? sm.x[sw(bq + 1)] : kNone;
+                    uint64_t ta = sm.x[sw(a)] + Sc;
+                    uint64_t kb = sm.x[sw(bq + 1)];
                     for (uint32_t st = d; st < dEnd; ++st) {
-                        const bool takeA = ta <= kb && a < nA;
+                        const bool takeA = ta <= kb;
                         uint16_t* dst = takeA ? &sm.aux[sw(a)] : &sm.sink[tid];
                         *dst = static_cast<uint16_t>(bq);
                         a += takeA ? 1u : 0u;
                         bq += takeA ? 0u : 1u;
-                        const uint32_t idx = takeA ? a : bq + 1;
-                        const uint64_t val = sm.x[sw(idx <= nB ? idx : nB)];
-                        ta = takeA ? (a < nA ? val + Sc : kNone) : ta;
-                        kb = takeA ? kb : (bq < nB ? val : kNone);
+                        const uint64_t val = sm.x[sw(takeA ? a : bq + 1)];
+                        ta = takeA ? val + Sc : ta;
+                        kb = takeA ? kb : val;
                     }
                     __syncthreads();
 #pragma unroll
@@ -703,8 +704,9 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
                     sm.xc[sw(kTile)] = xcb;
                     if (!packed) sm.aux[sw(kTile)] = static_cast<uint16_t>(runb);
                 }
-                __syncthreads();
                 end = kTile;  // later requests stream from the tile end
+                write_sentinels(sm, end);
+                __syncthreads();
             }
             best = block_min_key(best, sm);
             if (tid == 0) {
@@ -729,7 +731,7 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
     __syncthreads();
     if (tid == 0) {
         uint32_t last = 1;
-        if (G > 1) {
+        if (G > 1 || (P.slices > 1 && R > 1)) {
             uint64_t* ctr = P.counters + b;
             uint64_t old = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             uint64_t want;
@@ -739,7 +741,9 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
             } while (!__hip_atomic_compare_exchange_strong(ctr, &old, want, __ATOMIC_ACQ_REL,
                                                            __ATOMIC_RELAXED,
                                                            __HIP_MEMORY_SCOPE_AGENT));
-            last = (want & ((1ull << kEpochShift) - 1)) == G;
+            // every (tile group, slice) pair of the snapshot arrives once
+            const uint64_t arrivals = G * (R < P.slices ? R : P.slices);
+            last = (want & ((1ull << kEpochShift) - 1)) == arrivals;
         }
         sm.flag = last;
     }
@@ -766,12 +770,16 @@ struct Plan {
     uint64_t pc;           // partial slots per request
     uint64_t num_virtual;  // virtual workgroup ids
     uint32_t rot_bits;     // grid = 2^rot_bits workgroups
+    uint32_t slices;       // request slices (grid y)
     size_t part_bytes;     // partial keys
     size_t bytes;          // total workspace
 };
 
 // grid x block must stay below 2^32 work-items: 2^23 workgroups of 512 threads
 constexpr uint32_t kMaxRotBits = 23;
+constexpr uint64_t kWideGrid = 2048;  // workgroups wanted before slicing requests
+constexpr uint64_t kMaxSlices = 256;
+static_assert(kWideGrid * kMaxSlices < (1ull << kEpochShift), "tickets fit the counter");
 
 bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests, Plan* pl) {
     if (num_segments > (1ull << kMaxRotBits) || num_blocks > (1ull << 60) ||
@@ -787,6 +795,16 @@ bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests
     while ((1ull << bits) < pl->num_virtual) ++bits;
     if (bits > kMaxRotBits) return false;
     pl->rot_bits = bits;
+    // Few tiles but many requests per snapshot (one small pool, many requests):
+    // spread each snapshot's requests over up to kMaxSlices workgroups.
+    pl->slices = 1;
+    if (pl->num_virtual < kWideGrid && num_requests > num_segments) {
+        const uint64_t per_snapshot = (num_requests + num_segments - 1) / num_segments;
+        uint64_t want = (kWideGrid + pl->num_virtual - 1) / pl->num_virtual;
+        if (want > per_snapshot) want = per_snapshot;
+        if (want > kMaxSlices) want = kMaxSlices;
+        pl->slices = static_cast<uint32_t>(want);
+    }
     pl->part_bytes = (num_requests * pc * sizeof(Key) + 255) & ~static_cast<size_t>(255);
     pl->bytes = pl->part_bytes + num_segments * sizeof(uint64_t);
     return true;
@@ -851,11 +869,11 @@ coop_status_t coop_window_search(const uint64_t* size, const uint64_t* cost, con
     P.pc = pl.pc;
     P.epoch = g_calls.fetch_add(1, std::memory_order_relaxed) & kEpochMask;
     P.rot_bits = pl.rot_bits;
-    P.pad = 0;
+    P.slices = pl.slices;
     P.inv_slope = static_cast<double>(num_segments) /
                   (static_cast<double>(num_blocks) / kTile + static_cast<double>(num_segments));
 
-    hipLaunchKernelGGL(coop_window_search_kernel, dim3(1u << pl.rot_bits), dim3(kThreads), 0,
+    hipLaunchKernelGGL(coop_window_search_kernel, dim3(1u << pl.rot_bits, pl.slices), dim3(kThreads), 0,
                        static_cast<hipStream_t>(stream), P);
     if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
     return COOP_OK;
