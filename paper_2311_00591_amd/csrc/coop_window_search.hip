@@ -23,29 +23,34 @@
 //
 // Per tile
 // --------
-//  1. Stage: each thread loads kItems consecutive blocks (16-byte loads when
-//     aligned, all issued at once) and runs a segmented exclusive scan of size
-//     and of effective cost in registers (a pinned block closes its run); a
-//     block-wide scan joins the threads.  LDS receives, per block k, the key
-//     X[k] = (run id << 51) | (bytes of its run before k) and the matching
-//     cost prefix XC[k].  Keys are monotone over the whole tile, so "first
-//     end at or after S bytes in the same run" becomes a plain lower bound.
-//     Both arrays are XOR-swizzled so blocked and striped accesses avoid LDS
-//     bank conflicts.
-//  2. Halo: when the last run continues past the tile, up to kHaloCap more
-//     blocks of it (stopping at the first pinned block) are staged.
-//  3. Per request: the shortest window of every start is found for all
-//     starts at once by a merge path: the targets T_i = X[i] + S and the end
-//     keys X[k+1] are two sorted sequences; each thread merges a fixed-length
-//     slice (uniform work, no divergence) and records, for each start it
-//     meets, the first end whose key reaches its target.  Each thread then
-//     scores its own kItems starts (key (cost, bytes, start)) and a
-//     lexicographic argmin runs across the wavefront (shuffles) and the block
-//     (LDS).
-//  4. Starts whose window would end past the staged region (the run outlives
-//     the halo) are finished by a streaming pass over the rest of the run.
-// A tile whose run byte prefix reaches 2^51 (no room left for the run id)
-// keeps plain 64-bit prefixes and run ids, and bisects each start instead.
+//  1. Stage.  Each thread loads kItems consecutive blocks (16-byte loads when
+//     aligned); the first kHaloCap threads also load one block each of the
+//     halo, the blocks right after the tile, in the same round of loads.
+//     Three plain prefix sums run over the tile followed by the halo: bytes
+//     P, effective cost C (0 unless evictable) and the pinned count R.  A
+//     window [i, k) holds no pinned block iff R[i] == R[k], and then its bytes
+//     and cost are P[k] - P[i] and C[k] - C[i]; no reset at pinned blocks is
+//     needed.  The sums run per thread, per wavefront (DPP row shifts and
+//     broadcasts) and across the wavefronts (one barrier).  LDS receives, per
+//     staged boundary k, the key X[k] = R[k] << 51 | P[k] and C[k].  Keys
+//     increase with k, and for a start i the first end k with X[k] >= X[i] + S
+//     is its shortest window when R[k] == R[i], while no window from i exists
+//     inside the staged region otherwise.
+//  2. Requests.  Wavefronts take requests: one wavefront per request when the
+//     tile has at least as many requests as wavefronts, else up to kMaxWpr
+//     wavefronts share one.  The targets X[i] + S of the starts and the end
+//     keys X[k] are two sorted sequences; the lanes split their merge into
+//     equal slices of merge steps (merge path, one bisection per lane), and
+//     every step that takes a start meets that start's shortest window and
+//     scores it at once.  A lexicographic argmin over the lanes (DPP) gives
+//     the wavefront's answer; wavefronts sharing a request combine in LDS.
+//  3. Starts whose windows end past the staged region (the region's last run
+//     goes on) are a suffix of the tile, found by one search; the request's
+//     wavefront finishes them by walking the rest of the run 64 blocks at a
+//     time.
+// A tile that holds a block of 2^38 bytes or more keeps plain 64-bit
+// prefixes (P could outgrow the 51-bit field) with the run ids in a separate
+// array, stages no halo, and bisects per start.
 //
 // Combining tiles
 // ---------------
@@ -55,8 +60,9 @@
 // reduces the partials and writes the results.  Counters carry a per-call
 // epoch, so the workspace never needs clearing.
 //
-// All arithmetic is unsigned 64-bit integer; prefix differences are exact
-// whenever each run's byte and cost totals fit in 64 bits.
+// All arithmetic is unsigned 64-bit integer.  Prefix sums wrap modulo 2^64;
+// differences over a window are exact whenever each run's byte and cost
+// totals fit in 64 bits.
 
 #include <hip/hip_runtime.h>
 
@@ -74,25 +80,142 @@ constexpr uint32_t kItems = 8;
 constexpr uint32_t kTileLog2 = 12;
 constexpr uint32_t kTile = 1u << kTileLog2;
 static_assert(kTile == kThreads * kItems, "tile = threads x items");
-constexpr uint32_t kHaloCap = 256;  // also the chunk length of the streaming pass
-static_assert(kHaloCap <= kThreads, "one halo block per thread");
+constexpr uint32_t kHaloCap = 256;
+static_assert(kHaloCap <= 4 * 64, "the halo is scanned by the first four wavefronts");
 constexpr uint32_t kStage = kTile + kHaloCap;
-constexpr uint32_t kSent = 24;  // +infinity keys after the staged region (>= merge slice + 2)
-constexpr uint32_t kXN = kStage + 32;  // keys of blocks [0, kStage], sentinels, swizzle slack
+// Merge steps per lane at most: all starts and ends of a staged region over
+// one wavefront, rounded up to 2 mod 4 (see merge_steps).
+constexpr uint32_t kMaxSteps = ((kTile + kStage + 63) / 64 + 1) / 4 * 4 + 2;
+// LDS keys: boundaries [0, kStage], the sentinel after the last one, and the
+// positions a lane reads past the starts once they are used up.
+constexpr uint32_t kXN = ((kStage + 2 > kTile + kMaxSteps + 1 ? kStage + 2 : kTile + kMaxSteps + 1) +
+                          7) / 8 * 8;
 constexpr uint32_t kValBits = 51;
 constexpr uint64_t kValMask = (1ull << kValBits) - 1;
-// Blocks below 2^38 bytes keep any staged byte prefix (at most kStage < 2^13
-// blocks) below the 51-bit field of a key.
-constexpr uint64_t kBigBlock = 1ull << 38;
+constexpr uint32_t kRunShift = kValBits - 32;  // run id position in the high word of a key
+// With every block below 2^38 bytes, any staged prefix (at most kStage < 2^13
+// blocks) fits the 51-bit field, and no prefix wraps.
+constexpr uint32_t kBigHiLog2 = 38 - 32;
 static_assert(kStage < (1u << (kValBits - 38)), "staged prefixes must fit the key field");
-// A key above every real key and target that stays finite after adding S'.
-constexpr uint64_t kSentinel = ~0ull - kValMask;
+static_assert(kStage < (1u << 16), "pinned counts fit 16 bits");
 constexpr uint64_t kNone = ~0ull;
+constexpr uint32_t kNone32 = ~0u;
+constexpr uint32_t kMaxWpr = 4;                  // wavefronts that may share one request
 constexpr uint64_t kPartialBudget = 1ull << 22;  // partial keys (32 B each)
 constexpr uint32_t kEpochShift = 24;             // counter = epoch << 24 | tickets
 constexpr uint64_t kEpochMask = (1ull << 40) - 1;
 
+// DPP controls (GFX9 encoding).
+constexpr int kRowShr1 = 0x111, kRowShr2 = 0x112, kRowShr4 = 0x114, kRowShr8 = 0x118;
+constexpr int kRowBcast15 = 0x142, kRowBcast31 = 0x143;
+constexpr int kQuadXor1 = 0xB1, kQuadXor2 = 0x4E;  // quad_perm [1,0,3,2] and [2,3,0,1]
+constexpr int kRowHalfMirror = 0x141, kRowMirror = 0x140;
+
+// Lane move within the wavefront; lanes whose source is outside the row, or
+// whose row is masked off, get `old`.
+template <int Ctrl, int RowMask = 0xf>
+__device__ __forceinline__ uint32_t dpp32(uint32_t v, uint32_t old) {
+    return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(
+        static_cast<int>(old), static_cast<int>(v), Ctrl, RowMask, 0xf, false));
+}
+
+template <int Ctrl, int RowMask = 0xf>
+__device__ __forceinline__ uint64_t dpp64(uint64_t v, uint64_t old) {
+    const uint32_t lo = dpp32<Ctrl, RowMask>(static_cast<uint32_t>(v), static_cast<uint32_t>(old));
+    const uint32_t hi = dpp32<Ctrl, RowMask>(static_cast<uint32_t>(v >> 32),
+                                             static_cast<uint32_t>(old >> 32));
+    return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+__device__ __forceinline__ uint32_t readlane32(uint32_t v, uint32_t lane) {
+    return static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), static_cast<int>(lane)));
+}
+
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, uint32_t lane) {
+    return (static_cast<uint64_t>(readlane32(static_cast<uint32_t>(v >> 32), lane)) << 32) |
+           readlane32(static_cast<uint32_t>(v), lane);
+}
+
+__device__ __forceinline__ uint64_t shfl64(uint64_t v, uint32_t src) {
+    const uint32_t lo = __shfl(static_cast<uint32_t>(v), static_cast<int>(src), 64);
+    const uint32_t hi = __shfl(static_cast<uint32_t>(v >> 32), static_cast<int>(src), 64);
+    return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+__device__ __forceinline__ uint32_t uniform(uint32_t v) {
+    return static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(v)));
+}
+
+// Prefix-sum element: bytes, effective cost, and the pinned count in the low
+// 16 bits of r (blocks of 2^38 bytes or more are counted from bit 16 up).
+struct Sums {
+    uint64_t q, c;
+    uint32_t r;
+};
+
+template <int Ctrl, int RowMask>
+__device__ __forceinline__ void sum_step(Sums& s) {
+    s.q += dpp64<Ctrl, RowMask>(s.q, 0);
+    s.c += dpp64<Ctrl, RowMask>(s.c, 0);
+    s.r += dpp32<Ctrl, RowMask>(s.r, 0);
+}
+
+// Inclusive sums over the 16 lanes of each row.
+__device__ __forceinline__ void row_inclusive_sum(Sums& s) {
+    sum_step<kRowShr1, 0xf>(s);
+    sum_step<kRowShr2, 0xf>(s);
+    sum_step<kRowShr4, 0xf>(s);
+    sum_step<kRowShr8, 0xf>(s);
+}
+
+// Inclusive sums over the wavefront: rows, then row 0 into row 1 and row 2
+// into row 3, then row 1 into rows 2 and 3.
+__device__ __forceinline__ void wave_inclusive_sum(Sums& s) {
+    row_inclusive_sum(s);
+    sum_step<kRowBcast15, 0xa>(s);
+    sum_step<kRowBcast31, 0xc>(s);
+}
+
+__device__ __forceinline__ Sums readlane(const Sums& s, uint32_t lane) {
+    return Sums{readlane64(s.q, lane), readlane64(s.c, lane), readlane32(s.r, lane)};
+}
+
+// A lane's best window so far.  `excess` is bytes - S (>= 0 for a window that
+// meets the request), which orders like bytes and keeps every real window
+// below the empty value all-ones; `start` is a staged index.
+struct Cand {
+    uint64_t cost, excess;
+    uint32_t start;
+};
+
+__device__ __forceinline__ Cand cand_none() { return Cand{kNone, kNone, kNone32}; }
+
+__device__ __forceinline__ bool cand_less(const Cand& a, const Cand& b) {
+    if (a.cost != b.cost) return a.cost < b.cost;
+    if (a.excess != b.excess) return a.excess < b.excess;
+    return a.start < b.start;
+}
+
+template <int Ctrl, int RowMask>
+__device__ __forceinline__ void argmin_step(Cand& k) {
+    const Cand o{dpp64<Ctrl, RowMask>(k.cost, kNone), dpp64<Ctrl, RowMask>(k.excess, kNone),
+                 dpp32<Ctrl, RowMask>(k.start, kNone32)};
+    if (cand_less(o, k)) k = o;
+}
+
+// Lexicographic minimum over the wavefront; every lane gets it.
+__device__ __forceinline__ Cand wave_argmin(Cand k) {
+    argmin_step<kQuadXor1, 0xf>(k);
+    argmin_step<kQuadXor2, 0xf>(k);
+    argmin_step<kRowHalfMirror, 0xf>(k);
+    argmin_step<kRowMirror, 0xf>(k);
+    argmin_step<kRowBcast15, 0xa>(k);
+    argmin_step<kRowBcast31, 0xc>(k);
+    return Cand{readlane64(k.cost, 63), readlane64(k.excess, 63), readlane32(k.start, 63)};
+}
+
 // Candidate window: ordered by (cost, bytes, start); `end` rides along.
+// Start and end are snapshot-local.
 struct Key {
     uint64_t cost, bytes, start, end;
 };
@@ -104,68 +227,6 @@ __device__ __forceinline__ bool key_less(const Key& a, const Key& b) {
     if (a.bytes != b.bytes) return a.bytes < b.bytes;
     return a.start < b.start;
 }
-
-// Segmented-scan element over blocks where a pinned block closes its run:
-// `flag` says a pinned block occurred, q/c are the size and cost sums after
-// the last one, `cnt` counts pinned blocks.
-struct Seg {
-    uint32_t flag, cnt;
-    uint64_t q, c;
-};
-
-__device__ __forceinline__ Seg seg_identity() { return Seg{0u, 0u, 0ull, 0ull}; }
-
-// a precedes b.
-__device__ __forceinline__ Seg seg_combine(const Seg& a, const Seg& b) {
-    Seg r;
-    r.flag = a.flag | b.flag;
-    r.cnt = a.cnt + b.cnt;
-    r.q = b.flag ? b.q : a.q + b.q;
-    r.c = b.flag ? b.c : a.c + b.c;
-    return r;
-}
-
-__device__ __forceinline__ uint64_t shfl_up_u64(uint64_t v, unsigned d) {
-    const uint32_t lo = __shfl_up(static_cast<uint32_t>(v), d, 64);
-    const uint32_t hi = __shfl_up(static_cast<uint32_t>(v >> 32), d, 64);
-    return (static_cast<uint64_t>(hi) << 32) | lo;
-}
-
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
-    const uint32_t lo = __shfl_xor(static_cast<uint32_t>(v), m, 64);
-    const uint32_t hi = __shfl_xor(static_cast<uint32_t>(v >> 32), m, 64);
-    return (static_cast<uint64_t>(hi) << 32) | lo;
-}
-
-__device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
-    const uint32_t lo = __shfl(static_cast<uint32_t>(v), src, 64);
-    const uint32_t hi = __shfl(static_cast<uint32_t>(v >> 32), src, 64);
-    return (static_cast<uint64_t>(hi) << 32) | lo;
-}
-
-__device__ __forceinline__ Seg shfl_up_seg(const Seg& s, unsigned d) {
-    Seg r;
-    r.flag = __shfl_up(s.flag, d, 64);
-    r.cnt = __shfl_up(s.cnt, d, 64);
-    r.q = shfl_up_u64(s.q, d);
-    r.c = shfl_up_u64(s.c, d);
-    return r;
-}
-
-__device__ __forceinline__ Seg shfl_seg(const Seg& s, int src) {
-    Seg r;
-    r.flag = __shfl(s.flag, src, 64);
-    r.cnt = __shfl(s.cnt, src, 64);
-    r.q = shfl_u64(s.q, src);
-    r.c = shfl_u64(s.c, src);
-    return r;
-}
-
-// LDS slot of block index i: the low four bits are XORed with bits 3..6, a
-// permutation inside every aligned group of 16.  Thread t stages indices
-// 8t..8t+7, so for a fixed item the 16 lanes of a quarter-wave hit 16
-// different 8-byte bank pairs; consecutive indices stay distinct as well.
-__device__ __forceinline__ uint32_t sw(uint32_t i) { return i ^ ((i >> 3) & 15u); }
 
 struct Params {
     const uint64_t* size;
@@ -189,93 +250,13 @@ struct Params {
 };
 
 struct Smem {
-    uint64_t x[kXN];    // keys (run << 51 | byte prefix), or plain byte prefixes
-    uint64_t xc[kXN];   // exclusive effective-cost prefix
-    uint16_t aux[kXN];  // merge output (first end per start), or run ids
-    Seg wseg[kWaves];
-    Key wkey[kWaves];
-    uint32_t wmin[kWaves];
-    uint16_t sink[kThreads];  // per-lane target of merge writes that are not taken
-    uint32_t flag;
+    uint64_t x[kXN];    // keys R << 51 | P, or plain P in a tile with a huge block
+    uint64_t xc[kXN];   // C
+    uint16_t run[kXN];  // R, kept only in a tile with a huge block
+    Sums wsum[kWaves];  // per-wavefront totals of the tile
+    Sums hsum[4];       // per-wavefront totals of the halo
+    Key slot[kWaves];   // answers of wavefronts that share a request
 };
-
-// Exclusive block-wide scan of one Seg per thread; `total` receives the
-// aggregate of the whole block.  Each wave scans its lanes with shuffles;
-// the wave totals are scanned again by the first kWaves lanes of every wave.
-// Two barriers.
-__device__ Seg block_exclusive_scan(Seg x, Smem& sm, Seg& total) {
-    const uint32_t lane = threadIdx.x & 63u, w = threadIdx.x >> 6;
-    Seg inc = x;
-#pragma unroll
-    for (unsigned d = 1; d < 64; d <<= 1) {
-        const Seg o = shfl_up_seg(inc, d);
-        if (lane >= d) inc = seg_combine(o, inc);
-    }
-    Seg ex = shfl_up_seg(inc, 1);
-    if (lane == 0) ex = seg_identity();
-    if (lane == 63) sm.wseg[w] = inc;
-    __syncthreads();
-    Seg t = lane < kWaves ? sm.wseg[lane] : seg_identity();
-#pragma unroll
-    for (unsigned d = 1; d < kWaves; d <<= 1) {
-        const Seg o = shfl_up_seg(t, d);
-        if (lane >= d) t = seg_combine(o, t);
-    }
-    Seg before = shfl_seg(t, w ? static_cast<int>(w) - 1 : 0);
-    if (w == 0) before = seg_identity();
-    total = shfl_seg(t, kWaves - 1);
-    __syncthreads();
-    return seg_combine(before, ex);
-}
-
-// Block-wide minimum of a u32; result in every thread.  Two barriers.
-__device__ uint32_t block_min_u32(uint32_t x, Smem& sm) {
-    const uint32_t lane = threadIdx.x & 63u, w = threadIdx.x >> 6;
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) {
-        const uint32_t o = __shfl_xor(x, m, 64);
-        x = o < x ? o : x;
-    }
-    if (lane == 0) sm.wmin[w] = x;
-    __syncthreads();
-    uint32_t r = sm.wmin[0];
-#pragma unroll
-    for (uint32_t u = 1; u < kWaves; ++u) r = sm.wmin[u] < r ? sm.wmin[u] : r;
-    __syncthreads();
-    return r;
-}
-
-__device__ __forceinline__ Key shfl_xor_key(const Key& k, int m) {
-    Key o;
-    o.cost = shfl_xor_u64(k.cost, m);
-    o.bytes = shfl_xor_u64(k.bytes, m);
-    o.start = shfl_xor_u64(k.start, m);
-    o.end = shfl_xor_u64(k.end, m);
-    return o;
-}
-
-// Block-wide lexicographic argmin; the result is valid in thread 0 only.
-// Two barriers.
-__device__ Key block_min_key(Key k, Smem& sm) {
-    const uint32_t lane = threadIdx.x & 63u, w = threadIdx.x >> 6;
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) {
-        const Key o = shfl_xor_key(k, m);
-        if (key_less(o, k)) k = o;
-    }
-    if (lane == 0) sm.wkey[w] = k;
-    __syncthreads();
-    if (w == 0) {
-        k = lane < kWaves ? sm.wkey[lane] : key_none();
-#pragma unroll
-        for (int m = kWaves / 2; m >= 1; m >>= 1) {
-            const Key o = shfl_xor_key(k, m);
-            if (key_less(o, k)) k = o;
-        }
-    }
-    __syncthreads();
-    return k;
-}
 
 struct Snapshot {
     uint64_t b, s0, s1, q0, q1, first;  // first = f(b), the virtual id of its first tile
@@ -320,7 +301,7 @@ __device__ Snapshot locate_snapshot(const Params& P, uint64_t v) {
 }
 
 // Loads the kItems blocks [t0 + tid*kItems, +kItems) of a tile of nt blocks.
-// Blocks past nt read as pinned.  All loads are independent of each other.
+// Blocks past nt read as empty free blocks.  All loads are independent.
 __device__ __forceinline__ void load_items(const Params& P, uint64_t t0, uint32_t nt,
                                            uint64_t (&sz)[kItems], uint64_t (&ct)[kItems],
                                            uint8_t (&kd)[kItems]) {
@@ -353,7 +334,7 @@ __device__ __forceinline__ void load_items(const Params& P, uint64_t t0, uint32_
             const bool in = i < nt;
             sz[j] = in ? P.size[t0 + i] : 0;
             ct[j] = in ? P.cost[t0 + i] : 0;
-            kd[j] = in ? P.kind[t0 + i] : static_cast<uint8_t>(COOP_PINNED);
+            kd[j] = in ? P.kind[t0 + i] : static_cast<uint8_t>(COOP_FREE);
         }
     }
 }
@@ -364,124 +345,216 @@ __device__ __forceinline__ coop_window_t to_window(const Key& k, uint64_t S) {
     return coop_window_t{k.start, k.end, k.cost};
 }
 
-// Stages the blocks [pos, pos + m) after the tile (halo): keys at stage
-// indices [kTile, kTile + fp] (the last one is the boundary after the staged
-// blocks), continuing the prefixes cq/cc of run `run`.  The halo stops at the
-// first pinned block, or, in packed mode, before the first block of 2^38 bytes
-// or more (its prefix might not fit the key field); `cut` reports the second
-// case, in which the run goes on past the halo.  In packed mode the keys carry
-// the run id; otherwise aux holds it.  Returns fp.  Five barriers.
-__device__ uint32_t stage_halo(const Params& P, Smem& sm, uint64_t pos, uint32_t m, uint64_t cq,
-                               uint64_t cc, uint32_t run, bool packed, bool& cut) {
-    const uint32_t tid = threadIdx.x;
-    uint32_t stop = 2 * m;  // 2*index for a pinned block, 2*index+1 for an oversized one
-    uint64_t sz = 0, ct = 0;
-    if (tid < m) {
-        const uint8_t kd = P.kind[pos + tid];
-        sz = P.size[pos + tid];
-        ct = P.cost[pos + tid];
-        ct = kd == COOP_EVICTABLE ? ct : 0;
-        if (kd >= COOP_PINNED) stop = 2 * tid;
-        else if (packed && sz >= kBigBlock) stop = 2 * tid + 1;
-    }
-    const uint32_t first = block_min_u32(stop, sm);
-    const uint32_t fp = first >> 1;
-    cut = fp < m && (first & 1u);
-    const bool valid = tid < fp;
-    Seg x = seg_identity();
-    x.q = valid ? sz : 0;
-    x.c = valid ? ct : 0;
-    Seg tot;
-    const Seg ex = block_exclusive_scan(x, sm, tot);
-    const uint64_t rbits = packed ? static_cast<uint64_t>(run) << kValBits : 0;
-    if (valid) {
-        sm.x[sw(kTile + tid)] = rbits | (cq + ex.q);
-        sm.xc[sw(kTile + tid)] = cc + ex.c;
-        if (!packed) sm.aux[sw(kTile + tid)] = static_cast<uint16_t>(run);
-    }
-    if (tid == 0) {
-        sm.x[sw(kTile + fp)] = rbits | (cq + tot.q);
-        sm.xc[sw(kTile + fp)] = cc + tot.c;
-        if (!packed) sm.aux[sw(kTile + fp)] = static_cast<uint16_t>(run);
-    }
-    __syncthreads();
-    return fp;
+__device__ __forceinline__ uint64_t lds_u64(const uint64_t* base, uint32_t byte_off) {
+    return *reinterpret_cast<const uint64_t*>(reinterpret_cast<const char*>(base) + byte_off);
 }
 
-// +infinity keys after the staged region [0, end]: the merge path reads past
-// the end of both sequences without bounds checks.  The caller synchronises.
-__device__ __forceinline__ void write_sentinels(Smem& sm, uint32_t end) {
-    if (threadIdx.x < kSent) sm.x[sw(end + 1 + threadIdx.x)] = kSentinel;
+// Merge steps per lane for `total` merge elements over `lanes` lanes, rounded
+// up to 2 mod 4: lanes then start about an odd number of keys apart, which
+// spreads their first LDS reads over the banks.
+__device__ __forceinline__ uint32_t merge_steps(uint32_t total, uint32_t lanes) {
+    const uint32_t L = (total + lanes - 1) / lanes;
+    return ((L + 1) & ~3u) + 2;
 }
 
-// Finishes the pending starts [cur, nt): they all lie in the tile's last
-// run and their windows end past the staged region [0, end).  The rest of
-// the run is walked in chunks of kHaloCap blocks, staged (as inclusive
-// prefixes) over the halo space; each chunk resolves a prefix of the pending
-// starts, since their ends are monotone.  Candidates fold into `best`.
-// Uniform control flow.
-__device__ __forceinline__ void stream_pass(const Params& P, Smem& sm, uint32_t cur, uint32_t nt,
-                                            uint32_t end, bool packed, uint64_t t0, uint64_t s0,
-                                            uint64_t s1, uint64_t S, Key& best) {
-    const uint32_t tid = threadIdx.x;
-    const uint64_t tl = t0 - s0;
-    const uint64_t vmask = packed ? kValMask : kNone;
-    uint64_t cq = sm.x[sw(end)] & vmask, cc = sm.xc[sw(end)];
-    uint64_t pos = t0 + end;
-    __syncthreads();  // every thread has read the region end before it is reused
-    while (cur < nt && pos < s1) {
-        const uint64_t left = s1 - pos;
-        const uint32_t m = static_cast<uint32_t>(left < kHaloCap ? left : kHaloCap);
-        bool pinned = true;
-        uint64_t sz = 0, ct = 0;
-        if (tid < m) {
-            const uint8_t kd = P.kind[pos + tid];
-            pinned = kd >= COOP_PINNED;
-            sz = P.size[pos + tid];
-            ct = P.cost[pos + tid];
-            ct = kd == COOP_EVICTABLE ? ct : 0;
+// Packed keys.  This lane's slice of the merge of the targets X[i] + Sc
+// (starts i < nA) with the end keys X[1..nB]: merge steps [d, d + L).  Ties
+// take the start first, so a start is taken when the head end key is the
+// first one at or above its target: the shortest window from that start that
+// reaches S bytes, valid when both ends have the same run id.  Steps past the
+// lane's slice repeat work of the next lane (harmless: equal windows), and
+// starts past nA are ignored.  X[nB + 1] must be all-ones, which no target
+// exceeds: the end index never passes it.
+__device__ __forceinline__ void merge_pass(const Smem& sm, uint32_t nA, uint32_t nB, uint32_t d,
+                                           uint32_t L, uint64_t Sc, Cand& best,
+                                           uint32_t& best_end) {
+    // diagonal split: the number of starts among the first d merge elements
+    uint32_t lo = d > nB ? d - nB : 0, hi = d < nA ? d : nA;
+    while (lo < hi) {
+        const uint32_t mid = (lo + hi) >> 1;
+        // start `mid` precedes end key X[d - mid] iff its target is at or below it
+        const bool before = sm.x[mid] + Sc <= sm.x[d - mid];
+        lo = before ? mid + 1 : lo;
+        hi = before ? hi : mid;
+    }
+    uint32_t pA = lo * 8u, pB = (d - lo + 1) * 8u;  // byte offsets of X[a] and of X[b + 1]
+    const uint32_t endA = nA * 8u;
+    uint64_t bc = kNone, bx = kNone;
+    uint32_t bpa = kNone32, bpb = 0;
+    for (uint32_t k = 0; k < L; k += 2) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const uint64_t xa = lds_u64(sm.x, pA), kb = lds_u64(sm.x, pB);
+            const uint64_t ca = lds_u64(sm.xc, pA), cb = lds_u64(sm.xc, pB);
+            const uint64_t ta = xa + Sc;
+            const bool takeA = ta <= kb;
+            const bool same = (static_cast<uint32_t>(xa >> 32) ^ static_cast<uint32_t>(kb >> 32)) <
+                              (1u << kRunShift);
+            const bool valid = takeA & (pA < endA) & same;
+            const uint64_t cost = cb - ca, ex = kb - ta;  // ex = bytes - S
+            const bool better = valid & ((cost < bc) | ((cost == bc) & (ex < bx)));
+            bc = better ? cost : bc;
+            bx = better ? ex : bx;
+            bpa = better ? pA : bpa;
+            bpb = better ? pB : bpb;
+            pA += takeA ? 8u : 0u;
+            pB += takeA ? 0u : 8u;
         }
-        const uint32_t fp = block_min_u32(pinned ? tid : m, sm);
-        const bool valid = tid < fp;
-        Seg x = seg_identity();
-        x.q = valid ? sz : 0;
-        x.c = valid ? ct : 0;
-        Seg tot;
-        const Seg ex = block_exclusive_scan(x, sm, tot);
-        if (valid) {
-            sm.x[sw(kTile + tid)] = cq + ex.q + x.q;  // inclusive prefix at the chunk block
-            sm.xc[sw(kTile + tid)] = cc + ex.c + x.c;
+    }
+    // Within a lane starts are met in increasing order, so strict comparison
+    // kept the lowest start among equal (cost, bytes).
+    const Cand c{bc, bx, bpa == kNone32 ? kNone32 : bpa / 8u};
+    if (cand_less(c, best)) {
+        best = c;
+        best_end = bpb / 8u;
+    }
+}
+
+// Plain prefixes (a tile with a huge block): starts g, g + lanes, ... below
+// nA, each by two bisections: the end of its run, then its first end with
+// at least S bytes.
+__device__ __forceinline__ void plain_pass(const Smem& sm, uint32_t nA, uint32_t end, uint32_t g,
+                                           uint32_t lanes, uint64_t S, Cand& best,
+                                           uint32_t& best_end) {
+    for (uint32_t i = g; i < nA; i += lanes) {
+        const uint32_t run = sm.run[i];
+        const uint64_t base = sm.x[i];
+        uint32_t lo = i, hi = end;  // first k in [i, end) whose block closes the run
+        while (lo < hi) {
+            const uint32_t mid = (lo + hi) >> 1;
+            if (sm.run[mid + 1] != run) hi = mid; else lo = mid + 1;
         }
-        __syncthreads();
-        const uint64_t lastq = cq + tot.q;
-        uint32_t still = nt;
-        for (uint32_t i = cur + tid; i < nt; i += kThreads) {
-            const uint64_t base = sm.x[sw(i)] & vmask;
-            const uint64_t cbase = sm.xc[sw(i)];
-            if (fp > 0 && lastq - base >= S) {
-                uint32_t a = 0, hi = fp - 1;  // first chunk block with prefix - base >= S
-                while (a < hi) {
-                    const uint32_t mid = a + (hi - a) / 2;
-                    if (sm.x[sw(kTile + mid)] - base >= S) hi = mid; else a = mid + 1;
-                }
-                const Key cand{sm.xc[sw(kTile + a)] - cbase, sm.x[sw(kTile + a)] - base, tl + i,
-                               (pos - s0) + a + 1};
-                if (key_less(cand, best)) best = cand;
-            } else if (i < still) {
-                still = i;
+        const uint32_t rend = lo;
+        lo = i;
+        hi = rend;
+        while (lo < hi) {
+            const uint32_t mid = (lo + hi) >> 1;
+            if (sm.x[mid + 1] - base >= S) hi = mid; else lo = mid + 1;
+        }
+        if (lo < rend) {
+            const Cand c{sm.xc[lo + 1] - sm.xc[i], sm.x[lo + 1] - base - S, i};
+            if (cand_less(c, best)) {
+                best = c;
+                best_end = lo + 1;
             }
         }
-        cur = block_min_u32(still, sm);
-        if (fp < m) break;  // the run ends inside this chunk
+    }
+}
+
+// Uniform lower bound: the first i in [lo, hi) with pred(i) (pred monotone),
+// or hi.
+template <typename Pred>
+__device__ __forceinline__ uint32_t lower_bound(uint32_t lo, uint32_t hi, Pred pred) {
+    while (lo < hi) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (pred(mid)) hi = mid; else lo = mid + 1;
+    }
+    return lo;
+}
+
+// The first start whose window cannot end inside the staged region [0, end]
+// although its run reaches the region's end: starts i < nA with run id endrun
+// and fewer than S bytes from i to the region end.  Such starts form a suffix.
+__device__ __forceinline__ uint32_t pending_start(const Smem& sm, bool packed, uint32_t nA,
+                                                  uint64_t xend, uint32_t endrun, uint64_t S,
+                                                  uint64_t Sc) {
+    if (packed) {
+        // run id endrun and X[i] + Sc > X[end]
+        const uint64_t by_run = static_cast<uint64_t>(endrun) << kValBits;
+        const uint64_t by_bytes = xend >= Sc ? xend - Sc + 1 : 0;
+        const uint64_t thr = by_run > by_bytes ? by_run : by_bytes;
+        return lower_bound(0, nA, [&](uint32_t i) { return sm.x[i] >= thr; });
+    }
+    const uint32_t i0 = lower_bound(0, nA, [&](uint32_t i) { return sm.run[i] == endrun; });
+    return lower_bound(i0, nA, [&](uint32_t i) { return xend - sm.x[i] < S; });
+}
+
+// Finishes the pending starts [cur, nA): all lie in the staged region's last
+// run, which goes on at global block pos, where the run's prefixes are cq
+// (bytes) and cc (cost).  The wavefront walks the run 64 blocks at a time
+// (one per lane, wavefront prefix sums, the chunk kept in registers); each
+// chunk resolves a prefix of the pending starts, 64 at a time, since their
+// shortest ends are monotone.  Candidates fold into best / best_end (end
+// snapshot-local).
+__device__ void stream_pass(const Params& P, const Smem& sm, uint32_t cur, uint32_t nA, uint64_t pos,
+                            uint64_t s0, uint64_t s1, uint64_t cq, uint64_t cc, uint64_t vmask,
+                            uint64_t S, Cand& best, uint64_t& best_end) {
+    const uint32_t lane = threadIdx.x & 63u;
+    while (cur < nA && pos < s1) {
+        const uint64_t left = s1 - pos;
+        const uint32_t m = left < 64 ? static_cast<uint32_t>(left) : 64u;
+        const bool in = lane < m;
+        uint8_t kd = COOP_PINNED;
+        uint64_t sz = 0, ct = 0;
+        if (in) {
+            kd = P.kind[pos + lane];
+            sz = P.size[pos + lane];
+            ct = P.cost[pos + lane];
+        }
+        const uint64_t pinned = __ballot(kd >= COOP_PINNED);
+        const uint32_t fp = pinned ? static_cast<uint32_t>(__builtin_ctzll(pinned)) : 64u;  // <= m
+        const bool valid = lane < fp;
+        Sums s{valid ? sz : 0, valid && kd == COOP_EVICTABLE ? ct : 0, 0};
+        wave_inclusive_sum(s);
+        const uint64_t q = cq + s.q, c = cc + s.c;  // prefixes after this lane's block
+        const uint32_t lastl = fp ? fp - 1 : 0;
+        const uint64_t lastq = fp ? readlane64(q, lastl) : cq;
+        const uint64_t lastc = fp ? readlane64(c, lastl) : cc;
+        for (;;) {
+            const uint32_t i = cur + lane;
+            const bool act = i < nA;
+            const uint32_t ii = act ? i : nA - 1;
+            const uint64_t base = sm.x[ii] & vmask, cbase = sm.xc[ii];
+            const bool ok = act && fp > 0 && lastq - base >= S;
+            // the first chunk lane k < fp with q_k - base >= S
+            uint32_t lo = 0, hi = lastl;
+#pragma unroll
+            for (int st = 0; st < 6; ++st) {
+                const uint32_t mid = (lo + hi) >> 1;
+                const bool ge = shfl64(q, mid) - base >= S;
+                const bool more = lo < hi;
+                hi = more && ge ? mid : hi;
+                lo = more && !ge ? mid + 1 : lo;
+            }
+            const uint64_t qe = shfl64(q, lo), ce = shfl64(c, lo);
+            if (ok) {
+                const Cand cand{ce - cbase, qe - base - S, i};
+                if (cand_less(cand, best)) {
+                    best = cand;
+                    best_end = (pos - s0) + lo + 1;
+                }
+            }
+            const uint64_t res = __ballot(ok);
+            const uint32_t n = ~res ? static_cast<uint32_t>(__builtin_ctzll(~res)) : 64u;
+            cur += n;
+            if (n < 64 || cur >= nA) break;
+        }
+        if (fp < m) break;  // the run closes inside this chunk
         cq = lastq;
-        cc += tot.c;
+        cc = lastc;
         pos += m;
+    }
+}
+
+__device__ __forceinline__ void write_result(const Params& P, uint64_t q, uint64_t slot_index,
+                                             bool direct, bool first_tile, Key k, uint64_t S) {
+    if (direct) {
+        P.out[q] = to_window(k, S);
+    } else {
+        Key* slot = P.part + q * P.pc + slot_index;
+        if (!first_tile) {
+            const Key prev = *slot;
+            if (key_less(prev, k)) k = prev;
+        }
+        *slot = k;
     }
 }
 
 __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params P) {
     __shared__ Smem sm;
     const uint32_t tid = threadIdx.x;
+    const uint32_t lane = tid & 63u;
+    const uint32_t w = uniform(tid >> 6);
     // virtual id: the workgroup id rotated right by 5 bits within rot_bits bits
     const uint64_t v = (blockIdx.x >> 5) |
                        (static_cast<uint64_t>(blockIdx.x & 31u) << (P.rot_bits - 5));
@@ -503,223 +576,199 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
     const uint64_t G = stride == 1 ? tiles : (tiles + stride - 1) / stride;
     const uint64_t tau_end = p + stride < tiles ? p + stride : tiles;
     const bool direct = tiles == 1;
+    // requests of this slice, and wavefronts per request
+    const uint64_t K = (R - y + P.slices - 1) / P.slices;
+    uint32_t wpr = 1;
+    if (K < kWaves) {
+        uint32_t k2 = 1;
+        while (k2 < K) k2 <<= 1;
+        wpr = kWaves / k2 < kMaxWpr ? kWaves / k2 : kMaxWpr;
+    }
 
     for (uint64_t tau = p; tau < tau_end; ++tau) {
         const uint64_t t0 = s0 + (tau << kTileLog2);  // global index of the tile start
         const uint64_t tl = t0 - s0;                   // snapshot-local index of the tile start
         const uint32_t nt = static_cast<uint32_t>(s1 - t0 < kTile ? s1 - t0 : kTile);
-        // An opaque copy of the thread's first block index: addresses derived
-        // from it are recomputed in each loop instead of being kept live
-        // across the whole kernel (they would not fit in registers).
-        uint32_t i0 = tid * kItems;
-        asm volatile("" : "+v"(i0));
+        // halo blocks available after a full tile
+        const uint64_t after = s1 - t0 - nt;
+        const uint32_t hm = nt == kTile ? static_cast<uint32_t>(after < kHaloCap ? after : kHaloCap) : 0;
 
-        // ---- 1. stage: exclusive prefixes of this thread's kItems blocks
-        uint32_t pinmask = 0;
+        // ---- 1. stage
         bool packed;
+        uint32_t end;
+        uint64_t xend, xcend;
+        uint32_t endrun;
         {
             uint64_t sz[kItems], ct[kItems];
             uint8_t kd[kItems];
             load_items(P, t0, nt, sz, ct, kd);
-            uint64_t acc = 0, cacc = 0;
-            uint32_t runs = 0, flag = 0, lflags = 0, big = 0;
-            uint32_t xr[kItems];  // run id (pinned blocks before the block) within the thread
+            Sums h{0, 0, 0};
+            if (tid < hm) {
+                const uint64_t gp = t0 + kTile + tid;
+                const uint8_t k = P.kind[gp];
+                h.q = P.size[gp];
+                const uint64_t c = P.cost[gp];
+                h.c = k == COOP_EVICTABLE ? c : 0;
+                h.r = (k >= COOP_PINNED ? 1u : 0u) + ((h.q >> 32) >> kBigHiLog2 ? 1u << 16 : 0u);
+            }
+            const Sums hown = h;
+            // thread-local exclusive sums
+            Sums t{0, 0, 0};
+            uint32_t xr[kItems];
+            uint32_t hi_or = 0;
 #pragma unroll
             for (uint32_t j = 0; j < kItems; ++j) {
-                const uint64_t s_j = sz[j], c_j = kd[j] == COOP_EVICTABLE ? ct[j] : 0;
-                sz[j] = acc;  // from here on: byte / cost prefix of the run before block j
-                ct[j] = cacc;
-                xr[j] = runs;
-                lflags |= flag << j;
-                if (kd[j] >= COOP_PINNED) {
-                    pinmask |= 1u << j;
-                    acc = 0;
-                    cacc = 0;
-                    ++runs;
-                    flag = 1;
+                const uint64_t s_j = sz[j];
+                const uint64_t c_j = kd[j] == COOP_EVICTABLE ? ct[j] : 0;
+                sz[j] = t.q;
+                ct[j] = t.c;
+                xr[j] = t.r;
+                t.q += s_j;
+                t.c += c_j;
+                t.r += kd[j] >= COOP_PINNED ? 1u : 0u;
+                hi_or |= static_cast<uint32_t>(s_j >> 32);
+            }
+            if (hi_or >> kBigHiLog2) t.r += 1u << 16;
+            Sums wi = t;
+            wave_inclusive_sum(wi);
+            if (w < 4 && hm) wave_inclusive_sum(h);  // inclusive halo sums (waves 0..3)
+            if (lane == 63) {
+                sm.wsum[w] = wi;
+                if (w < 4) sm.hsum[w] = h;
+            }
+            __syncthreads();
+            // lanes 0..7: wavefront totals of the tile, 8..11: of the halo
+            Sums bsum{0, 0, 0};
+            if (lane < kWaves) bsum = sm.wsum[lane];
+            else if (lane < kWaves + 4 && hm) bsum = sm.hsum[lane - kWaves];
+            row_inclusive_sum(bsum);
+            const Sums tile_tot = readlane(bsum, kWaves - 1);
+            const Sums all_tot = readlane(bsum, kWaves + 3);
+            Sums carry = readlane(bsum, w ? w - 1 : 0);
+            if (w == 0) carry = Sums{0, 0, 0};
+            // halo wavefront w < 4: tile total + the earlier halo wavefronts
+            const Sums hcarry = readlane(bsum, kWaves - 1 + (w < 4 ? w : 0));
+            // thread exclusive = block carry + wavefront inclusive - own total
+            const Sums base{carry.q + wi.q - t.q, carry.c + wi.c - t.c, carry.r + wi.r - t.r};
+
+            packed = (tile_tot.r >> 16) == 0;
+            const bool use_halo = packed && hm && (all_tot.r >> 16) == 0;
+            end = use_halo ? kTile + hm : nt;
+            const Sums et = use_halo ? all_tot : tile_tot;
+            endrun = et.r & 0xffffu;
+            xend = packed ? (static_cast<uint64_t>(endrun) << kValBits) | et.q : et.q;
+            xcend = et.c;
+
+            // LDS: boundaries [0, end) by their owners, end and the sentinel by the last thread
+            const uint32_t i0 = tid * kItems;
+            const bool all_mine = i0 + kItems <= end;
+            if (packed) {
+                uint64_t xv[kItems], cv[kItems];
+#pragma unroll
+                for (uint32_t j = 0; j < kItems; ++j) {
+                    const uint64_t pq = base.q + sz[j];
+                    const uint32_t rr = base.r + xr[j];
+                    xv[j] = pq | (static_cast<uint64_t>(rr) << kValBits);
+                    cv[j] = base.c + ct[j];
+                }
+                if (all_mine) {
+#pragma unroll
+                    for (uint32_t j = 0; j < kItems; j += 2) {
+                        *reinterpret_cast<ulonglong2*>(&sm.x[i0 + j]) = ulonglong2{xv[j], xv[j + 1]};
+                        *reinterpret_cast<ulonglong2*>(&sm.xc[i0 + j]) = ulonglong2{cv[j], cv[j + 1]};
+                    }
                 } else {
-                    acc += s_j;
-                    cacc += c_j;
-                    big |= s_j >= kBigBlock ? 1u : 0u;
+#pragma unroll
+                    for (uint32_t j = 0; j < kItems; ++j) {
+                        if (i0 + j < end) {
+                            sm.x[i0 + j] = xv[j];
+                            sm.xc[i0 + j] = cv[j];
+                        }
+                    }
+                }
+                if (use_halo && tid < hm) {
+                    // halo boundary kTile + tid: carry + wavefront inclusive - own block
+                    const uint64_t pq = hcarry.q + h.q - hown.q;
+                    const uint32_t rr = hcarry.r + h.r - hown.r;
+                    sm.x[kTile + tid] = pq | (static_cast<uint64_t>(rr) << kValBits);
+                    sm.xc[kTile + tid] = hcarry.c + h.c - hown.c;
+                }
+            } else {
+#pragma unroll
+                for (uint32_t j = 0; j < kItems; ++j) {
+                    if (i0 + j < end) {
+                        sm.x[i0 + j] = base.q + sz[j];
+                        sm.xc[i0 + j] = base.c + ct[j];
+                        sm.run[i0 + j] = static_cast<uint16_t>(base.r + xr[j]);
+                    }
                 }
             }
-            Seg tot;
-            const Seg carry = block_exclusive_scan(Seg{flag, runs, acc, cacc}, sm, tot);
-#pragma unroll
-            for (uint32_t j = 0; j < kItems; ++j) {
-                const bool own = (lflags >> j) & 1u;
-                sz[j] = own ? sz[j] : carry.q + sz[j];
-                ct[j] = own ? ct[j] : carry.c + ct[j];
-                xr[j] += carry.cnt;
-            }
-            const uint64_t lastq = flag ? acc : carry.q + acc;  // prefix after the last block
-            const uint64_t lastc = flag ? cacc : carry.c + cacc;
-            const uint32_t lastr = carry.cnt + runs;
-            // with every block below 2^38 bytes, every prefix fits the key field
-            packed = !__syncthreads_or(big);
-#pragma unroll
-            for (uint32_t j = 0; j < kItems; ++j) {
-                const uint32_t s = sw(i0 + j);
-                sm.x[s] = packed ? (static_cast<uint64_t>(xr[j]) << kValBits) | sz[j] : sz[j];
-                sm.xc[s] = ct[j];
-                if (!packed) sm.aux[s] = static_cast<uint16_t>(xr[j]);
-            }
-            if (tid == kThreads - 1) {  // boundary after the tile
-                sm.x[sw(kTile)] = packed ? (static_cast<uint64_t>(lastr) << kValBits) | lastq
-                                         : lastq;
-                sm.xc[sw(kTile)] = lastc;
-                if (!packed) sm.aux[sw(kTile)] = static_cast<uint16_t>(lastr);
+            if (tid == kThreads - 1) {
+                sm.x[end] = xend;
+                sm.xc[end] = xcend;
+                sm.run[end] = static_cast<uint16_t>(endrun);
+                sm.x[end + 1] = kNone;  // sentinel end key
             }
             __syncthreads();
         }
         const uint64_t vmask = packed ? kValMask : kNone;
-        // the boundary after the tile: kept to restore it after a streaming pass
-        const uint64_t xb = sm.x[sw(kTile)];
-        const uint64_t xcb = sm.xc[sw(kTile)];
-        const uint32_t runb = packed ? static_cast<uint32_t>(xb >> kValBits) : sm.aux[sw(kTile)];
+        const bool open = t0 + end < s1;  // the region's last run may go on
 
-        // ---- 2. halo: the rest of the last run, up to kHaloCap blocks
-        uint32_t end = nt;
-        bool open = false;
-        {
-            const uint32_t runl = packed ? static_cast<uint32_t>(sm.x[sw(kTile - 1)] >> kValBits)
-                                         : sm.aux[sw(kTile - 1)];
-            const bool last_open = nt == kTile && runb == runl;  // block kTile-1 is not pinned
-            if (last_open && t0 + kTile < s1) {
-                const uint64_t pos = t0 + kTile;
-                const uint64_t left = s1 - pos;
-                const uint32_t m = static_cast<uint32_t>(left < kHaloCap ? left : kHaloCap);
-                bool cut;
-                const uint32_t fp = stage_halo(P, sm, pos, m, xb & vmask, xcb, runb, packed, cut);
-                end = kTile + fp;
-                // open: the run goes on past the staged blocks
-                open = cut || (fp == m && left > m);
+        // ---- 2./3. requests: wavefront task vw = request (vw / wpr), slice (vw % wpr)
+        const uint64_t tasks = K * wpr;
+        uint64_t S_next = 0;
+        if (w < tasks) S_next = P.req_size[q0 + y + (w / wpr) * P.slices];
+        for (uint64_t vw = w; vw < tasks; vw += kWaves) {
+            const uint64_t rl = vw / wpr;
+            const uint32_t sl = static_cast<uint32_t>(vw % wpr);
+            const uint64_t q = q0 + y + rl * P.slices;
+            const uint64_t S = S_next;
+            if (vw + kWaves < tasks) S_next = P.req_size[q0 + y + ((vw + kWaves) / wpr) * P.slices];
+            Cand best = cand_none();
+            uint64_t best_end = 0;
+            if (S != 0 && nt != 0) {
+                const uint64_t Sc = S < (1ull << kValBits) ? S : (1ull << kValBits);
+                const uint32_t lanes = 64u * wpr;
+                const uint32_t gl = sl * 64u + lane;
+                uint32_t e32 = 0;
+                if (packed) {
+                    const uint32_t total = nt + end;
+                    const uint32_t L = merge_steps(total, lanes);
+                    const uint32_t d = gl * L < total ? gl * L : total;
+                    merge_pass(sm, nt, end, d, L, Sc, best, e32);
+                } else {
+                    plain_pass(sm, nt, end, gl, lanes, S, best, e32);
+                }
+                best_end = tl + e32;
+                if (open && sl == 0) {
+                    const uint32_t cur = pending_start(sm, packed, nt, xend, endrun, S, Sc);
+                    if (cur < nt)
+                        stream_pass(P, sm, cur, nt, t0 + end, s0, s1, xend & vmask, xcend, vmask, S,
+                                    best, best_end);
+                }
+            }
+            const Cand m = wave_argmin(best);
+            Key k = key_none();
+            if (m.start != kNone32) {
+                const uint64_t won = __ballot(best.start == m.start);
+                const uint64_t e = readlane64(best_end, static_cast<uint32_t>(__builtin_ctzll(won)));
+                k = Key{m.cost, m.excess + S, tl + m.start, e};
+            }
+            if (lane == 0) {
+                if (wpr == 1) write_result(P, q, g, direct, tau == p, k, S);
+                else sm.slot[vw] = k;
             }
         }
-        const uint32_t endrun = runb;  // the run reaching the end of the staged region
-        write_sentinels(sm, end);
-        __syncthreads();
-
-        // ---- 3. the snapshot's requests of this slice
-        for (uint64_t r = y; r < R; r += P.slices) {
-            const uint64_t q = q0 + r;
-            const uint64_t S = P.req_size[q];
-            Key best = key_none();
-            uint32_t pend = nt;
-            uint32_t i0 = tid * kItems;  // opaque again, see above
-            asm volatile("" : "+v"(i0));
-            if (S != 0) {
-                if (packed) {
-                    // merge path: A = targets X[i] + S' of starts [0, nt), B = end keys
-                    // X[1..end].  S' = min(S, field maximum): a target that carries
-                    // into the next run id lies above every end of its own run, which
-                    // is exactly the infeasible case; the scoring below re-checks.
-                    const uint64_t Sc = S < kValMask ? S : kValMask;
-                    const uint32_t nA = nt, nB = end, total = nA + nB;
-                    const uint32_t L = (total + kThreads - 1) / kThreads;
-                    const uint32_t d = tid * L < total ? tid * L : total;
-                    const uint32_t dEnd = d + L < total ? d + L : total;
-                    uint32_t lo = d > nB ? d - nB : 0, hi = d < nA ? d : nA;
-                    while (lo < hi) {
-                        const uint32_t mid = (lo + hi) >> 1;
-                        // start `mid` comes before end d-1-mid iff its target <= X[d-mid]
-                        const bool before = sm.x[sw(mid)] + Sc <= sm.x[sw(d - mid)];
-                        lo = before ? mid + 1 : lo;
-                        hi = before ? hi : mid;
-                    }
-                    // Past the ends the sentinels compare above every target, so all
-                    // remaining starts take "no end in the region" (e = end).  Starts
-                    // past nA are phantoms: their entries are never read.
-                    uint32_t a = lo, bq = d - lo;
-                    uint64_t ta = sm.x[sw(a)] + Sc;
-                    uint64_t kb = sm.x[sw(bq + 1)];
-                    for (uint32_t st = d; st < dEnd; ++st) {
-                        const bool takeA = ta <= kb;
-                        uint16_t* dst = takeA ? &sm.aux[sw(a)] : &sm.sink[tid];
-                        *dst = static_cast<uint16_t>(bq);
-                        a += takeA ? 1u : 0u;
-                        bq += takeA ? 0u : 1u;
-                        const uint64_t val = sm.x[sw(takeA ? a : bq + 1)];
-                        ta = takeA ? val + Sc : ta;
-                        kb = takeA ? kb : val;
-                    }
-                    __syncthreads();
-#pragma unroll
-                    for (uint32_t j = 0; j < kItems; ++j) {
-                        const uint32_t i = i0 + j;
-                        if (i >= nt || ((pinmask >> j) & 1u)) continue;
-                        const uint32_t e = sm.aux[sw(i)];
-                        const uint64_t xi = sm.x[sw(i)];
-                        const uint32_t run = static_cast<uint32_t>(xi >> kValBits);
-                        if (e < end) {
-                            const uint64_t v1 = sm.x[sw(e + 1)];
-                            const uint64_t bytes = (v1 & kValMask) - (xi & kValMask);
-                            if (static_cast<uint32_t>(v1 >> kValBits) == run && bytes >= S) {
-                                const Key cand{sm.xc[sw(e + 1)] - sm.xc[sw(i)], bytes, tl + i,
-                                               tl + e + 1};
-                                if (key_less(cand, best)) best = cand;
-                            }
-                        } else if (open && run == endrun && i < pend) {
-                            pend = i;  // the window leaves the staged region
-                        }
-                    }
-                } else {
-                    // plain prefixes: find the run end, then the shortest end, by bisection
-#pragma unroll 1
-                    for (uint32_t j = 0; j < kItems; ++j) {
-                        const uint32_t i = i0 + j;
-                        if (i >= nt || ((pinmask >> j) & 1u)) continue;
-                        const uint32_t run = sm.aux[sw(i)];
-                        const uint64_t base = sm.x[sw(i)];
-                        uint32_t lo = i, hi = end;  // first k in [i, end) that closes the run
-                        while (lo < hi) {
-                            const uint32_t mid = (lo + hi) >> 1;
-                            if (sm.aux[sw(mid + 1)] != run) hi = mid; else lo = mid + 1;
-                        }
-                        const uint32_t rend = lo;  // pinned block ending the run, or end
-                        lo = i;
-                        hi = rend;
-                        while (lo < hi) {
-                            const uint32_t mid = (lo + hi) >> 1;
-                            if (sm.x[sw(mid + 1)] - base >= S) hi = mid; else lo = mid + 1;
-                        }
-                        if (lo < rend) {
-                            const Key cand{sm.xc[sw(lo + 1)] - sm.xc[sw(i)], sm.x[sw(lo + 1)] - base,
-                                           tl + i, tl + lo + 1};
-                            if (key_less(cand, best)) best = cand;
-                        } else if (rend == end && open && i < pend) {
-                            pend = i;
-                        }
-                    }
+        if (wpr > 1) {
+            __syncthreads();
+            if (tid < K) {
+                const uint64_t q = q0 + y + static_cast<uint64_t>(tid) * P.slices;
+                Key k = sm.slot[tid * wpr];
+                for (uint32_t u = 1; u < wpr; ++u) {
+                    const Key o = sm.slot[tid * wpr + u];
+                    if (key_less(o, k)) k = o;
                 }
-            }
-            // ---- 4. starts whose windows run past the staged region
-            const uint32_t cur = open ? block_min_u32(pend, sm) : nt;
-            if (cur < nt) {
-                stream_pass(P, sm, cur, nt, end, packed, t0, s0, s1, S, best);
-                // the streaming chunks overwrote the halo: keep only the tile
-                __syncthreads();
-                if (tid == 0) {
-                    sm.x[sw(kTile)] = xb;
-                    sm.xc[sw(kTile)] = xcb;
-                    if (!packed) sm.aux[sw(kTile)] = static_cast<uint16_t>(runb);
-                }
-                end = kTile;  // later requests stream from the tile end
-                write_sentinels(sm, end);
-                __syncthreads();
-            }
-            best = block_min_key(best, sm);
-            if (tid == 0) {
-                if (direct) {
-                    P.out[q] = to_window(best, S);
-                } else {
-                    Key* slot = P.part + q * P.pc + g;
-                    if (tau != p) {
-                        const Key prev = *slot;
-                        if (key_less(prev, best)) best = prev;
-                    }
-                    *slot = best;
-                }
+                write_result(P, q, g, direct, tau == p, k, P.req_size[q]);
             }
         }
         __syncthreads();  // LDS reused by the next tile
@@ -729,6 +778,7 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
     // ---- combine the partial keys of the snapshot's workgroups
     __threadfence();
     __syncthreads();
+    __shared__ uint32_t last_flag;
     if (tid == 0) {
         uint32_t last = 1;
         if (G > 1 || (P.slices > 1 && R > 1)) {
@@ -745,10 +795,10 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
             const uint64_t arrivals = G * (R < P.slices ? R : P.slices);
             last = (want & ((1ull << kEpochShift) - 1)) == arrivals;
         }
-        sm.flag = last;
+        last_flag = last;
     }
     __syncthreads();
-    if (!sm.flag) return;
+    if (!last_flag) return;
     __threadfence();
     for (uint64_t r = tid; r < R; r += kThreads) {
         const uint64_t q = q0 + r;
