@@ -100,8 +100,8 @@ static_assert(kStage < (1u << (kValBits - 38)), "staged prefixes must fit the ke
 static_assert(kStage < (1u << 16), "pinned counts fit 16 bits");
 constexpr uint64_t kNone = ~0ull;
 constexpr uint32_t kNone32 = ~0u;
-constexpr uint32_t kMaxWpr = 4;                  // wavefronts that may share one request
-constexpr uint64_t kPartialBudget = 1ull << 22;  // partial keys (32 B each)
+constexpr uint32_t kMaxWpr = 8;                  // wavefronts that may share one request
+constexpr uint64_t kPartialBudget = 1ull << 23;  // partial keys (32 B each) before chunks grow
 constexpr uint32_t kEpochShift = 24;             // counter = epoch << 24 | tickets
 constexpr uint64_t kEpochMask = (1ull << 40) - 1;
 
@@ -236,17 +236,18 @@ struct Params {
     const uint64_t* req_size;
     const uint64_t* req_off;
     coop_window_t* out;
-    Key* part;             // [num_requests][pc]
-    uint64_t* counters;    // [num_segments]
+    Key* part;             // [num_requests][pc] partial keys
+    uint64_t* counters;    // [slices][num_segments] arrival tickets
     uint64_t num_blocks;
     uint64_t num_segments;
     uint64_t num_requests;
-    uint64_t num_virtual;  // floor(num_blocks / kTile) + num_segments
-    uint64_t pc;
+    uint64_t num_virtual;  // tile ids per slice: floor(num_blocks / kTile) + num_segments
+    uint64_t units;        // work units: slices * num_virtual
+    uint64_t chunk;        // consecutive units per workgroup
+    uint64_t pc;           // partial slots per request
     uint64_t epoch;
-    uint32_t rot_bits;     // the grid is 2^rot_bits workgroups (x) by slices (y)
-    uint32_t slices;       // request slices: workgroup y takes requests y, y + slices, ...
-    double inv_slope;      // guess of b per virtual id, for the snapshot lookup
+    uint64_t slices;       // request slices: slice y takes requests y, y + slices, ...
+    double inv_slope;      // guess of b per tile id, for the first snapshot lookup
 };
 
 struct Smem {
@@ -256,64 +257,142 @@ struct Smem {
     Sums wsum[kWaves];  // per-wavefront totals of the tile
     Sums hsum[4];       // per-wavefront totals of the halo
     Key slot[kWaves];   // answers of wavefronts that share a request
+    uint64_t slot_s[kWaves];
 };
 
-struct Snapshot {
-    uint64_t b, s0, s1, q0, q1, first;  // first = f(b), the virtual id of its first tile
+__device__ __forceinline__ uint64_t first_id(uint64_t b, uint64_t seg_b) {
+    return (seg_b >> kTileLog2) + b;
+}
+
+// Position in the snapshot list: the offsets of snapshot b and of the two
+// after it.  The third pair is loaded ahead, so that stepping to the next
+// snapshot needs no wait.
+struct Cursor {
+    uint64_t y, b;
+    uint64_t sb, sb1, sb2;  // seg[b], seg[b + 1], seg[min(b + 2, B)]
+    uint64_t rb, rb1, rb2;  // req_off likewise
 };
 
-// The snapshot b holding virtual id v: the largest b in [0, B) with
-// f(b) = floor(seg[b] / kTile) + b <= v.  A guess from the average snapshot
-// length is tried first, with its request offsets loaded alongside, so that
-// uniform batches settle in one round of loads.  Offsets are clamped to the
-// array lengths: malformed offsets give wrong answers, never an
-// out-of-bounds access.
-__device__ Snapshot locate_snapshot(const Params& P, uint64_t v) {
+// Places the cursor on the snapshot holding tile id v: the largest b in
+// [0, B) with f(b) = floor(seg[b] / kTile) + b <= v.  A guess from the
+// average snapshot length is tried first, so uniform batches settle in one
+// round of loads; otherwise a bisection.
+__device__ void cursor_locate(const Params& P, uint64_t v, Cursor& c) {
     const uint64_t B = P.num_segments;
     uint64_t g = static_cast<uint64_t>(static_cast<double>(v) * P.inv_slope);
     if (g >= B) g = B - 1;
     uint64_t sg = P.seg[g], sg1 = P.seg[g + 1];
-    uint64_t rg = P.req_off[g], rg1 = P.req_off[g + 1];
-    auto f = [&](uint64_t bb, uint64_t seg_b) { return (seg_b >> kTileLog2) + bb; };
-    const bool hit = f(g, sg) <= v && (g + 1 == B || f(g + 1, sg1) > v);
+    const bool hit = first_id(g, sg) <= v && (g + 1 == B || first_id(g + 1, sg1) > v);
     uint64_t b = g;
     if (!hit) {
         uint64_t lo = 0, hi = B;  // f(lo) <= v < f(hi) (f(B) taken as infinite)
-        if (f(g, sg) <= v) lo = g; else hi = g;
+        if (first_id(g, sg) <= v) lo = g; else hi = g;
         while (hi - lo > 1) {
             const uint64_t mid = lo + (hi - lo) / 2;
-            if (f(mid, P.seg[mid]) <= v) lo = mid; else hi = mid;
+            if (first_id(mid, P.seg[mid]) <= v) lo = mid; else hi = mid;
         }
         b = lo;
         sg = P.seg[b];
         sg1 = P.seg[b + 1];
-        rg = P.req_off[b];
-        rg1 = P.req_off[b + 1];
     }
-    Snapshot sn;
-    sn.b = b;
-    sn.first = f(b, sg);
-    sn.s1 = sg1 < P.num_blocks ? sg1 : P.num_blocks;
-    sn.s0 = sg < sn.s1 ? sg : sn.s1;
-    sn.q1 = rg1 < P.num_requests ? rg1 : P.num_requests;
-    sn.q0 = rg < sn.q1 ? rg : sn.q1;
-    return sn;
+    const uint64_t b2 = b + 2 < B ? b + 2 : B;
+    c.b = b;
+    c.sb = sg;
+    c.sb1 = sg1;
+    c.sb2 = P.seg[b2];
+    c.rb = P.req_off[b];
+    c.rb1 = P.req_off[b + 1];
+    c.rb2 = P.req_off[b2];
 }
 
-// Loads the kItems blocks [t0 + tid*kItems, +kItems) of a tile of nt blocks.
-// Blocks past nt read as empty free blocks.  All loads are independent.
-__device__ __forceinline__ void load_items(const Params& P, uint64_t t0, uint32_t nt,
+// Moves the cursor forward to the snapshot holding tile id v (v not below
+// the cursor's first id).
+__device__ __forceinline__ void cursor_advance(const Params& P, uint64_t v, Cursor& c) {
+    const uint64_t B = P.num_segments;
+    while (c.b + 1 < B && v >= first_id(c.b + 1, c.sb1)) {
+        ++c.b;
+        c.sb = c.sb1;
+        c.sb1 = c.sb2;
+        c.rb = c.rb1;
+        c.rb1 = c.rb2;
+        const uint64_t b2 = c.b + 2 < B ? c.b + 2 : B;
+        c.sb2 = P.seg[b2];
+        c.rb2 = P.req_off[b2];
+    }
+}
+
+// One tile to search: tile p of snapshot b, for the requests of slice y.
+// The workgroups whose chunks hold the tiles of (b, y) are G consecutive
+// ones; this one is the g-th.  `first` / `last`: the first / last tile of
+// (b, y) in this workgroup's chunk.  Offsets are clamped to the array
+// lengths: malformed offsets give wrong answers, never an out-of-bounds
+// access.
+struct Job {
+    uint64_t u, y, b, s0, s1, q0, R, K, tiles, p, g, G;
+    bool first, last, direct;
+};
+
+// The first unit in [u, u_end) holding a tile to search (a tile of a
+// snapshot with requests in the unit's slice); false if there is none.
+__device__ bool next_job(const Params& P, Cursor& c, bool& have_cursor, uint64_t u,
+                         uint64_t u_begin, uint64_t u_end, Job& job) {
+    for (; u < u_end; ++u) {
+        const uint64_t y = u / P.num_virtual, v = u - y * P.num_virtual;
+        if (!have_cursor || y != c.y) {
+            cursor_locate(P, v, c);
+            c.y = y;
+            have_cursor = true;
+        } else {
+            cursor_advance(P, v, c);
+        }
+        const uint64_t s1 = c.sb1 < P.num_blocks ? c.sb1 : P.num_blocks;
+        const uint64_t s0 = c.sb < s1 ? c.sb : s1;
+        const uint64_t q1 = c.rb1 < P.num_requests ? c.rb1 : P.num_requests;
+        const uint64_t q0 = c.rb < q1 ? c.rb : q1;
+        const uint64_t R = q1 - q0, nb = s1 - s0;
+        const uint64_t tiles = nb ? (nb + kTile - 1) >> kTileLog2 : 1;
+        const uint64_t f = first_id(c.b, c.sb);
+        const uint64_t p = v - f;  // wraps (and is skipped) if the offsets are malformed
+        if (p >= tiles || y >= R) continue;
+        const uint64_t ub = y * P.num_virtual + f;  // unit of tile 0 of (b, y)
+        const uint64_t lo = ub > u_begin ? ub : u_begin;
+        const uint64_t hi = ub + tiles < u_end ? ub + tiles : u_end;
+        job.u = u;
+        job.y = y;
+        job.b = c.b;
+        job.s0 = s0;
+        job.s1 = s1;
+        job.q0 = q0;
+        job.R = R;
+        job.K = (R - y + P.slices - 1) / P.slices;
+        job.tiles = tiles;
+        job.p = p;
+        const uint64_t i_lo = ub / P.chunk, i_hi = (ub + tiles - 1) / P.chunk;
+        job.G = i_hi - i_lo + 1;
+        if (job.G > P.pc) job.G = P.pc;  // only with malformed offsets
+        job.g = blockIdx.x - i_lo;
+        job.first = u == lo;
+        job.last = u + 1 == hi;
+        job.direct = job.G == 1;
+        return true;
+    }
+    return false;
+}
+
+// Loads the kItems blocks [t0 + tid*kItems, +kItems) of a tile of nt blocks;
+// the kinds stay packed, one byte per block.  Blocks past nt read as empty
+// free blocks.  All loads are independent.
+__device__ __forceinline__ void load_items(const Params& P, uint64_t t0, uint32_t nt, uint32_t tid,
                                            uint64_t (&sz)[kItems], uint64_t (&ct)[kItems],
-                                           uint8_t (&kd)[kItems]) {
-    uint32_t i0 = threadIdx.x * kItems;
-    asm volatile("" : "+v"(i0));
+                                           uint2& kd) {
+    const uint32_t i0 = tid * kItems;
     const bool aligned = ((reinterpret_cast<uintptr_t>(P.size) | reinterpret_cast<uintptr_t>(P.cost)) &
                           15u) == 0 &&
                          (reinterpret_cast<uintptr_t>(P.kind) & 7u) == 0;
     if (nt == kTile && (t0 & 7u) == 0 && aligned) {
         const ulonglong2* ps = reinterpret_cast<const ulonglong2*>(P.size + t0 + i0);
         const ulonglong2* pc = reinterpret_cast<const ulonglong2*>(P.cost + t0 + i0);
-        const uint2 k2 = *reinterpret_cast<const uint2*>(P.kind + t0 + i0);
+        kd = *reinterpret_cast<const uint2*>(P.kind + t0 + i0);
 #pragma unroll
         for (uint32_t j = 0; j < kItems / 2; ++j) {
             const ulonglong2 a = ps[j], b = pc[j];
@@ -322,20 +401,62 @@ __device__ __forceinline__ void load_items(const Params& P, uint64_t t0, uint32_
             ct[2 * j] = b.x;
             ct[2 * j + 1] = b.y;
         }
-#pragma unroll
-        for (uint32_t j = 0; j < 4; ++j) {
-            kd[j] = static_cast<uint8_t>(k2.x >> (8 * j));
-            kd[j + 4] = static_cast<uint8_t>(k2.y >> (8 * j));
-        }
     } else {
+        kd = uint2{0u, 0u};
 #pragma unroll
         for (uint32_t j = 0; j < kItems; ++j) {
             const uint32_t i = i0 + j;
             const bool in = i < nt;
             sz[j] = in ? P.size[t0 + i] : 0;
             ct[j] = in ? P.cost[t0 + i] : 0;
-            kd[j] = in ? P.kind[t0 + i] : static_cast<uint8_t>(COOP_FREE);
+            const uint32_t k = in ? P.kind[t0 + i] : static_cast<uint32_t>(COOP_FREE);
+            if (j < 4) kd.x |= k << (8 * j);
+            else kd.y |= k << (8 * (j - 4));
         }
+    }
+}
+
+// A tile's blocks as loaded, one thread's share: kItems blocks of the tile
+// and one halo block for the first kHaloCap threads.
+struct TileRegs {
+    uint64_t sz[kItems], ct[kItems];
+    uint2 kd;  // kind of block j in byte j
+    uint64_t hq, hc;
+    uint32_t hk;
+};
+
+__device__ __forceinline__ uint32_t kind_of(const uint2& kd, uint32_t j) {
+    return ((j < 4 ? kd.x : kd.y) >> (8 * (j & 3))) & 0xffu;
+}
+
+struct TileGeom {
+    uint64_t t0;  // global index of the tile start
+    uint32_t nt;  // blocks in the tile
+    uint32_t hm;  // halo blocks after a full tile
+};
+
+__device__ __forceinline__ TileGeom tile_geom(const Job& job) {
+    TileGeom t;
+    t.t0 = job.s0 + (job.p << kTileLog2);
+    const uint64_t left = job.s1 - t.t0;
+    t.nt = static_cast<uint32_t>(left < kTile ? left : kTile);
+    const uint64_t after = left - t.nt;
+    t.hm = t.nt == kTile ? static_cast<uint32_t>(after < kHaloCap ? after : kHaloCap) : 0;
+    return t;
+}
+
+// Issues every load of a tile; nothing waits for them here.
+__device__ __forceinline__ void issue_loads(const Params& P, const TileGeom& t, uint32_t tid,
+                                            TileRegs& r) {
+    load_items(P, t.t0, t.nt, tid, r.sz, r.ct, r.kd);
+    r.hq = 0;
+    r.hc = 0;
+    r.hk = COOP_FREE;
+    if (tid < t.hm) {
+        const uint64_t gp = t.t0 + kTile + tid;
+        r.hk = P.kind[gp];
+        r.hq = P.size[gp];
+        r.hc = P.cost[gp];
     }
 }
 
@@ -476,10 +597,9 @@ __device__ __forceinline__ uint32_t pending_start(const Smem& sm, bool packed, u
 // chunk resolves a prefix of the pending starts, 64 at a time, since their
 // shortest ends are monotone.  Candidates fold into best / best_end (end
 // snapshot-local).
-__device__ void stream_pass(const Params& P, const Smem& sm, uint32_t cur, uint32_t nA, uint64_t pos,
-                            uint64_t s0, uint64_t s1, uint64_t cq, uint64_t cc, uint64_t vmask,
-                            uint64_t S, Cand& best, uint64_t& best_end) {
-    const uint32_t lane = threadIdx.x & 63u;
+__device__ void stream_pass(const Params& P, const Smem& sm, uint32_t lane, uint32_t cur, uint32_t nA,
+                            uint64_t pos, uint64_t s0, uint64_t s1, uint64_t cq, uint64_t cc,
+                            uint64_t vmask, uint64_t S, Cand& best, uint64_t& best_end) {
     while (cur < nA && pos < s1) {
         const uint64_t left = s1 - pos;
         const uint32_t m = left < 64 ? static_cast<uint32_t>(left) : 64u;
@@ -536,279 +656,324 @@ __device__ void stream_pass(const Params& P, const Smem& sm, uint32_t cur, uint3
     }
 }
 
-__device__ __forceinline__ void write_result(const Params& P, uint64_t q, uint64_t slot_index,
-                                             bool direct, bool first_tile, Key k, uint64_t S) {
-    if (direct) {
-        P.out[q] = to_window(k, S);
-    } else {
-        Key* slot = P.part + q * P.pc + slot_index;
-        if (!first_tile) {
-            const Key prev = *slot;
-            if (key_less(prev, k)) k = prev;
+// What staging left in LDS.
+struct TileState {
+    bool packed;     // keys R << 51 | P; otherwise plain P with R in sm.run
+    uint32_t end;    // staged boundaries [0, end]
+    uint32_t endrun; // R at the region end
+    uint64_t xend;   // X at the region end
+    uint64_t xcend;  // C at the region end
+};
+
+// Prefix sums of a tile (and its halo) into LDS: X[k], C[k] for k < end by
+// their owners, the region end and the sentinel X[end + 1] = all-ones by the
+// last thread.  Two barriers; the second ends the staging.
+__device__ __forceinline__ TileState stage_tile(Smem& sm, uint32_t nt, uint32_t hm, uint32_t tid,
+                                                TileRegs& r) {
+    const uint32_t lane = tid & 63u;
+    const uint32_t w = uniform(tid >> 6);
+    Sums h{0, 0, 0};
+    if (tid < hm) {
+        h.q = r.hq;
+        h.c = r.hk == COOP_EVICTABLE ? r.hc : 0;
+        h.r = (r.hk >= COOP_PINNED ? 1u : 0u) + ((r.hq >> 32) >> kBigHiLog2 ? 1u << 16 : 0u);
+    }
+    const Sums hown = h;
+    // thread-local exclusive sums
+    Sums t{0, 0, 0};
+    uint32_t xr[kItems];
+    uint32_t hi_or = 0;
+#pragma unroll
+    for (uint32_t j = 0; j < kItems; ++j) {
+        const uint64_t s_j = r.sz[j];
+        const uint32_t k_j = kind_of(r.kd, j);
+        const uint64_t c_j = k_j == COOP_EVICTABLE ? r.ct[j] : 0;
+        r.sz[j] = t.q;
+        r.ct[j] = t.c;
+        xr[j] = t.r;
+        t.q += s_j;
+        t.c += c_j;
+        t.r += k_j >= COOP_PINNED ? 1u : 0u;
+        hi_or |= static_cast<uint32_t>(s_j >> 32);
+    }
+    if (hi_or >> kBigHiLog2) t.r += 1u << 16;
+    Sums wi = t;
+    wave_inclusive_sum(wi);
+    if (w < 4 && hm) wave_inclusive_sum(h);  // inclusive halo sums (wavefronts 0..3)
+    if (lane == 63) {
+        sm.wsum[w] = wi;
+        if (w < 4) sm.hsum[w] = h;
+    }
+    __syncthreads();
+    // lanes 0..7: wavefront totals of the tile, 8..11: of the halo
+    Sums bsum{0, 0, 0};
+    if (lane < kWaves) bsum = sm.wsum[lane];
+    else if (lane < kWaves + 4 && hm) bsum = sm.hsum[lane - kWaves];
+    row_inclusive_sum(bsum);
+    const Sums tile_tot = readlane(bsum, kWaves - 1);
+    const Sums all_tot = readlane(bsum, kWaves + 3);
+    Sums carry = readlane(bsum, w ? w - 1 : 0);
+    if (w == 0) carry = Sums{0, 0, 0};
+    // halo wavefront w < 4: tile total + the earlier halo wavefronts
+    const Sums hcarry = readlane(bsum, kWaves - 1 + (w < 4 ? w : 0));
+    // thread exclusive = block carry + wavefront inclusive - own total
+    const Sums base{carry.q + wi.q - t.q, carry.c + wi.c - t.c, carry.r + wi.r - t.r};
+
+    TileState ts;
+    ts.packed = (tile_tot.r >> 16) == 0;
+    const bool use_halo = ts.packed && hm && (all_tot.r >> 16) == 0;
+    ts.end = use_halo ? kTile + hm : nt;
+    const Sums et = use_halo ? all_tot : tile_tot;
+    ts.endrun = et.r & 0xffffu;
+    ts.xend = ts.packed ? (static_cast<uint64_t>(ts.endrun) << kValBits) | et.q : et.q;
+    ts.xcend = et.c;
+
+    const uint32_t i0 = tid * kItems;
+    if (ts.packed) {
+        uint64_t xv[kItems], cv[kItems];
+#pragma unroll
+        for (uint32_t j = 0; j < kItems; ++j) {
+            const uint64_t pq = base.q + r.sz[j];
+            const uint32_t rr = base.r + xr[j];
+            xv[j] = pq | (static_cast<uint64_t>(rr) << kValBits);
+            cv[j] = base.c + r.ct[j];
         }
-        *slot = k;
+        if (i0 + kItems <= ts.end) {
+#pragma unroll
+            for (uint32_t j = 0; j < kItems; j += 2) {
+                *reinterpret_cast<ulonglong2*>(&sm.x[i0 + j]) = ulonglong2{xv[j], xv[j + 1]};
+                *reinterpret_cast<ulonglong2*>(&sm.xc[i0 + j]) = ulonglong2{cv[j], cv[j + 1]};
+            }
+        } else {
+#pragma unroll
+            for (uint32_t j = 0; j < kItems; ++j) {
+                if (i0 + j < ts.end) {
+                    sm.x[i0 + j] = xv[j];
+                    sm.xc[i0 + j] = cv[j];
+                }
+            }
+        }
+        if (use_halo && tid < hm) {
+            // halo boundary kTile + tid: carry + wavefront inclusive - own block
+            const uint64_t pq = hcarry.q + h.q - hown.q;
+            const uint32_t rr = hcarry.r + h.r - hown.r;
+            sm.x[kTile + tid] = pq | (static_cast<uint64_t>(rr) << kValBits);
+            sm.xc[kTile + tid] = hcarry.c + h.c - hown.c;
+        }
+    } else {
+#pragma unroll
+        for (uint32_t j = 0; j < kItems; ++j) {
+            if (i0 + j < ts.end) {
+                sm.x[i0 + j] = base.q + r.sz[j];
+                sm.xc[i0 + j] = base.c + r.ct[j];
+                sm.run[i0 + j] = static_cast<uint16_t>(base.r + xr[j]);
+            }
+        }
+    }
+    if (tid == kThreads - 1) {
+        sm.x[ts.end] = ts.xend;
+        sm.xc[ts.end] = ts.xcend;
+        sm.run[ts.end] = static_cast<uint16_t>(ts.endrun);
+        sm.x[ts.end + 1] = kNone;  // sentinel end key
+    }
+    __syncthreads();
+    return ts;
+}
+
+// A Key read with a vector load: the scalar cache does not see this
+// workgroup's earlier stores to the same slot.
+__device__ __forceinline__ Key load_key_vector(const Key* p) {
+    uint32_t z = 0;
+    asm volatile("" : "+v"(z));
+    return p[z];
+}
+
+__device__ __forceinline__ Key readlane_key(const Key& k, uint32_t lane) {
+    return Key{readlane64(k.cost, lane), readlane64(k.bytes, lane), readlane64(k.start, lane),
+               readlane64(k.end, lane)};
+}
+
+// Folds this tile's answer for request q into the workgroup's running key
+// and stores it: the final result once the workgroup has covered the whole
+// snapshot alone, else its partial slot.
+__device__ __forceinline__ void store_answer(const Params& P, const Job& job, uint64_t q, Key k,
+                                             const Key& prev, uint64_t S) {
+    if (!job.first && key_less(prev, k)) k = prev;
+    if (job.last && job.direct) P.out[q] = to_window(k, S);
+    else P.part[q * P.pc + job.g] = k;
+}
+
+// The shortest-window search of one tile for every request of the job's
+// slice (see the file comment, steps 2 and 3).
+__device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const Job& job,
+                                              const TileGeom& tg, const TileState& ts,
+                                              uint32_t wpr, uint32_t tid, const Key& acc) {
+    const uint32_t lane = tid & 63u;
+    const uint32_t w = uniform(tid >> 6);
+    const uint64_t tl = tg.t0 - job.s0;
+    const uint32_t nt = tg.nt, end = ts.end;
+    const uint64_t vmask = ts.packed ? kValMask : kNone;
+    const bool open = tg.t0 + end < job.s1;  // the region's last run may go on
+    const uint64_t tasks = job.K * wpr;
+    for (uint64_t vw = w; vw < tasks; vw += kWaves) {
+        const uint64_t rl = vw / wpr;
+        const uint32_t sl = static_cast<uint32_t>(vw % wpr);
+        const uint64_t q = job.q0 + job.y + rl * P.slices;
+        const uint64_t S = P.req_size[q];
+        Cand best = cand_none();
+        uint64_t best_end = 0;
+        if (S != 0 && nt != 0) {
+            const uint64_t Sc = S < (1ull << kValBits) ? S : (1ull << kValBits);
+            const uint32_t lanes = 64u * wpr;
+            const uint32_t gl = sl * 64u + lane;
+            uint32_t e32 = 0;
+            if (ts.packed) {
+                const uint32_t total = nt + end;
+                const uint32_t L = merge_steps(total, lanes);
+                const uint32_t d = gl * L < total ? gl * L : total;
+                merge_pass(sm, nt, end, d, L, Sc, best, e32);
+            } else {
+                plain_pass(sm, nt, end, gl, lanes, S, best, e32);
+            }
+            best_end = tl + e32;
+            if (open && sl == 0) {
+                const uint32_t cur = pending_start(sm, ts.packed, nt, ts.xend, ts.endrun, S, Sc);
+                if (cur < nt)
+                    stream_pass(P, sm, lane, cur, nt, tg.t0 + end, job.s0, job.s1, ts.xend & vmask,
+                                ts.xcend, vmask, S, best, best_end);
+            }
+        }
+        const Cand m = wave_argmin(best);
+        Key k = key_none();
+        if (m.start != kNone32) {
+            const uint64_t won = __ballot(best.start == m.start);
+            const uint64_t e = readlane64(best_end, static_cast<uint32_t>(__builtin_ctzll(won)));
+            k = Key{m.cost, m.excess + S, tl + m.start, e};
+        }
+        if (wpr == 1) {
+            // this wavefront's request number rl / kWaves sits in lane rl / kWaves of acc
+            const uint64_t kk = rl / kWaves;
+            Key prev = key_none();
+            if (!job.first)
+                prev = kk < 64 ? readlane_key(acc, static_cast<uint32_t>(kk))
+                               : load_key_vector(P.part + q * P.pc + job.g);
+            if (lane == 0) store_answer(P, job, q, k, prev, S);
+        } else if (lane == 0) {
+            sm.slot[vw] = k;
+            sm.slot_s[vw] = S;
+        }
+    }
+    if (wpr > 1) {
+        __syncthreads();
+        if (tid < job.K) {
+            Key k = sm.slot[tid * wpr];
+            for (uint32_t u = 1; u < wpr; ++u) {
+                const Key o = sm.slot[tid * wpr + u];
+                if (key_less(o, k)) k = o;
+            }
+            store_answer(P, job, job.q0 + job.y + tid * P.slices, k, acc, sm.slot_s[tid * wpr]);
+        }
+    }
+}
+
+// After the last tile of (b, y) in this workgroup, when other workgroups
+// hold tiles of it too: a ticket on the (b, y) counter; the last of the G
+// arrivals reduces the G partial keys of every request of the slice.
+__device__ void combine_partials(const Params& P, const Job& job, uint32_t tid, uint32_t& last_flag) {
+    __threadfence();
+    __syncthreads();
+    if (tid == 0) {
+        uint64_t* ctr = P.counters + job.y * P.num_segments + job.b;
+        uint64_t old = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        uint64_t want;
+        do {
+            want = (old >> kEpochShift) == P.epoch ? old + 1 : (P.epoch << kEpochShift) | 1ull;
+        } while (!__hip_atomic_compare_exchange_strong(ctr, &old, want, __ATOMIC_ACQ_REL,
+                                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+        last_flag = (want & ((1ull << kEpochShift) - 1)) == job.G;
+    }
+    __syncthreads();
+    if (!last_flag) return;
+    __threadfence();
+    // tpr threads per request (a power of two within a wavefront), each
+    // taking every tpr-th slot; then a shuffle reduction inside the group
+    uint32_t tpr = 64;
+    while (tpr > 1 && static_cast<uint64_t>(tpr) * job.K > kThreads) tpr >>= 1;
+    const uint32_t groups = kThreads / tpr, sub = tid % tpr;
+    for (uint64_t k0 = 0; k0 < job.K; k0 += groups) {
+        const uint64_t k = k0 + tid / tpr;
+        const bool act = k < job.K;
+        const uint64_t q = job.q0 + job.y + (act ? k : 0) * P.slices;
+        Key best = key_none();
+        if (act) {
+            for (uint64_t gg = sub; gg < job.G; gg += tpr) {
+                const Key o = P.part[q * P.pc + gg];
+                if (key_less(o, best)) best = o;
+            }
+        }
+        for (uint32_t m = tpr >> 1; m >= 1; m >>= 1) {
+            Key o;
+            o.cost = __shfl_xor(best.cost, static_cast<int>(m), 64);
+            o.bytes = __shfl_xor(best.bytes, static_cast<int>(m), 64);
+            o.start = __shfl_xor(best.start, static_cast<int>(m), 64);
+            o.end = __shfl_xor(best.end, static_cast<int>(m), 64);
+            if (key_less(o, best)) best = o;
+        }
+        if (act && sub == 0) P.out[q] = to_window(best, P.req_size[q]);
     }
 }
 
 __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params P) {
     __shared__ Smem sm;
-    const uint32_t tid = threadIdx.x;
-    const uint32_t lane = tid & 63u;
-    const uint32_t w = uniform(tid >> 6);
-    // virtual id: the workgroup id rotated right by 5 bits within rot_bits bits
-    const uint64_t v = (blockIdx.x >> 5) |
-                       (static_cast<uint64_t>(blockIdx.x & 31u) << (P.rot_bits - 5));
-    if (v >= P.num_virtual) return;
-
-    const Snapshot sn = locate_snapshot(P, v);
-    const uint64_t b = sn.b, s0 = sn.s0, s1 = sn.s1, q0 = sn.q0;
-    const uint64_t R = sn.q1 - q0;
-    const uint64_t nb = s1 - s0;
-    const uint64_t tiles = nb ? (nb + kTile - 1) >> kTileLog2 : 1;
-    const uint64_t p = v - sn.first;  // wraps (and exits) if the offsets are malformed
-    // request slice: this workgroup answers requests y, y + slices, ... of the snapshot
-    const uint32_t y = blockIdx.y;
-    if (p >= tiles || R == 0 || y >= R) return;
-    // At most pc workgroups per snapshot: each takes `stride` consecutive tiles.
-    const uint64_t stride = tiles <= P.pc ? 1 : (tiles + P.pc - 1) / P.pc;
-    if (stride != 1 && p % stride != 0) return;
-    const uint64_t g = stride == 1 ? p : p / stride;
-    const uint64_t G = stride == 1 ? tiles : (tiles + stride - 1) / stride;
-    const uint64_t tau_end = p + stride < tiles ? p + stride : tiles;
-    const bool direct = tiles == 1;
-    // requests of this slice, and wavefronts per request
-    const uint64_t K = (R - y + P.slices - 1) / P.slices;
-    uint32_t wpr = 1;
-    if (K < kWaves) {
-        uint32_t k2 = 1;
-        while (k2 < K) k2 <<= 1;
-        wpr = kWaves / k2 < kMaxWpr ? kWaves / k2 : kMaxWpr;
-    }
-
-    for (uint64_t tau = p; tau < tau_end; ++tau) {
-        const uint64_t t0 = s0 + (tau << kTileLog2);  // global index of the tile start
-        const uint64_t tl = t0 - s0;                   // snapshot-local index of the tile start
-        const uint32_t nt = static_cast<uint32_t>(s1 - t0 < kTile ? s1 - t0 : kTile);
-        // halo blocks available after a full tile
-        const uint64_t after = s1 - t0 - nt;
-        const uint32_t hm = nt == kTile ? static_cast<uint32_t>(after < kHaloCap ? after : kHaloCap) : 0;
-
-        // ---- 1. stage
-        bool packed;
-        uint32_t end;
-        uint64_t xend, xcend;
-        uint32_t endrun;
-        {
-            uint64_t sz[kItems], ct[kItems];
-            uint8_t kd[kItems];
-            load_items(P, t0, nt, sz, ct, kd);
-            Sums h{0, 0, 0};
-            if (tid < hm) {
-                const uint64_t gp = t0 + kTile + tid;
-                const uint8_t k = P.kind[gp];
-                h.q = P.size[gp];
-                const uint64_t c = P.cost[gp];
-                h.c = k == COOP_EVICTABLE ? c : 0;
-                h.r = (k >= COOP_PINNED ? 1u : 0u) + ((h.q >> 32) >> kBigHiLog2 ? 1u << 16 : 0u);
-            }
-            const Sums hown = h;
-            // thread-local exclusive sums
-            Sums t{0, 0, 0};
-            uint32_t xr[kItems];
-            uint32_t hi_or = 0;
-#pragma unroll
-            for (uint32_t j = 0; j < kItems; ++j) {
-                const uint64_t s_j = sz[j];
-                const uint64_t c_j = kd[j] == COOP_EVICTABLE ? ct[j] : 0;
-                sz[j] = t.q;
-                ct[j] = t.c;
-                xr[j] = t.r;
-                t.q += s_j;
-                t.c += c_j;
-                t.r += kd[j] >= COOP_PINNED ? 1u : 0u;
-                hi_or |= static_cast<uint32_t>(s_j >> 32);
-            }
-            if (hi_or >> kBigHiLog2) t.r += 1u << 16;
-            Sums wi = t;
-            wave_inclusive_sum(wi);
-            if (w < 4 && hm) wave_inclusive_sum(h);  // inclusive halo sums (waves 0..3)
-            if (lane == 63) {
-                sm.wsum[w] = wi;
-                if (w < 4) sm.hsum[w] = h;
-            }
-            __syncthreads();
-            // lanes 0..7: wavefront totals of the tile, 8..11: of the halo
-            Sums bsum{0, 0, 0};
-            if (lane < kWaves) bsum = sm.wsum[lane];
-            else if (lane < kWaves + 4 && hm) bsum = sm.hsum[lane - kWaves];
-            row_inclusive_sum(bsum);
-            const Sums tile_tot = readlane(bsum, kWaves - 1);
-            const Sums all_tot = readlane(bsum, kWaves + 3);
-            Sums carry = readlane(bsum, w ? w - 1 : 0);
-            if (w == 0) carry = Sums{0, 0, 0};
-            // halo wavefront w < 4: tile total + the earlier halo wavefronts
-            const Sums hcarry = readlane(bsum, kWaves - 1 + (w < 4 ? w : 0));
-            // thread exclusive = block carry + wavefront inclusive - own total
-            const Sums base{carry.q + wi.q - t.q, carry.c + wi.c - t.c, carry.r + wi.r - t.r};
-
-            packed = (tile_tot.r >> 16) == 0;
-            const bool use_halo = packed && hm && (all_tot.r >> 16) == 0;
-            end = use_halo ? kTile + hm : nt;
-            const Sums et = use_halo ? all_tot : tile_tot;
-            endrun = et.r & 0xffffu;
-            xend = packed ? (static_cast<uint64_t>(endrun) << kValBits) | et.q : et.q;
-            xcend = et.c;
-
-            // LDS: boundaries [0, end) by their owners, end and the sentinel by the last thread
-            const uint32_t i0 = tid * kItems;
-            const bool all_mine = i0 + kItems <= end;
-            if (packed) {
-                uint64_t xv[kItems], cv[kItems];
-#pragma unroll
-                for (uint32_t j = 0; j < kItems; ++j) {
-                    const uint64_t pq = base.q + sz[j];
-                    const uint32_t rr = base.r + xr[j];
-                    xv[j] = pq | (static_cast<uint64_t>(rr) << kValBits);
-                    cv[j] = base.c + ct[j];
-                }
-                if (all_mine) {
-#pragma unroll
-                    for (uint32_t j = 0; j < kItems; j += 2) {
-                        *reinterpret_cast<ulonglong2*>(&sm.x[i0 + j]) = ulonglong2{xv[j], xv[j + 1]};
-                        *reinterpret_cast<ulonglong2*>(&sm.xc[i0 + j]) = ulonglong2{cv[j], cv[j + 1]};
-                    }
-                } else {
-#pragma unroll
-                    for (uint32_t j = 0; j < kItems; ++j) {
-                        if (i0 + j < end) {
-                            sm.x[i0 + j] = xv[j];
-                            sm.xc[i0 + j] = cv[j];
-                        }
-                    }
-                }
-                if (use_halo && tid < hm) {
-                    // halo boundary kTile + tid: carry + wavefront inclusive - own block
-                    const uint64_t pq = hcarry.q + h.q - hown.q;
-                    const uint32_t rr = hcarry.r + h.r - hown.r;
-                    sm.x[kTile + tid] = pq | (static_cast<uint64_t>(rr) << kValBits);
-                    sm.xc[kTile + tid] = hcarry.c + h.c - hown.c;
-                }
-            } else {
-#pragma unroll
-                for (uint32_t j = 0; j < kItems; ++j) {
-                    if (i0 + j < end) {
-                        sm.x[i0 + j] = base.q + sz[j];
-                        sm.xc[i0 + j] = base.c + ct[j];
-                        sm.run[i0 + j] = static_cast<uint16_t>(base.r + xr[j]);
-                    }
-                }
-            }
-            if (tid == kThreads - 1) {
-                sm.x[end] = xend;
-                sm.xc[end] = xcend;
-                sm.run[end] = static_cast<uint16_t>(endrun);
-                sm.x[end + 1] = kNone;  // sentinel end key
-            }
-            __syncthreads();
-        }
-        const uint64_t vmask = packed ? kValMask : kNone;
-        const bool open = t0 + end < s1;  // the region's last run may go on
-
-        // ---- 2./3. requests: wavefront task vw = request (vw / wpr), slice (vw % wpr)
-        const uint64_t tasks = K * wpr;
-        uint64_t S_next = 0;
-        if (w < tasks) S_next = P.req_size[q0 + y + (w / wpr) * P.slices];
-        for (uint64_t vw = w; vw < tasks; vw += kWaves) {
-            const uint64_t rl = vw / wpr;
-            const uint32_t sl = static_cast<uint32_t>(vw % wpr);
-            const uint64_t q = q0 + y + rl * P.slices;
-            const uint64_t S = S_next;
-            if (vw + kWaves < tasks) S_next = P.req_size[q0 + y + ((vw + kWaves) / wpr) * P.slices];
-            Cand best = cand_none();
-            uint64_t best_end = 0;
-            if (S != 0 && nt != 0) {
-                const uint64_t Sc = S < (1ull << kValBits) ? S : (1ull << kValBits);
-                const uint32_t lanes = 64u * wpr;
-                const uint32_t gl = sl * 64u + lane;
-                uint32_t e32 = 0;
-                if (packed) {
-                    const uint32_t total = nt + end;
-                    const uint32_t L = merge_steps(total, lanes);
-                    const uint32_t d = gl * L < total ? gl * L : total;
-                    merge_pass(sm, nt, end, d, L, Sc, best, e32);
-                } else {
-                    plain_pass(sm, nt, end, gl, lanes, S, best, e32);
-                }
-                best_end = tl + e32;
-                if (open && sl == 0) {
-                    const uint32_t cur = pending_start(sm, packed, nt, xend, endrun, S, Sc);
-                    if (cur < nt)
-                        stream_pass(P, sm, cur, nt, t0 + end, s0, s1, xend & vmask, xcend, vmask, S,
-                                    best, best_end);
-                }
-            }
-            const Cand m = wave_argmin(best);
-            Key k = key_none();
-            if (m.start != kNone32) {
-                const uint64_t won = __ballot(best.start == m.start);
-                const uint64_t e = readlane64(best_end, static_cast<uint32_t>(__builtin_ctzll(won)));
-                k = Key{m.cost, m.excess + S, tl + m.start, e};
-            }
-            if (lane == 0) {
-                if (wpr == 1) write_result(P, q, g, direct, tau == p, k, S);
-                else sm.slot[vw] = k;
-            }
-        }
-        if (wpr > 1) {
-            __syncthreads();
-            if (tid < K) {
-                const uint64_t q = q0 + y + static_cast<uint64_t>(tid) * P.slices;
-                Key k = sm.slot[tid * wpr];
-                for (uint32_t u = 1; u < wpr; ++u) {
-                    const Key o = sm.slot[tid * wpr + u];
-                    if (key_less(o, k)) k = o;
-                }
-                write_result(P, q, g, direct, tau == p, k, P.req_size[q]);
-            }
-        }
-        __syncthreads();  // LDS reused by the next tile
-    }
-    if (direct) return;
-
-    // ---- combine the partial keys of the snapshot's workgroups
-    __threadfence();
-    __syncthreads();
     __shared__ uint32_t last_flag;
-    if (tid == 0) {
-        uint32_t last = 1;
-        if (G > 1 || (P.slices > 1 && R > 1)) {
-            uint64_t* ctr = P.counters + b;
-            uint64_t old = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            uint64_t want;
-            do {
-                want = (old >> kEpochShift) == P.epoch ? old + 1
-                                                       : (P.epoch << kEpochShift) | 1ull;
-            } while (!__hip_atomic_compare_exchange_strong(ctr, &old, want, __ATOMIC_ACQ_REL,
-                                                           __ATOMIC_RELAXED,
-                                                           __HIP_MEMORY_SCOPE_AGENT));
-            // every (tile group, slice) pair of the snapshot arrives once
-            const uint64_t arrivals = G * (R < P.slices ? R : P.slices);
-            last = (want & ((1ull << kEpochShift) - 1)) == arrivals;
+    const uint32_t tid = threadIdx.x;
+    const uint32_t w = uniform(tid >> 6);
+    const uint64_t u_begin = static_cast<uint64_t>(blockIdx.x) * P.chunk;
+    const uint64_t u_end = u_begin + P.chunk < P.units ? u_begin + P.chunk : P.units;
+    Cursor cur;
+    bool have_cursor = false;
+    Job job;
+    if (!next_job(P, cur, have_cursor, u_begin, u_begin, u_end, job)) return;
+    TileGeom tg = tile_geom(job);
+    TileRegs regs;
+    issue_loads(P, tg, tid, regs);
+    for (;;) {
+        // The thread index, opaque to the compiler: values derived from it
+        // are recomputed in every iteration instead of being kept live (and
+        // spilled) across the loop.
+        uint32_t t = threadIdx.x;
+        asm volatile("" : "+v"(t));
+        // ---- 1. stage the tile whose blocks are in (or on their way to) regs
+        const TileState ts = stage_tile(sm, tg.nt, tg.hm, t, regs);
+        uint32_t wpr = 1;
+        if (job.K < kWaves) {
+            uint32_t k2 = 1;
+            while (k2 < job.K) k2 <<= 1;
+            wpr = kWaves / k2 < kMaxWpr ? kWaves / k2 : kMaxWpr;
         }
-        last_flag = last;
-    }
-    __syncthreads();
-    if (!last_flag) return;
-    __threadfence();
-    for (uint64_t r = tid; r < R; r += kThreads) {
-        const uint64_t q = q0 + r;
-        const Key* row = P.part + q * P.pc;
-        Key best = row[0];
-        for (uint64_t gg = 1; gg < G; ++gg) {
-            const Key o = row[gg];
-            if (key_less(o, best)) best = o;
+        // The workgroup's running keys for the slice's requests, read before
+        // the next tile's loads are issued (loads complete in issue order).
+        Key acc = key_none();
+        if (!job.first) {
+            const uint64_t rl = wpr == 1 ? w + static_cast<uint64_t>(kWaves) * (t & 63u) : t;
+            if (rl < job.K)
+                acc = load_key_vector(P.part + (job.q0 + job.y + rl * P.slices) * P.pc + job.g);
         }
-        P.out[q] = to_window(best, P.req_size[q]);
+        // ---- prefetch the next tile of this workgroup's chunk
+        Job next;
+        const bool has_next = next_job(P, cur, have_cursor, job.u + 1, u_begin, u_end, next);
+        TileGeom tn = tg;
+        if (has_next) {
+            tn = tile_geom(next);
+            issue_loads(P, tn, t, regs);
+        }
+        // ---- 2./3. the requests
+        tile_requests(P, sm, job, tg, ts, wpr, t, acc);
+        __syncthreads();  // LDS is restaged next
+        if (job.last && !job.direct) combine_partials(P, job, t, last_flag);
+        if (!has_next) break;
+        job = next;
+        tg = tn;
     }
 }
 
@@ -817,46 +982,62 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
 // ---------------------------------------------------------------------------
 
 struct Plan {
+    uint64_t num_virtual;  // tile ids per slice
+    uint64_t slices;       // request slices
+    uint64_t units;        // slices * num_virtual
+    uint64_t chunk;        // units per workgroup
+    uint64_t grid;         // workgroups
     uint64_t pc;           // partial slots per request
-    uint64_t num_virtual;  // virtual workgroup ids
-    uint32_t rot_bits;     // grid = 2^rot_bits workgroups
-    uint32_t slices;       // request slices (grid y)
     size_t part_bytes;     // partial keys
     size_t bytes;          // total workspace
 };
 
-// grid x block must stay below 2^32 work-items: 2^23 workgroups of 512 threads
-constexpr uint32_t kMaxRotBits = 23;
-constexpr uint64_t kWideGrid = 2048;  // workgroups wanted before slicing requests
+// Two workgroups of kThreads fit one CU (LDS); 256 CUs.  Workgroups past the
+// resident ones are still correct (nothing waits on another workgroup).
+constexpr uint64_t kGridWGs = 512;
 constexpr uint64_t kMaxSlices = 256;
-static_assert(kWideGrid * kMaxSlices < (1ull << kEpochShift), "tickets fit the counter");
+constexpr uint64_t kSliceRequests = 512;  // requests per snapshot before slicing them
+static_assert(kGridWGs < (1ull << kEpochShift), "tickets fit the counter");
 
 bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests, Plan* pl) {
-    if (num_segments > (1ull << kMaxRotBits) || num_blocks > (1ull << 60) ||
-        num_requests > (1ull << 40))
+    if (num_segments > (1ull << 32) || num_blocks > (1ull << 60) || num_requests > (1ull << 40))
         return false;
-    const uint64_t max_tiles = num_blocks ? (num_blocks + kTile - 1) >> kTileLog2 : 1;
-    uint64_t pc = num_requests ? kPartialBudget / num_requests : 1;
-    if (pc < 1) pc = 1;
-    if (pc > max_tiles) pc = max_tiles;
-    pl->pc = pc;
-    pl->num_virtual = (num_blocks >> kTileLog2) + num_segments;
-    uint32_t bits = 5;
-    while ((1ull << bits) < pl->num_virtual) ++bits;
-    if (bits > kMaxRotBits) return false;
-    pl->rot_bits = bits;
-    // Few tiles but many requests per snapshot (one small pool, many requests):
-    // spread each snapshot's requests over up to kMaxSlices workgroups.
-    pl->slices = 1;
-    if (pl->num_virtual < kWideGrid && num_requests > num_segments) {
+    const uint64_t nv = (num_blocks >> kTileLog2) + num_segments;
+    uint64_t slices = 1;
+    if (num_requests > num_segments) {
         const uint64_t per_snapshot = (num_requests + num_segments - 1) / num_segments;
-        uint64_t want = (kWideGrid + pl->num_virtual - 1) / pl->num_virtual;
-        if (want > per_snapshot) want = per_snapshot;
-        if (want > kMaxSlices) want = kMaxSlices;
-        pl->slices = static_cast<uint32_t>(want);
+        // few tiles: spread each snapshot's requests over more workgroups
+        if (nv < kGridWGs) {
+            uint64_t want = (kGridWGs + nv - 1) / nv;
+            if (want > per_snapshot) want = per_snapshot;
+            if (want > slices) slices = want;
+        }
+        // many requests per snapshot: fewer per workgroup, fewer partial keys
+        const uint64_t want = (per_snapshot + kSliceRequests - 1) / kSliceRequests;
+        if (want > slices) slices = want;
+        if (slices > kMaxSlices) slices = kMaxSlices;
     }
+    pl->num_virtual = nv;
+    pl->slices = slices;
+    pl->units = slices * nv;
+    const uint64_t grid = pl->units < kGridWGs ? pl->units : kGridWGs;
+    uint64_t chunk = (pl->units + grid - 1) / grid;
+    // A snapshot has at most T tiles, which span at most ceil(T / chunk) + 1
+    // chunks: the partial slots a request needs.  Past the budget, chunks
+    // grow instead (fewer workgroups).
+    const uint64_t T = num_blocks ? (num_blocks + kTile - 1) >> kTileLog2 : 1;
+    const uint64_t cap = kPartialBudget / num_requests > 2 ? kPartialBudget / num_requests : 2;
+    if ((T + chunk - 1) / chunk + 1 > cap) {
+        const uint64_t need = (T + cap - 2) / (cap - 1);
+        if (need > chunk) chunk = need;
+    }
+    pl->chunk = chunk;
+    pl->grid = (pl->units + chunk - 1) / chunk;
+    uint64_t pc = (T + chunk - 1) / chunk + 1;
+    if (pc > pl->grid) pc = pl->grid;
+    pl->pc = pc;
     pl->part_bytes = (num_requests * pc * sizeof(Key) + 255) & ~static_cast<size_t>(255);
-    pl->bytes = pl->part_bytes + num_segments * sizeof(uint64_t);
+    pl->bytes = pl->part_bytes + slices * num_segments * sizeof(uint64_t);
     return true;
 }
 
@@ -916,15 +1097,16 @@ coop_status_t coop_window_search(const uint64_t* size, const uint64_t* cost, con
     P.num_segments = num_segments;
     P.num_requests = num_requests;
     P.num_virtual = pl.num_virtual;
+    P.units = pl.units;
+    P.chunk = pl.chunk;
     P.pc = pl.pc;
     P.epoch = g_calls.fetch_add(1, std::memory_order_relaxed) & kEpochMask;
-    P.rot_bits = pl.rot_bits;
     P.slices = pl.slices;
     P.inv_slope = static_cast<double>(num_segments) /
                   (static_cast<double>(num_blocks) / kTile + static_cast<double>(num_segments));
 
-    hipLaunchKernelGGL(coop_window_search_kernel, dim3(1u << pl.rot_bits, pl.slices), dim3(kThreads), 0,
-                       static_cast<hipStream_t>(stream), P);
+    hipLaunchKernelGGL(coop_window_search_kernel, dim3(static_cast<uint32_t>(pl.grid)),
+                       dim3(kThreads), 0, static_cast<hipStream_t>(stream), P);
     if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
     return COOP_OK;
 }
