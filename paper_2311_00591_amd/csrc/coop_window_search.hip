@@ -242,13 +242,22 @@ struct Params {
     uint64_t num_segments;
     uint64_t num_requests;
     uint64_t num_virtual;  // tile ids per slice: floor(num_blocks / kTile) + num_segments
-    uint64_t units;        // work units: slices * num_virtual
+    uint64_t units;        // work units: slices * num_virtual (below 2^32)
     uint64_t chunk;        // consecutive units per workgroup
+    uint64_t chunk_magic;  // ceil(2^64 / chunk), for division by chunk
+    uint64_t nv_magic;     // ceil(2^64 / num_virtual)
     uint64_t pc;           // partial slots per request
     uint64_t epoch;
-    uint64_t slices;       // request slices: slice y takes requests y, y + slices, ...
+    uint32_t slices_log2;  // request slices (a power of two): slice y takes y, y + slices, ...
     double inv_slope;      // guess of b per tile id, for the first snapshot lookup
 };
+
+// floor(n / d) for n < 2^32, with magic = ceil(2^64 / d) (0 for d = 1):
+// the high word of n * magic (Lemire, Kaser and Kurz, "Faster remainder by
+// direct computation", 2019).
+__device__ __forceinline__ uint64_t div_magic(uint64_t n, uint64_t magic) {
+    return magic ? __umul64hi(n, magic) : n;
+}
 
 struct Smem {
     uint64_t x[kXN];    // keys R << 51 | P, or plain P in a tile with a huge block
@@ -334,10 +343,14 @@ struct Job {
 
 // The first unit in [u, u_end) holding a tile to search (a tile of a
 // snapshot with requests in the unit's slice); false if there is none.
-__device__ bool next_job(const Params& P, Cursor& c, bool& have_cursor, uint64_t u,
-                         uint64_t u_begin, uint64_t u_end, Job& job) {
-    for (; u < u_end; ++u) {
-        const uint64_t y = u / P.num_virtual, v = u - y * P.num_virtual;
+// (y, v) is unit u as (slice, tile id) and moves along with it.
+__device__ bool next_job(const Params& P, Cursor& c, bool& have_cursor, uint64_t u, uint64_t& y,
+                         uint64_t& v, uint64_t u_begin, uint64_t u_end, Job& job) {
+    for (; u < u_end; ++u, ++v) {
+        if (v == P.num_virtual) {
+            v = 0;
+            ++y;
+        }
         if (!have_cursor || y != c.y) {
             cursor_locate(P, v, c);
             c.y = y;
@@ -353,7 +366,7 @@ __device__ bool next_job(const Params& P, Cursor& c, bool& have_cursor, uint64_t
         const uint64_t tiles = nb ? (nb + kTile - 1) >> kTileLog2 : 1;
         const uint64_t f = first_id(c.b, c.sb);
         const uint64_t p = v - f;  // wraps (and is skipped) if the offsets are malformed
-        if (p >= tiles || y >= R) continue;
+        if (p >= tiles || y >= R) continue;  // (the loop moves v with u)
         const uint64_t ub = y * P.num_virtual + f;  // unit of tile 0 of (b, y)
         const uint64_t lo = ub > u_begin ? ub : u_begin;
         const uint64_t hi = ub + tiles < u_end ? ub + tiles : u_end;
@@ -364,10 +377,11 @@ __device__ bool next_job(const Params& P, Cursor& c, bool& have_cursor, uint64_t
         job.s1 = s1;
         job.q0 = q0;
         job.R = R;
-        job.K = (R - y + P.slices - 1) / P.slices;
+        job.K = ((R - y - 1) >> P.slices_log2) + 1;
         job.tiles = tiles;
         job.p = p;
-        const uint64_t i_lo = ub / P.chunk, i_hi = (ub + tiles - 1) / P.chunk;
+        const uint64_t ue = ub + tiles - 1 < P.units ? ub + tiles - 1 : P.units - 1;
+        const uint64_t i_lo = div_magic(ub, P.chunk_magic), i_hi = div_magic(ue, P.chunk_magic);
         job.G = i_hi - i_lo + 1;
         if (job.G > P.pc) job.G = P.pc;  // only with malformed offsets
         job.g = blockIdx.x - i_lo;
@@ -379,20 +393,20 @@ __device__ bool next_job(const Params& P, Cursor& c, bool& have_cursor, uint64_t
     return false;
 }
 
-// Loads the kItems blocks [t0 + tid*kItems, +kItems) of a tile of nt blocks;
-// the kinds stay packed, one byte per block.  Blocks past nt read as empty
-// free blocks.  All loads are independent.
+// Issues the loads of the kItems blocks [t0 + tid*kItems, +kItems) of a
+// tile of nt > 0 blocks: 16-byte loads of size and cost when the tile is full
+// and aligned, else one load per block at a clamped index (blocks past nt
+// are masked when staged).  Nothing here uses the loaded values, so no
+// instruction waits for them.
 __device__ __forceinline__ void load_items(const Params& P, uint64_t t0, uint32_t nt, uint32_t tid,
                                            uint64_t (&sz)[kItems], uint64_t (&ct)[kItems],
-                                           uint2& kd) {
+                                           uint32_t (&kd)[kItems]) {
     const uint32_t i0 = tid * kItems;
     const bool aligned = ((reinterpret_cast<uintptr_t>(P.size) | reinterpret_cast<uintptr_t>(P.cost)) &
-                          15u) == 0 &&
-                         (reinterpret_cast<uintptr_t>(P.kind) & 7u) == 0;
-    if (nt == kTile && (t0 & 7u) == 0 && aligned) {
+                          15u) == 0;
+    if (nt == kTile && (t0 & 1u) == 0 && aligned) {
         const ulonglong2* ps = reinterpret_cast<const ulonglong2*>(P.size + t0 + i0);
         const ulonglong2* pc = reinterpret_cast<const ulonglong2*>(P.cost + t0 + i0);
-        kd = *reinterpret_cast<const uint2*>(P.kind + t0 + i0);
 #pragma unroll
         for (uint32_t j = 0; j < kItems / 2; ++j) {
             const ulonglong2 a = ps[j], b = pc[j];
@@ -402,17 +416,17 @@ __device__ __forceinline__ void load_items(const Params& P, uint64_t t0, uint32_
             ct[2 * j + 1] = b.y;
         }
     } else {
-        kd = uint2{0u, 0u};
 #pragma unroll
         for (uint32_t j = 0; j < kItems; ++j) {
-            const uint32_t i = i0 + j;
-            const bool in = i < nt;
-            sz[j] = in ? P.size[t0 + i] : 0;
-            ct[j] = in ? P.cost[t0 + i] : 0;
-            const uint32_t k = in ? P.kind[t0 + i] : static_cast<uint32_t>(COOP_FREE);
-            if (j < 4) kd.x |= k << (8 * j);
-            else kd.y |= k << (8 * (j - 4));
+            const uint32_t i = i0 + j < nt ? i0 + j : nt - 1;
+            sz[j] = P.size[t0 + i];
+            ct[j] = P.cost[t0 + i];
         }
+    }
+#pragma unroll
+    for (uint32_t j = 0; j < kItems; ++j) {
+        const uint32_t i = i0 + j < nt ? i0 + j : nt - 1;
+        kd[j] = P.kind[t0 + i];
     }
 }
 
@@ -420,14 +434,10 @@ __device__ __forceinline__ void load_items(const Params& P, uint64_t t0, uint32_
 // and one halo block for the first kHaloCap threads.
 struct TileRegs {
     uint64_t sz[kItems], ct[kItems];
-    uint2 kd;  // kind of block j in byte j
+    uint32_t kd[kItems];
     uint64_t hq, hc;
     uint32_t hk;
 };
-
-__device__ __forceinline__ uint32_t kind_of(const uint2& kd, uint32_t j) {
-    return ((j < 4 ? kd.x : kd.y) >> (8 * (j & 3))) & 0xffu;
-}
 
 struct TileGeom {
     uint64_t t0;  // global index of the tile start
@@ -448,7 +458,7 @@ __device__ __forceinline__ TileGeom tile_geom(const Job& job) {
 // Issues every load of a tile; nothing waits for them here.
 __device__ __forceinline__ void issue_loads(const Params& P, const TileGeom& t, uint32_t tid,
                                             TileRegs& r) {
-    load_items(P, t.t0, t.nt, tid, r.sz, r.ct, r.kd);
+    if (t.nt) load_items(P, t.t0, t.nt, tid, r.sz, r.ct, r.kd);
     r.hq = 0;
     r.hc = 0;
     r.hk = COOP_FREE;
@@ -679,6 +689,16 @@ __device__ __forceinline__ TileState stage_tile(Smem& sm, uint32_t nt, uint32_t 
         h.r = (r.hk >= COOP_PINNED ? 1u : 0u) + ((r.hq >> 32) >> kBigHiLog2 ? 1u << 16 : 0u);
     }
     const Sums hown = h;
+    // blocks past nt (a partial tile) count as empty free blocks
+    if (nt < kTile) {
+        const uint32_t i0 = tid * kItems;
+#pragma unroll
+        for (uint32_t j = 0; j < kItems; ++j) {
+            const bool in = i0 + j < nt;
+            r.sz[j] = in ? r.sz[j] : 0;
+            r.kd[j] = in ? r.kd[j] : static_cast<uint32_t>(COOP_FREE);
+        }
+    }
     // thread-local exclusive sums
     Sums t{0, 0, 0};
     uint32_t xr[kItems];
@@ -686,7 +706,7 @@ __device__ __forceinline__ TileState stage_tile(Smem& sm, uint32_t nt, uint32_t 
 #pragma unroll
     for (uint32_t j = 0; j < kItems; ++j) {
         const uint64_t s_j = r.sz[j];
-        const uint32_t k_j = kind_of(r.kd, j);
+        const uint32_t k_j = r.kd[j] & 0xffu;
         const uint64_t c_j = k_j == COOP_EVICTABLE ? r.ct[j] : 0;
         r.sz[j] = t.q;
         r.ct[j] = t.c;
@@ -730,26 +750,22 @@ __device__ __forceinline__ TileState stage_tile(Smem& sm, uint32_t nt, uint32_t 
 
     const uint32_t i0 = tid * kItems;
     if (ts.packed) {
-        uint64_t xv[kItems], cv[kItems];
-#pragma unroll
-        for (uint32_t j = 0; j < kItems; ++j) {
-            const uint64_t pq = base.q + r.sz[j];
-            const uint32_t rr = base.r + xr[j];
-            xv[j] = pq | (static_cast<uint64_t>(rr) << kValBits);
-            cv[j] = base.c + r.ct[j];
-        }
+        auto key = [&](uint32_t j) {
+            return (base.q + r.sz[j]) | (static_cast<uint64_t>(base.r + xr[j]) << kValBits);
+        };
         if (i0 + kItems <= ts.end) {
 #pragma unroll
             for (uint32_t j = 0; j < kItems; j += 2) {
-                *reinterpret_cast<ulonglong2*>(&sm.x[i0 + j]) = ulonglong2{xv[j], xv[j + 1]};
-                *reinterpret_cast<ulonglong2*>(&sm.xc[i0 + j]) = ulonglong2{cv[j], cv[j + 1]};
+                *reinterpret_cast<ulonglong2*>(&sm.x[i0 + j]) = ulonglong2{key(j), key(j + 1)};
+                *reinterpret_cast<ulonglong2*>(&sm.xc[i0 + j]) =
+                    ulonglong2{base.c + r.ct[j], base.c + r.ct[j + 1]};
             }
         } else {
 #pragma unroll
             for (uint32_t j = 0; j < kItems; ++j) {
                 if (i0 + j < ts.end) {
-                    sm.x[i0 + j] = xv[j];
-                    sm.xc[i0 + j] = cv[j];
+                    sm.x[i0 + j] = key(j);
+                    sm.xc[i0 + j] = base.c + r.ct[j];
                 }
             }
         }
@@ -793,21 +809,40 @@ __device__ __forceinline__ Key readlane_key(const Key& k, uint32_t lane) {
                readlane64(k.end, lane)};
 }
 
-// Folds this tile's answer for request q into the workgroup's running key
-// and stores it: the final result once the workgroup has covered the whole
-// snapshot alone, else its partial slot.
-__device__ __forceinline__ void store_answer(const Params& P, const Job& job, uint64_t q, Key k,
-                                             const Key& prev, uint64_t S) {
-    if (!job.first && key_less(prev, k)) k = prev;
+// Stores the workgroup's key for request q: the final result once the
+// workgroup has covered the whole snapshot alone, else its partial slot.
+__device__ __forceinline__ void store_answer(const Params& P, const Job& job, uint64_t q, const Key& k,
+                                             uint64_t S) {
     if (job.last && job.direct) P.out[q] = to_window(k, S);
     else P.part[q * P.pc + job.g] = k;
 }
 
+// This wavefront's answer from per-lane bests: the lexicographic minimum,
+// with its end taken from a lane that holds it.
+__device__ __forceinline__ Key wave_answer(const Cand& best, uint64_t best_end, uint64_t tl,
+                                           uint64_t S) {
+    const Cand m = wave_argmin(best);
+    if (m.start == kNone32) return key_none();
+    const uint64_t won = __ballot(best.start == m.start);
+    const uint64_t e = readlane64(best_end, static_cast<uint32_t>(__builtin_ctzll(won)));
+    return Key{m.cost, m.excess + S, tl + m.start, e};
+}
+
+__device__ __forceinline__ Key min_key(const Key& a, const Key& b) { return key_less(b, a) ? b : a; }
+
 // The shortest-window search of one tile for every request of the job's
-// slice (see the file comment, steps 2 and 3).
+// slice (see the file comment, steps 2 and 3).  Wavefront w takes tasks
+// w, w + kWaves, ...; task vw is slice vw % wpr of request vw / wpr.  The
+// wavefront's n-th task keeps its state in lane n: request size (s_lane),
+// running key over this workgroup's tiles of the snapshot (acc, one
+// wavefront per request), and first pending start.  The first loop touches
+// only LDS, so it never waits for the prefetched loads; the loads of the
+// rarer paths (streaming past the staged region, more than 64 tasks per
+// wavefront) come after it.
 __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const Job& job,
                                               const TileGeom& tg, const TileState& ts,
-                                              uint32_t wpr, uint32_t tid, const Key& acc) {
+                                              uint32_t wpr, uint32_t tid, Key& acc,
+                                              uint64_t s_lane) {
     const uint32_t lane = tid & 63u;
     const uint32_t w = uniform(tid >> 6);
     const uint64_t tl = tg.t0 - job.s0;
@@ -815,16 +850,23 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
     const uint64_t vmask = ts.packed ? kValMask : kNone;
     const bool open = tg.t0 + end < job.s1;  // the region's last run may go on
     const uint64_t tasks = job.K * wpr;
-    for (uint64_t vw = w; vw < tasks; vw += kWaves) {
-        const uint64_t rl = vw / wpr;
-        const uint32_t sl = static_cast<uint32_t>(vw % wpr);
-        const uint64_t q = job.q0 + job.y + rl * P.slices;
-        const uint64_t S = P.req_size[q];
+    const uint32_t wl2 = static_cast<uint32_t>(__builtin_ctz(wpr));
+    const uint32_t lanes = 64u * wpr;
+    auto request = [&](uint64_t vw) { return job.q0 + job.y + ((vw >> wl2) << P.slices_log2); };
+    // this wavefront's tasks held in lanes
+    const uint64_t mine = tasks > w ? (tasks - w + kWaves - 1) / kWaves : 0;
+    const uint32_t held = mine < 64 ? static_cast<uint32_t>(mine) : 64u;
+    uint32_t pend = nt;  // lane n: first pending start of task n
+
+    // ---- in-region windows of every held task
+    for (uint32_t n = 0; n < held; ++n) {
+        const uint64_t vw = w + static_cast<uint64_t>(kWaves) * n;
+        const uint32_t sl = static_cast<uint32_t>(vw & (wpr - 1));
+        const uint64_t S = readlane64(s_lane, wpr == 1 ? n : static_cast<uint32_t>(vw >> wl2));
         Cand best = cand_none();
         uint64_t best_end = 0;
         if (S != 0 && nt != 0) {
             const uint64_t Sc = S < (1ull << kValBits) ? S : (1ull << kValBits);
-            const uint32_t lanes = 64u * wpr;
             const uint32_t gl = sl * 64u + lane;
             uint32_t e32 = 0;
             if (ts.packed) {
@@ -838,40 +880,79 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
             best_end = tl + e32;
             if (open && sl == 0) {
                 const uint32_t cur = pending_start(sm, ts.packed, nt, ts.xend, ts.endrun, S, Sc);
-                if (cur < nt)
-                    stream_pass(P, sm, lane, cur, nt, tg.t0 + end, job.s0, job.s1, ts.xend & vmask,
-                                ts.xcend, vmask, S, best, best_end);
+                if (lane == n) pend = cur;
             }
         }
-        const Cand m = wave_argmin(best);
-        Key k = key_none();
-        if (m.start != kNone32) {
-            const uint64_t won = __ballot(best.start == m.start);
-            const uint64_t e = readlane64(best_end, static_cast<uint32_t>(__builtin_ctzll(won)));
-            k = Key{m.cost, m.excess + S, tl + m.start, e};
-        }
+        Key k = wave_answer(best, best_end, tl, S);
         if (wpr == 1) {
-            // this wavefront's request number rl / kWaves sits in lane rl / kWaves of acc
-            const uint64_t kk = rl / kWaves;
-            Key prev = key_none();
-            if (!job.first)
-                prev = kk < 64 ? readlane_key(acc, static_cast<uint32_t>(kk))
-                               : load_key_vector(P.part + q * P.pc + job.g);
-            if (lane == 0) store_answer(P, job, q, k, prev, S);
+            k = min_key(readlane_key(acc, n), k);
+            if (lane == n) acc = k;
         } else if (lane == 0) {
             sm.slot[vw] = k;
             sm.slot_s[vw] = S;
         }
     }
-    if (wpr > 1) {
+    // ---- windows that leave the staged region (the region's last run goes on)
+    uint64_t todo = __ballot(lane < held && pend < nt);
+    while (todo) {
+        const uint32_t n = static_cast<uint32_t>(__builtin_ctzll(todo));
+        todo &= todo - 1;
+        const uint64_t vw = w + static_cast<uint64_t>(kWaves) * n;
+        const uint64_t S = readlane64(s_lane, wpr == 1 ? n : static_cast<uint32_t>(vw >> wl2));
+        Cand best = cand_none();
+        uint64_t best_end = 0;
+        stream_pass(P, sm, lane, readlane32(pend, n), nt, tg.t0 + end, job.s0, job.s1,
+                    ts.xend & vmask, ts.xcend, vmask, S, best, best_end);
+        const Key k = wave_answer(best, best_end, tl, S);
+        if (wpr == 1) {
+            const Key a = min_key(readlane_key(acc, n), k);
+            if (lane == n) acc = a;
+        } else if (lane == 0) {
+            sm.slot[vw] = min_key(sm.slot[vw], k);
+        }
+    }
+    if (wpr == 1) {
+        // results of the held tasks, one per lane
+        if (job.last && lane < held)
+            store_answer(P, job, request(w + static_cast<uint64_t>(kWaves) * lane), acc, s_lane);
+        // ---- tasks past 64 per wavefront: running keys in the partial slots
+        for (uint64_t vw = w + 64ull * kWaves; vw < tasks; vw += kWaves) {
+            const uint64_t q = request(vw);
+            const uint64_t S = P.req_size[q];
+            Cand best = cand_none();
+            uint64_t best_end = 0;
+            if (S != 0 && nt != 0) {
+                const uint64_t Sc = S < (1ull << kValBits) ? S : (1ull << kValBits);
+                uint32_t e32 = 0;
+                if (ts.packed) {
+                    const uint32_t total = nt + end;
+                    const uint32_t L = merge_steps(total, 64u);
+                    const uint32_t d = lane * L < total ? lane * L : total;
+                    merge_pass(sm, nt, end, d, L, Sc, best, e32);
+                } else {
+                    plain_pass(sm, nt, end, lane, 64u, S, best, e32);
+                }
+                best_end = tl + e32;
+                if (open) {
+                    const uint32_t cur = pending_start(sm, ts.packed, nt, ts.xend, ts.endrun, S, Sc);
+                    if (cur < nt)
+                        stream_pass(P, sm, lane, cur, nt, tg.t0 + end, job.s0, job.s1, ts.xend & vmask,
+                                    ts.xcend, vmask, S, best, best_end);
+                }
+            }
+            Key k = wave_answer(best, best_end, tl, S);
+            if (!job.first) k = min_key(load_key_vector(P.part + q * P.pc + job.g), k);
+            if (lane == 0) store_answer(P, job, q, k, S);
+        }
+    } else {
         __syncthreads();
         if (tid < job.K) {
-            Key k = sm.slot[tid * wpr];
-            for (uint32_t u = 1; u < wpr; ++u) {
-                const Key o = sm.slot[tid * wpr + u];
-                if (key_less(o, k)) k = o;
-            }
-            store_answer(P, job, job.q0 + job.y + tid * P.slices, k, acc, sm.slot_s[tid * wpr]);
+            Key k = sm.slot[tid << wl2];
+            for (uint32_t u = 1; u < wpr; ++u) k = min_key(k, sm.slot[(tid << wl2) + u]);
+            acc = job.first ? k : min_key(acc, k);
+            if (job.last)
+                store_answer(P, job, job.q0 + job.y + (static_cast<uint64_t>(tid) << P.slices_log2),
+                             acc, sm.slot_s[tid << wl2]);
         }
     }
 }
@@ -903,7 +984,7 @@ __device__ void combine_partials(const Params& P, const Job& job, uint32_t tid, 
     for (uint64_t k0 = 0; k0 < job.K; k0 += groups) {
         const uint64_t k = k0 + tid / tpr;
         const bool act = k < job.K;
-        const uint64_t q = job.q0 + job.y + (act ? k : 0) * P.slices;
+        const uint64_t q = job.q0 + job.y + ((act ? k : 0) << P.slices_log2);
         Key best = key_none();
         if (act) {
             for (uint64_t gg = sub; gg < job.G; gg += tpr) {
@@ -933,42 +1014,49 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
     Cursor cur;
     bool have_cursor = false;
     Job job;
-    if (!next_job(P, cur, have_cursor, u_begin, u_begin, u_end, job)) return;
+    uint64_t uy = div_magic(u_begin, P.nv_magic);  // unit u_begin as (slice, tile id)
+    uint64_t uv = u_begin - uy * P.num_virtual;
+    if (!next_job(P, cur, have_cursor, u_begin, uy, uv, u_begin, u_end, job)) return;
     TileGeom tg = tile_geom(job);
     TileRegs regs;
     issue_loads(P, tg, tid, regs);
+    // running keys of the current (snapshot, slice) over this workgroup's
+    // tiles: lane j of wavefront w holds request w + kWaves * j (one
+    // wavefront per request), thread j request j (shared requests)
+    Key acc = key_none();
     for (;;) {
         // The thread index, opaque to the compiler: values derived from it
         // are recomputed in every iteration instead of being kept live (and
         // spilled) across the loop.
         uint32_t t = threadIdx.x;
         asm volatile("" : "+v"(t));
-        // ---- 1. stage the tile whose blocks are in (or on their way to) regs
-        const TileState ts = stage_tile(sm, tg.nt, tg.hm, t, regs);
         uint32_t wpr = 1;
         if (job.K < kWaves) {
             uint32_t k2 = 1;
             while (k2 < job.K) k2 <<= 1;
             wpr = kWaves / k2 < kMaxWpr ? kWaves / k2 : kMaxWpr;
         }
-        // The workgroup's running keys for the slice's requests, read before
-        // the next tile's loads are issued (loads complete in issue order).
-        Key acc = key_none();
-        if (!job.first) {
-            const uint64_t rl = wpr == 1 ? w + static_cast<uint64_t>(kWaves) * (t & 63u) : t;
-            if (rl < job.K)
-                acc = load_key_vector(P.part + (job.q0 + job.y + rl * P.slices) * P.pc + job.g);
+        // The request sizes, one per lane (see tile_requests), loaded now and
+        // waited for before the prefetch below: loads complete in issue
+        // order, so a load waited on during the requests would wait for the
+        // prefetch too.
+        uint64_t s_lane = 0;
+        {
+            const uint64_t rl = wpr == 1 ? w + static_cast<uint64_t>(kWaves) * (t & 63u) : (t & 63u);
+            if (rl < job.K) s_lane = P.req_size[job.q0 + job.y + (rl << P.slices_log2)];
         }
+        // ---- 1. stage the tile whose blocks are in (or on their way to) regs
+        const TileState ts = stage_tile(sm, tg.nt, tg.hm, t, regs);
+        asm volatile("" : "+v"(s_lane));
+        if (job.first) acc = key_none();
         // ---- prefetch the next tile of this workgroup's chunk
         Job next;
-        const bool has_next = next_job(P, cur, have_cursor, job.u + 1, u_begin, u_end, next);
-        TileGeom tn = tg;
-        if (has_next) {
-            tn = tile_geom(next);
-            issue_loads(P, tn, t, regs);
-        }
+        ++uv;
+        const bool has_next = next_job(P, cur, have_cursor, job.u + 1, uy, uv, u_begin, u_end, next);
+        const TileGeom tn = has_next ? tile_geom(next) : TileGeom{tg.t0, 0u, 0u};
+        issue_loads(P, tn, t, regs);
         // ---- 2./3. the requests
-        tile_requests(P, sm, job, tg, ts, wpr, t, acc);
+        tile_requests(P, sm, job, tg, ts, wpr, t, acc, s_lane);
         __syncthreads();  // LDS is restaged next
         if (job.last && !job.direct) combine_partials(P, job, t, last_flag);
         if (!has_next) break;
@@ -983,7 +1071,8 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
 
 struct Plan {
     uint64_t num_virtual;  // tile ids per slice
-    uint64_t slices;       // request slices
+    uint64_t slices;       // request slices (a power of two)
+    uint32_t slices_log2;
     uint64_t units;        // slices * num_virtual
     uint64_t chunk;        // units per workgroup
     uint64_t grid;         // workgroups
@@ -1017,8 +1106,13 @@ bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests
         if (want > slices) slices = want;
         if (slices > kMaxSlices) slices = kMaxSlices;
     }
+    uint32_t slices_log2 = 0;
+    while ((1ull << slices_log2) < slices) ++slices_log2;
+    slices = 1ull << slices_log2;
+    if (slices * nv >= (1ull << 32)) return false;
     pl->num_virtual = nv;
     pl->slices = slices;
+    pl->slices_log2 = slices_log2;
     pl->units = slices * nv;
     const uint64_t grid = pl->units < kGridWGs ? pl->units : kGridWGs;
     uint64_t chunk = (pl->units + grid - 1) / grid;
@@ -1040,6 +1134,9 @@ bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests
     pl->bytes = pl->part_bytes + slices * num_segments * sizeof(uint64_t);
     return true;
 }
+
+// ceil(2^64 / d) for d >= 2, and 0 for d = 1 (see div_magic).
+uint64_t magic(uint64_t d) { return d == 1 ? 0 : ~0ull / d + 1; }
 
 std::atomic<uint64_t> g_calls{
     static_cast<uint64_t>(std::chrono::steady_clock::now().time_since_epoch().count())};
@@ -1099,9 +1196,11 @@ coop_status_t coop_window_search(const uint64_t* size, const uint64_t* cost, con
     P.num_virtual = pl.num_virtual;
     P.units = pl.units;
     P.chunk = pl.chunk;
+    P.chunk_magic = magic(pl.chunk);
+    P.nv_magic = magic(pl.num_virtual);
     P.pc = pl.pc;
     P.epoch = g_calls.fetch_add(1, std::memory_order_relaxed) & kEpochMask;
-    P.slices = pl.slices;
+    P.slices_log2 = pl.slices_log2;
     P.inv_slope = static_cast<double>(num_segments) /
                   (static_cast<double>(num_blocks) / kTile + static_cast<double>(num_segments));
 
