@@ -100,7 +100,7 @@ static_assert(kStage < (1u << (kValBits - 38)), "staged prefixes must fit the ke
 static_assert(kStage < (1u << 16), "pinned counts fit 16 bits");
 constexpr uint64_t kNone = ~0ull;
 constexpr uint32_t kNone32 = ~0u;
-constexpr uint32_t kMaxWpr = 8;                  // wavefronts that may share one request
+constexpr uint32_t kMaxWpr = 4;                  // wavefronts that may share one request
 constexpr uint64_t kPartialBudget = 1ull << 23;  // partial keys (32 B each) before chunks grow
 constexpr uint32_t kEpochShift = 24;             // counter = epoch << 24 | tickets
 constexpr uint64_t kEpochMask = (1ull << 40) - 1;
@@ -146,8 +146,8 @@ __device__ __forceinline__ uint32_t uniform(uint32_t v) {
     return static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(v)));
 }
 
-// Prefix-sum element: bytes, effective cost, and the pinned count in the low
-// 16 bits of r (blocks of 2^38 bytes or more are counted from bit 16 up).
+// Prefix-sum element: bytes (or packed key), effective cost, pinned count (or
+// a flag).
 struct Sums {
     uint64_t q, c;
     uint32_t r;
@@ -252,6 +252,14 @@ struct Params {
     double inv_slope;      // guess of b per tile id, for the first snapshot lookup
 };
 
+// A read of an array the kernel never writes (offsets, request sizes)
+// through the constant address space: uniform indices then become scalar
+// loads, which do not queue behind the vector loads in flight.
+typedef const __attribute__((address_space(4))) uint64_t* ConstU64;
+__device__ __forceinline__ uint64_t ld_const(const uint64_t* p, uint64_t i) {
+    return ((ConstU64)(p))[i];
+}
+
 // floor(n / d) for n < 2^32, with magic = ceil(2^64 / d) (0 for d = 1):
 // the high word of n * magic (Lemire, Kaser and Kurz, "Faster remainder by
 // direct computation", 2019).
@@ -290,7 +298,7 @@ __device__ void cursor_locate(const Params& P, uint64_t v, Cursor& c) {
     const uint64_t B = P.num_segments;
     uint64_t g = static_cast<uint64_t>(static_cast<double>(v) * P.inv_slope);
     if (g >= B) g = B - 1;
-    uint64_t sg = P.seg[g], sg1 = P.seg[g + 1];
+    uint64_t sg = ld_const(P.seg, g), sg1 = ld_const(P.seg, g + 1);
     const bool hit = first_id(g, sg) <= v && (g + 1 == B || first_id(g + 1, sg1) > v);
     uint64_t b = g;
     if (!hit) {
@@ -298,20 +306,20 @@ __device__ void cursor_locate(const Params& P, uint64_t v, Cursor& c) {
         if (first_id(g, sg) <= v) lo = g; else hi = g;
         while (hi - lo > 1) {
             const uint64_t mid = lo + (hi - lo) / 2;
-            if (first_id(mid, P.seg[mid]) <= v) lo = mid; else hi = mid;
+            if (first_id(mid, ld_const(P.seg, mid)) <= v) lo = mid; else hi = mid;
         }
         b = lo;
-        sg = P.seg[b];
-        sg1 = P.seg[b + 1];
+        sg = ld_const(P.seg, b);
+        sg1 = ld_const(P.seg, b + 1);
     }
     const uint64_t b2 = b + 2 < B ? b + 2 : B;
     c.b = b;
     c.sb = sg;
     c.sb1 = sg1;
-    c.sb2 = P.seg[b2];
-    c.rb = P.req_off[b];
-    c.rb1 = P.req_off[b + 1];
-    c.rb2 = P.req_off[b2];
+    c.sb2 = ld_const(P.seg, b2);
+    c.rb = ld_const(P.req_off, b);
+    c.rb1 = ld_const(P.req_off, b + 1);
+    c.rb2 = ld_const(P.req_off, b2);
 }
 
 // Moves the cursor forward to the snapshot holding tile id v (v not below
@@ -325,8 +333,8 @@ __device__ __forceinline__ void cursor_advance(const Params& P, uint64_t v, Curs
         c.rb = c.rb1;
         c.rb1 = c.rb2;
         const uint64_t b2 = c.b + 2 < B ? c.b + 2 : B;
-        c.sb2 = P.seg[b2];
-        c.rb2 = P.req_off[b2];
+        c.sb2 = ld_const(P.seg, b2);
+        c.rb2 = ld_const(P.req_off, b2);
     }
 }
 
@@ -675,115 +683,138 @@ struct TileState {
     uint64_t xcend;  // C at the region end
 };
 
-// Prefix sums of a tile (and its halo) into LDS: X[k], C[k] for k < end by
-// their owners, the region end and the sentinel X[end + 1] = all-ones by the
-// last thread.  Two barriers; the second ends the staging.
-__device__ __forceinline__ TileState stage_tile(Smem& sm, uint32_t nt, uint32_t hm, uint32_t tid,
+template <int Ctrl, int RowMask>
+__device__ __forceinline__ void sum2_step(Sums& s) {
+    s.q += dpp64<Ctrl, RowMask>(s.q, 0);
+    s.c += dpp64<Ctrl, RowMask>(s.c, 0);
+}
+
+// Inclusive sums of q and c (r untouched) over the rows, and over the wavefront.
+__device__ __forceinline__ void row_inclusive_sum2(Sums& s) {
+    sum2_step<kRowShr1, 0xf>(s);
+    sum2_step<kRowShr2, 0xf>(s);
+    sum2_step<kRowShr4, 0xf>(s);
+    sum2_step<kRowShr8, 0xf>(s);
+}
+
+__device__ __forceinline__ void wave_inclusive_sum2(Sums& s) {
+    row_inclusive_sum2(s);
+    sum2_step<kRowBcast15, 0xa>(s);
+    sum2_step<kRowBcast31, 0xc>(s);
+}
+
+// Stages a tile (and its halo) into LDS.  One pass of prefix sums: the key
+// itself, X = sum of (size + 2^51 per pinned block), which is R << 51 | P
+// exactly while P stays below 2^51 (every block below 2^38 bytes), C, and the
+// pinned count R.  X[k], C[k] for k < end are written by their owners, the
+// region end and the sentinel X[end + 1] = all-ones by the last thread.  A
+// tile holding a block of 2^38 bytes or more is staged plain instead: P =
+// X - 2^51 R (exact modulo 2^64), R in sm.run, no halo.  Two barriers.
+__device__ __forceinline__ TileState stage_tile(Smem& sm, const TileGeom& tg, uint32_t tid,
                                                 TileRegs& r) {
     const uint32_t lane = tid & 63u;
     const uint32_t w = uniform(tid >> 6);
-    Sums h{0, 0, 0};
+    const uint32_t nt = tg.nt, hm = tg.hm;
+    constexpr uint64_t kRunOne = 1ull << kValBits;
+    constexpr uint32_t kBigFlag = 1u << 31;  // in the R field of a wavefront total
+    uint64_t hx = 0, hc = 0;
+    bool hbig = false;
     if (tid < hm) {
-        h.q = r.hq;
-        h.c = r.hk == COOP_EVICTABLE ? r.hc : 0;
-        h.r = (r.hk >= COOP_PINNED ? 1u : 0u) + ((r.hq >> 32) >> kBigHiLog2 ? 1u << 16 : 0u);
+        hx = r.hq + (r.hk >= COOP_PINNED ? kRunOne : 0);
+        hc = r.hk == COOP_EVICTABLE ? r.hc : 0;
+        hbig = (r.hq >> 32) >> kBigHiLog2;
     }
-    const Sums hown = h;
-    // blocks past nt (a partial tile) count as empty free blocks
-    if (nt < kTile) {
-        const uint32_t i0 = tid * kItems;
-#pragma unroll
-        for (uint32_t j = 0; j < kItems; ++j) {
-            const bool in = i0 + j < nt;
-            r.sz[j] = in ? r.sz[j] : 0;
-            r.kd[j] = in ? r.kd[j] : static_cast<uint32_t>(COOP_FREE);
-        }
-    }
-    // thread-local exclusive sums
+    const uint64_t hx_own = hx, hc_own = hc;
+    const uint32_t i0 = tid * kItems;
+    // thread-local exclusive sums (blocks past nt: empty free blocks)
     Sums t{0, 0, 0};
-    uint32_t xr[kItems];
     uint32_t hi_or = 0;
 #pragma unroll
     for (uint32_t j = 0; j < kItems; ++j) {
-        const uint64_t s_j = r.sz[j];
-        const uint32_t k_j = r.kd[j] & 0xffu;
+        const bool in = nt == kTile || i0 + j < nt;
+        const uint64_t s_j = in ? r.sz[j] : 0;
+        const uint32_t k_j = in ? (r.kd[j] & 0xffu) : static_cast<uint32_t>(COOP_FREE);
+        r.kd[j] = k_j;
         const uint64_t c_j = k_j == COOP_EVICTABLE ? r.ct[j] : 0;
+        const uint32_t p_j = k_j >= COOP_PINNED ? 1u : 0u;
         r.sz[j] = t.q;
         r.ct[j] = t.c;
-        xr[j] = t.r;
-        t.q += s_j;
+        t.q += s_j + (static_cast<uint64_t>(p_j) << kValBits);
         t.c += c_j;
-        t.r += k_j >= COOP_PINNED ? 1u : 0u;
+        t.r += p_j;
         hi_or |= static_cast<uint32_t>(s_j >> 32);
     }
-    if (hi_or >> kBigHiLog2) t.r += 1u << 16;
     Sums wi = t;
     wave_inclusive_sum(wi);
-    if (w < 4 && hm) wave_inclusive_sum(h);  // inclusive halo sums (wavefronts 0..3)
+    Sums hs{hx, hc, 0};
+    if (w < 4 && hm) wave_inclusive_sum2(hs);
+    const bool wbig = __ballot((hi_or >> kBigHiLog2) != 0) != 0;
+    const bool whbig = __ballot(hbig) != 0;
     if (lane == 63) {
-        sm.wsum[w] = wi;
-        if (w < 4) sm.hsum[w] = h;
+        sm.wsum[w] = Sums{wi.q, wi.c, wi.r | (wbig ? kBigFlag : 0u)};
+        if (w < 4) sm.hsum[w] = Sums{hs.q, hs.c, whbig ? kBigFlag : 0u};
     }
     __syncthreads();
     // lanes 0..7: wavefront totals of the tile, 8..11: of the halo
     Sums bsum{0, 0, 0};
     if (lane < kWaves) bsum = sm.wsum[lane];
     else if (lane < kWaves + 4 && hm) bsum = sm.hsum[lane - kWaves];
+    const uint64_t bigs = __ballot((bsum.r & kBigFlag) != 0);
+    bsum.r &= ~kBigFlag;
     row_inclusive_sum(bsum);
     const Sums tile_tot = readlane(bsum, kWaves - 1);
-    const Sums all_tot = readlane(bsum, kWaves + 3);
     Sums carry = readlane(bsum, w ? w - 1 : 0);
     if (w == 0) carry = Sums{0, 0, 0};
-    // halo wavefront w < 4: tile total + the earlier halo wavefronts
-    const Sums hcarry = readlane(bsum, kWaves - 1 + (w < 4 ? w : 0));
-    // thread exclusive = block carry + wavefront inclusive - own total
-    const Sums base{carry.q + wi.q - t.q, carry.c + wi.c - t.c, carry.r + wi.r - t.r};
+    const uint64_t base_x = carry.q + wi.q - t.q, base_c = carry.c + wi.c - t.c;
 
     TileState ts;
-    ts.packed = (tile_tot.r >> 16) == 0;
-    const bool use_halo = ts.packed && hm && (all_tot.r >> 16) == 0;
-    ts.end = use_halo ? kTile + hm : nt;
-    const Sums et = use_halo ? all_tot : tile_tot;
-    ts.endrun = et.r & 0xffffu;
-    ts.xend = ts.packed ? (static_cast<uint64_t>(ts.endrun) << kValBits) | et.q : et.q;
-    ts.xcend = et.c;
-
-    const uint32_t i0 = tid * kItems;
+    ts.packed = (bigs & ((1u << kWaves) - 1)) == 0;
     if (ts.packed) {
-        auto key = [&](uint32_t j) {
-            return (base.q + r.sz[j]) | (static_cast<uint64_t>(base.r + xr[j]) << kValBits);
-        };
+        const bool use_halo = hm && !(bigs >> kWaves);
+        const Sums all_tot = readlane(bsum, kWaves + 3);
+        // halo wavefront w < 4: tile total + the earlier halo wavefronts
+        const uint32_t hl = kWaves - 1 + (w < 4 ? w : 0);
+        const uint64_t hcarry_x = readlane64(bsum.q, hl), hcarry_c = readlane64(bsum.c, hl);
+        ts.end = use_halo ? kTile + hm : nt;
+        ts.xend = use_halo ? all_tot.q : tile_tot.q;
+        ts.xcend = use_halo ? all_tot.c : tile_tot.c;
+        ts.endrun = static_cast<uint32_t>(ts.xend >> kValBits);
         if (i0 + kItems <= ts.end) {
 #pragma unroll
             for (uint32_t j = 0; j < kItems; j += 2) {
-                *reinterpret_cast<ulonglong2*>(&sm.x[i0 + j]) = ulonglong2{key(j), key(j + 1)};
+                *reinterpret_cast<ulonglong2*>(&sm.x[i0 + j]) =
+                    ulonglong2{base_x + r.sz[j], base_x + r.sz[j + 1]};
                 *reinterpret_cast<ulonglong2*>(&sm.xc[i0 + j]) =
-                    ulonglong2{base.c + r.ct[j], base.c + r.ct[j + 1]};
+                    ulonglong2{base_c + r.ct[j], base_c + r.ct[j + 1]};
             }
         } else {
 #pragma unroll
             for (uint32_t j = 0; j < kItems; ++j) {
                 if (i0 + j < ts.end) {
-                    sm.x[i0 + j] = key(j);
-                    sm.xc[i0 + j] = base.c + r.ct[j];
+                    sm.x[i0 + j] = base_x + r.sz[j];
+                    sm.xc[i0 + j] = base_c + r.ct[j];
                 }
             }
         }
         if (use_halo && tid < hm) {
             // halo boundary kTile + tid: carry + wavefront inclusive - own block
-            const uint64_t pq = hcarry.q + h.q - hown.q;
-            const uint32_t rr = hcarry.r + h.r - hown.r;
-            sm.x[kTile + tid] = pq | (static_cast<uint64_t>(rr) << kValBits);
-            sm.xc[kTile + tid] = hcarry.c + h.c - hown.c;
+            sm.x[kTile + tid] = hcarry_x + hs.q - hx_own;
+            sm.xc[kTile + tid] = hcarry_c + hs.c - hc_own;
         }
     } else {
+        uint32_t rr = carry.r + wi.r - t.r;  // pinned blocks before this thread's first block
+        ts.end = nt;
+        ts.endrun = tile_tot.r;
+        ts.xend = tile_tot.q - (static_cast<uint64_t>(tile_tot.r) << kValBits);
+        ts.xcend = tile_tot.c;
 #pragma unroll
         for (uint32_t j = 0; j < kItems; ++j) {
-            if (i0 + j < ts.end) {
-                sm.x[i0 + j] = base.q + r.sz[j];
-                sm.xc[i0 + j] = base.c + r.ct[j];
-                sm.run[i0 + j] = static_cast<uint16_t>(base.r + xr[j]);
+            if (i0 + j < nt) {
+                sm.x[i0 + j] = base_x + r.sz[j] - (static_cast<uint64_t>(rr) << kValBits);
+                sm.xc[i0 + j] = base_c + r.ct[j];
+                sm.run[i0 + j] = static_cast<uint16_t>(rr);
             }
+            rr += r.kd[j] >= COOP_PINNED ? 1u : 0u;
         }
     }
     if (tid == kThreads - 1) {
@@ -918,7 +949,7 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
         // ---- tasks past 64 per wavefront: running keys in the partial slots
         for (uint64_t vw = w + 64ull * kWaves; vw < tasks; vw += kWaves) {
             const uint64_t q = request(vw);
-            const uint64_t S = P.req_size[q];
+            const uint64_t S = ld_const(P.req_size, q);
             Cand best = cand_none();
             uint64_t best_end = 0;
             if (S != 0 && nt != 0) {
@@ -1045,14 +1076,18 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
             const uint64_t rl = wpr == 1 ? w + static_cast<uint64_t>(kWaves) * (t & 63u) : (t & 63u);
             if (rl < job.K) s_lane = P.req_size[job.q0 + job.y + (rl << P.slices_log2)];
         }
-        // ---- 1. stage the tile whose blocks are in (or on their way to) regs
-        const TileState ts = stage_tile(sm, tg.nt, tg.hm, t, regs);
-        asm volatile("" : "+v"(s_lane));
-        if (job.first) acc = key_none();
-        // ---- prefetch the next tile of this workgroup's chunk
+        // The next tile of this workgroup's chunk, found before staging: its
+        // scalar loads (snapshot offsets) then complete during the staging
+        // barriers.  An outstanding scalar load would hold up every LDS wait
+        // of the request phase (they share a counter).
         Job next;
         ++uv;
         const bool has_next = next_job(P, cur, have_cursor, job.u + 1, uy, uv, u_begin, u_end, next);
+        // ---- 1. stage the tile whose blocks are in (or on their way to) regs
+        const TileState ts = stage_tile(sm, tg, t, regs);
+        asm volatile("" : "+v"(s_lane));
+        if (job.first) acc = key_none();
+        // ---- prefetch the next tile
         const TileGeom tn = has_next ? tile_geom(next) : TileGeom{tg.t0, 0u, 0u};
         issue_loads(P, tn, t, regs);
         // ---- 2./3. the requests
