@@ -402,22 +402,25 @@ __device__ bool next_job(const Params& P, Cursor& c, bool& have_cursor, uint64_t
 }
 
 // Issues the loads of the kItems blocks [t0 + tid*kItems, +kItems) of a
-// tile of nt > 0 blocks: 16-byte loads of size and cost when the tile is full
-// and aligned, else one load per block at a clamped index (blocks past nt
-// are masked when staged).  Nothing here uses the loaded values, so no
-// instruction waits for them.
+// tile of nt > 0 blocks: 16-byte loads of size and cost when the tile starts
+// on an even block, else one load per block, at clamped indices (blocks
+// past nt are masked when staged).  Nothing here uses the loaded values, so
+// no instruction waits for them.
 __device__ __forceinline__ void load_items(const Params& P, uint64_t t0, uint32_t nt, uint32_t tid,
                                            uint64_t (&sz)[kItems], uint64_t (&ct)[kItems],
                                            uint32_t (&kd)[kItems]) {
     const uint32_t i0 = tid * kItems;
     const bool aligned = ((reinterpret_cast<uintptr_t>(P.size) | reinterpret_cast<uintptr_t>(P.cost)) &
                           15u) == 0;
-    if (nt == kTile && (t0 & 1u) == 0 && aligned) {
-        const ulonglong2* ps = reinterpret_cast<const ulonglong2*>(P.size + t0 + i0);
-        const ulonglong2* pc = reinterpret_cast<const ulonglong2*>(P.cost + t0 + i0);
+    // pairs of blocks [i, i + 1); the pair holding block nt - 1 may reach one
+    // block past the tile, which must then exist
+    if (nt >= 2 && (t0 & 1u) == 0 && aligned && ((nt & 1u) == 0 || t0 + nt < P.num_blocks)) {
+        const uint32_t last = (nt - 1) & ~1u;  // pairs past the tile read this one
 #pragma unroll
         for (uint32_t j = 0; j < kItems / 2; ++j) {
-            const ulonglong2 a = ps[j], b = pc[j];
+            const uint32_t i = i0 + 2 * j < last ? i0 + 2 * j : last;
+            const ulonglong2 a = *reinterpret_cast<const ulonglong2*>(P.size + t0 + i);
+            const ulonglong2 b = *reinterpret_cast<const ulonglong2*>(P.cost + t0 + i);
             sz[2 * j] = a.x;
             sz[2 * j + 1] = a.y;
             ct[2 * j] = b.x;
@@ -450,16 +453,18 @@ struct TileRegs {
 struct TileGeom {
     uint64_t t0;  // global index of the tile start
     uint32_t nt;  // blocks in the tile
-    uint32_t hm;  // halo blocks after a full tile
+    uint32_t hm;  // halo blocks: the next blocks of the snapshot, up to kHaloCap
 };
 
+// Tile p of a snapshot: its blocks [s0 + p * kTile, +kTile), clipped to the
+// snapshot, and the halo after it.
 __device__ __forceinline__ TileGeom tile_geom(const Job& job) {
     TileGeom t;
     t.t0 = job.s0 + (job.p << kTileLog2);
     const uint64_t left = job.s1 - t.t0;
     t.nt = static_cast<uint32_t>(left < kTile ? left : kTile);
     const uint64_t after = left - t.nt;
-    t.hm = t.nt == kTile ? static_cast<uint32_t>(after < kHaloCap ? after : kHaloCap) : 0;
+    t.hm = static_cast<uint32_t>(after < kHaloCap ? after : kHaloCap);
     return t;
 }
 
@@ -471,7 +476,7 @@ __device__ __forceinline__ void issue_loads(const Params& P, const TileGeom& t, 
     r.hc = 0;
     r.hk = COOP_FREE;
     if (tid < t.hm) {
-        const uint64_t gp = t.t0 + kTile + tid;
+        const uint64_t gp = t.t0 + t.nt + tid;
         r.hk = P.kind[gp];
         r.hq = P.size[gp];
         r.hc = P.cost[gp];
@@ -775,11 +780,11 @@ __device__ __forceinline__ TileState stage_tile(Smem& sm, const TileGeom& tg, ui
         // halo wavefront w < 4: tile total + the earlier halo wavefronts
         const uint32_t hl = kWaves - 1 + (w < 4 ? w : 0);
         const uint64_t hcarry_x = readlane64(bsum.q, hl), hcarry_c = readlane64(bsum.c, hl);
-        ts.end = use_halo ? kTile + hm : nt;
+        ts.end = use_halo ? nt + hm : nt;
         ts.xend = use_halo ? all_tot.q : tile_tot.q;
         ts.xcend = use_halo ? all_tot.c : tile_tot.c;
         ts.endrun = static_cast<uint32_t>(ts.xend >> kValBits);
-        if (i0 + kItems <= ts.end) {
+        if (i0 + kItems <= nt) {
 #pragma unroll
             for (uint32_t j = 0; j < kItems; j += 2) {
                 *reinterpret_cast<ulonglong2*>(&sm.x[i0 + j]) =
@@ -790,16 +795,16 @@ __device__ __forceinline__ TileState stage_tile(Smem& sm, const TileGeom& tg, ui
         } else {
 #pragma unroll
             for (uint32_t j = 0; j < kItems; ++j) {
-                if (i0 + j < ts.end) {
+                if (i0 + j < nt) {
                     sm.x[i0 + j] = base_x + r.sz[j];
                     sm.xc[i0 + j] = base_c + r.ct[j];
                 }
             }
         }
         if (use_halo && tid < hm) {
-            // halo boundary kTile + tid: carry + wavefront inclusive - own block
-            sm.x[kTile + tid] = hcarry_x + hs.q - hx_own;
-            sm.xc[kTile + tid] = hcarry_c + hs.c - hc_own;
+            // halo boundary nt + tid: carry + wavefront inclusive - own block
+            sm.x[nt + tid] = hcarry_x + hs.q - hx_own;
+            sm.xc[nt + tid] = hcarry_c + hs.c - hc_own;
         }
     } else {
         uint32_t rr = carry.r + wi.r - t.r;  // pinned blocks before this thread's first block
@@ -1154,7 +1159,7 @@ bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests
     // A snapshot has at most T tiles, which span at most ceil(T / chunk) + 1
     // chunks: the partial slots a request needs.  Past the budget, chunks
     // grow instead (fewer workgroups).
-    const uint64_t T = num_blocks ? (num_blocks + kTile - 1) >> kTileLog2 : 1;
+    const uint64_t T = num_blocks ? (num_blocks + kTile - 1) >> kTileLog2 : 1;  // tiles of one snapshot, at most
     const uint64_t cap = kPartialBudget / num_requests > 2 ? kPartialBudget / num_requests : 2;
     if ((T + chunk - 1) / chunk + 1 > cap) {
         const uint64_t need = (T + cap - 2) / (cap - 1);
