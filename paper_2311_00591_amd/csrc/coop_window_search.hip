@@ -371,7 +371,8 @@ __device__ bool next_job(const Params& P, Cursor& c, bool& have_cursor, uint64_t
         const uint64_t q1 = c.rb1 < P.num_requests ? c.rb1 : P.num_requests;
         const uint64_t q0 = c.rb < q1 ? c.rb : q1;
         const uint64_t R = q1 - q0, nb = s1 - s0;
-        const uint64_t tiles = nb ? (nb + kTile - 1) >> kTileLog2 : 1;
+        // tiles start at floor8(s0) + p * kTile (see tile_geom)
+        const uint64_t tiles = nb ? (s1 - (s0 & ~7ull) + kTile - 1) >> kTileLog2 : 1;
         const uint64_t f = first_id(c.b, c.sb);
         const uint64_t p = v - f;  // wraps (and is skipped) if the offsets are malformed
         if (p >= tiles || y >= R) continue;  // (the loop moves v with u)
@@ -402,23 +403,24 @@ __device__ bool next_job(const Params& P, Cursor& c, bool& have_cursor, uint64_t
 }
 
 // Issues the loads of the kItems blocks [t0 + tid*kItems, +kItems) of a
-// tile of nt > 0 blocks: 16-byte loads of size and cost when the tile starts
-// on an even block, else one load per block, at clamped indices (blocks
-// past nt are masked when staged).  Nothing here uses the loaded values, so
-// no instruction waits for them.
+// tile of nt > 0 blocks starting on a multiple of 8: 16-byte loads of size
+// and cost pairs and one 8-byte load of the kinds, at indices clamped to the
+// tile (blocks past nt are masked when staged), when every such load stays
+// inside the arrays; else one load per block.  On the first path nothing
+// uses the loaded values, so no instruction waits for them; the second
+// (arrays not aligned, or the very end of the arrays) packs the kinds at once.
 __device__ __forceinline__ void load_items(const Params& P, uint64_t t0, uint32_t nt, uint32_t tid,
                                            uint64_t (&sz)[kItems], uint64_t (&ct)[kItems],
-                                           uint32_t (&kd)[kItems]) {
+                                           uint32_t (&kd)[2]) {
     const uint32_t i0 = tid * kItems;
     const bool aligned = ((reinterpret_cast<uintptr_t>(P.size) | reinterpret_cast<uintptr_t>(P.cost)) &
-                          15u) == 0;
-    // pairs of blocks [i, i + 1); the pair holding block nt - 1 may reach one
-    // block past the tile, which must then exist
-    if (nt >= 2 && (t0 & 1u) == 0 && aligned && ((nt & 1u) == 0 || t0 + nt < P.num_blocks)) {
-        const uint32_t last = (nt - 1) & ~1u;  // pairs past the tile read this one
+                          15u) == 0 &&
+                         (reinterpret_cast<uintptr_t>(P.kind) & 7u) == 0;
+    if (aligned && (t0 & 7u) == 0 && t0 + ((nt + 7u) & ~7u) <= P.num_blocks) {
+        const uint32_t last2 = (nt - 1) & ~1u, last8 = (nt - 1) & ~7u;
 #pragma unroll
         for (uint32_t j = 0; j < kItems / 2; ++j) {
-            const uint32_t i = i0 + 2 * j < last ? i0 + 2 * j : last;
+            const uint32_t i = i0 + 2 * j < last2 ? i0 + 2 * j : last2;
             const ulonglong2 a = *reinterpret_cast<const ulonglong2*>(P.size + t0 + i);
             const ulonglong2 b = *reinterpret_cast<const ulonglong2*>(P.cost + t0 + i);
             sz[2 * j] = a.x;
@@ -426,18 +428,19 @@ __device__ __forceinline__ void load_items(const Params& P, uint64_t t0, uint32_
             ct[2 * j] = b.x;
             ct[2 * j + 1] = b.y;
         }
+        const uint2 k2 = *reinterpret_cast<const uint2*>(P.kind + t0 + (i0 < last8 ? i0 : last8));
+        kd[0] = k2.x;
+        kd[1] = k2.y;
     } else {
+        kd[0] = 0;
+        kd[1] = 0;
 #pragma unroll
         for (uint32_t j = 0; j < kItems; ++j) {
             const uint32_t i = i0 + j < nt ? i0 + j : nt - 1;
             sz[j] = P.size[t0 + i];
             ct[j] = P.cost[t0 + i];
+            kd[j >> 2] |= static_cast<uint32_t>(P.kind[t0 + i]) << (8 * (j & 3));
         }
-    }
-#pragma unroll
-    for (uint32_t j = 0; j < kItems; ++j) {
-        const uint32_t i = i0 + j < nt ? i0 + j : nt - 1;
-        kd[j] = P.kind[t0 + i];
     }
 }
 
@@ -445,22 +448,26 @@ __device__ __forceinline__ void load_items(const Params& P, uint64_t t0, uint32_
 // and one halo block for the first kHaloCap threads.
 struct TileRegs {
     uint64_t sz[kItems], ct[kItems];
-    uint32_t kd[kItems];
+    uint32_t kd[2];  // kind of block j in byte j & 3 of kd[j / 4]
     uint64_t hq, hc;
     uint32_t hk;
 };
 
 struct TileGeom {
-    uint64_t t0;  // global index of the tile start
-    uint32_t nt;  // blocks in the tile
-    uint32_t hm;  // halo blocks: the next blocks of the snapshot, up to kHaloCap
+    uint64_t t0;    // global index of the tile start (a multiple of 8)
+    uint32_t nt;    // blocks in the tile, counting the lead
+    uint32_t hm;    // halo blocks: the next blocks of the snapshot, up to kHaloCap
+    uint32_t lead;  // blocks before the snapshot start (first tile only): pinned phantoms
 };
 
-// Tile p of a snapshot: its blocks [s0 + p * kTile, +kTile), clipped to the
-// snapshot, and the halo after it.
+// Tile p of a snapshot covers [a + p * kTile, +kTile) clipped to the snapshot
+// end, with a = floor8(s0): every tile starts on a multiple of 8.  The
+// first tile's blocks before s0 (fewer than 8) are staged as empty pinned
+// blocks, so that no window starts at or crosses them.  The halo follows.
 __device__ __forceinline__ TileGeom tile_geom(const Job& job) {
     TileGeom t;
-    t.t0 = job.s0 + (job.p << kTileLog2);
+    t.t0 = (job.s0 & ~7ull) + (job.p << kTileLog2);
+    t.lead = job.p == 0 ? static_cast<uint32_t>(job.s0 - t.t0) : 0u;
     const uint64_t left = job.s1 - t.t0;
     t.nt = static_cast<uint32_t>(left < kTile ? left : kTile);
     const uint64_t after = left - t.nt;
@@ -731,15 +738,21 @@ __device__ __forceinline__ TileState stage_tile(Smem& sm, const TileGeom& tg, ui
     }
     const uint64_t hx_own = hx, hc_own = hc;
     const uint32_t i0 = tid * kItems;
-    // thread-local exclusive sums (blocks past nt: empty free blocks)
+    // thread-local exclusive sums (blocks past nt: empty free blocks; blocks
+    // before the lead: empty pinned blocks)
+    const uint32_t lead = tg.lead;
     Sums t{0, 0, 0};
     uint32_t hi_or = 0;
+    uint32_t kinds[kItems];
 #pragma unroll
     for (uint32_t j = 0; j < kItems; ++j) {
-        const bool in = nt == kTile || i0 + j < nt;
+        const bool in = (nt == kTile || i0 + j < nt) && i0 + j >= lead;
         const uint64_t s_j = in ? r.sz[j] : 0;
-        const uint32_t k_j = in ? (r.kd[j] & 0xffu) : static_cast<uint32_t>(COOP_FREE);
-        r.kd[j] = k_j;
+        const uint32_t raw = (r.kd[j >> 2] >> (8 * (j & 3))) & 0xffu;
+        const uint32_t k_j = in ? raw
+                                : (i0 + j < lead ? static_cast<uint32_t>(COOP_PINNED)
+                                                 : static_cast<uint32_t>(COOP_FREE));
+        kinds[j] = k_j;
         const uint64_t c_j = k_j == COOP_EVICTABLE ? r.ct[j] : 0;
         const uint32_t p_j = k_j >= COOP_PINNED ? 1u : 0u;
         r.sz[j] = t.q;
@@ -819,7 +832,7 @@ __device__ __forceinline__ TileState stage_tile(Smem& sm, const TileGeom& tg, ui
                 sm.xc[i0 + j] = base_c + r.ct[j];
                 sm.run[i0 + j] = static_cast<uint16_t>(rr);
             }
-            rr += r.kd[j] >= COOP_PINNED ? 1u : 0u;
+            rr += kinds[j] >= COOP_PINNED ? 1u : 0u;
         }
     }
     if (tid == kThreads - 1) {
@@ -1093,7 +1106,7 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
         asm volatile("" : "+v"(s_lane));
         if (job.first) acc = key_none();
         // ---- prefetch the next tile
-        const TileGeom tn = has_next ? tile_geom(next) : TileGeom{tg.t0, 0u, 0u};
+        const TileGeom tn = has_next ? tile_geom(next) : TileGeom{tg.t0, 0u, 0u, 0u};
         issue_loads(P, tn, t, regs);
         // ---- 2./3. the requests
         tile_requests(P, sm, job, tg, ts, wpr, t, acc, s_lane);
@@ -1159,7 +1172,7 @@ bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests
     // A snapshot has at most T tiles, which span at most ceil(T / chunk) + 1
     // chunks: the partial slots a request needs.  Past the budget, chunks
     // grow instead (fewer workgroups).
-    const uint64_t T = num_blocks ? (num_blocks + kTile - 1) >> kTileLog2 : 1;  // tiles of one snapshot, at most
+    const uint64_t T = ((num_blocks + kTile - 1) >> kTileLog2) + 1;  // tiles of one snapshot, at most
     const uint64_t cap = kPartialBudget / num_requests > 2 ? kPartialBudget / num_requests : 2;
     if ((T + chunk - 1) / chunk + 1 > cap) {
         const uint64_t need = (T + cap - 2) / (cap - 1);
