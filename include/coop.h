@@ -67,6 +67,31 @@ coop_status_t coop_window_search_workspace_size(uint64_t num_blocks,
                                                 uint64_t num_requests,
                                                 size_t *bytes_out);
 
+/* How coop_window_search splits a batch of these dimensions: host-side
+ * planning only, for diagnostics and tests.  A unit is one tile of up to
+ * 4096 blocks of a snapshot for one slice of that snapshot's requests.  Each
+ * of the `workgroups` persistent workgroups first sweeps a chunk of
+ * first_chunk_units consecutive units (all of them lie below first_units);
+ * the units from first_units on are claimed from a queue in chunks of at
+ * least queued_chunk_units units, which the kernel lengthens until no
+ * snapshot spans more than partial_slots - 2 chunks.  chunks_max bounds the
+ * number of chunks; partial_slots is the number of partial results kept per
+ * request.  Returns COOP_ERR_INVALID if plan_out is NULL or the batch is too
+ * large to launch. */
+typedef struct {
+    uint64_t workgroups;
+    uint64_t slices;
+    uint64_t units;
+    uint64_t first_chunk_units;
+    uint64_t first_units;
+    uint64_t queued_chunk_units;
+    uint64_t chunks_max;
+    uint64_t partial_slots;
+} coop_plan_t;
+
+coop_status_t coop_window_search_plan(uint64_t num_blocks, uint64_t num_segments,
+                                      uint64_t num_requests, coop_plan_t *plan_out);
+
 /*
  * coop_window_search -- enqueue the search for every request of a batch.
  *

@@ -36,6 +36,13 @@ class CoopError(RuntimeError):
         self.status = status
 
 
+class CoopPlan(ctypes.Structure):
+    """coop_plan_t."""
+    _fields_ = [(name, ctypes.c_uint64) for name in (
+        "workgroups", "slices", "units", "first_chunk_units", "first_units",
+        "queued_chunk_units", "chunks_max", "partial_slots")]
+
+
 def load_library():
     """Loads libcoop.so; raises if it has not been built."""
     global _lib
@@ -52,6 +59,8 @@ def load_library():
     lib.coop_status_string.restype = ctypes.c_char_p
     lib.coop_window_search_workspace_size.argtypes = [u64, u64, u64, ctypes.POINTER(sz)]
     lib.coop_window_search_workspace_size.restype = ctypes.c_int
+    lib.coop_window_search_plan.argtypes = [u64, u64, u64, ctypes.POINTER(CoopPlan)]
+    lib.coop_window_search_plan.restype = ctypes.c_int
     lib.coop_window_search.argtypes = [vp, vp, vp, u64, vp, u64, vp, vp, u64, vp, vp, sz, vp]
     lib.coop_window_search.restype = ctypes.c_int
     _lib = lib
@@ -70,6 +79,14 @@ def workspace_size(num_blocks: int, num_segments: int, num_requests: int) -> int
     _check(load_library().coop_window_search_workspace_size(
         int(num_blocks), int(num_segments), int(num_requests), ctypes.byref(out)))
     return out.value
+
+
+def plan_info(num_blocks: int, num_segments: int, num_requests: int) -> dict:
+    """How the library splits a batch of these counts (coop_plan_t as a dict)."""
+    plan = CoopPlan()
+    _check(load_library().coop_window_search_plan(
+        int(num_blocks), int(num_segments), int(num_requests), ctypes.byref(plan)))
+    return {name: int(getattr(plan, name)) for name, _ in CoopPlan._fields_}
 
 
 def _u64_tensor(t: torch.Tensor, name: str, device) -> torch.Tensor:

@@ -7,19 +7,19 @@
 //
 // Work decomposition
 // ------------------
-// Each snapshot b of N_b blocks is cut into tiles of kTile blocks
-// (ceil(N_b / kTile) tiles, one for an empty snapshot).  A workgroup owns a
-// tile and answers every request of the snapshot for the starts in its tile.
-// Workgroups need no host planning: with f(b) = floor(seg[b] / kTile) + b,
-// the tiles of snapshot b are the virtual ids [f(b), f(b) + tiles_b), and f
-// is strictly increasing, so a search over seg_offsets names the snapshot.
-// Ids that name no tile exit at once.  The hardware deals workgroups round
-// robin to the 8 XCDs and their shader engines; the virtual id is a 5-bit
-// rotation of the workgroup id, so every XCD and engine sees an even mix of
-// tiles and empty ids, and consecutive tiles land on the same XCD (halo
-// reads hit its L2).  A snapshot uses at most `pc` workgroups (the
-// partial-key budget per request); with more tiles, each workgroup takes a
-// group of consecutive tiles.
+// Each snapshot b of N_b blocks is cut into tiles of kTile blocks (one for
+// an empty snapshot).  With f(b) = floor(seg[b] / kTile) + b, the tiles of
+// snapshot b are the tile ids [f(b), f(b) + tiles_b), and f is strictly
+// increasing, so a search over seg_offsets names the snapshot of any id; ids
+// that name no tile are skipped.  A work unit is one tile id for one slice
+// of the snapshot's requests.  The grid is persistent (two workgroups per
+// CU).  Units are cut into chunks of consecutive units: workgroup w first
+// takes chunk w (a large one), then claims small chunks from a queue until
+// it runs dry.  The queue evens out the finish times: of the two workgroups
+// on a CU, the one dispatched first wins the instruction arbitration and
+// runs ahead, and snapshots differ in cost.  A workgroup walks its chunk
+// with a cursor over the snapshot list, and loads the next tile into
+// registers while it answers the requests of the current one.
 //
 // Per tile
 // --------
@@ -54,11 +54,11 @@
 //
 // Combining tiles
 // ---------------
-// A snapshot with one tile writes its results directly.  Otherwise every
-// workgroup writes one partial key per request into the workspace and takes
-// a ticket on a per-snapshot counter; the workgroup holding the last ticket
-// reduces the partials and writes the results.  Counters carry a per-call
-// epoch, so the workspace never needs clearing.
+// A snapshot held by one chunk writes its results directly.  Otherwise every
+// chunk writes one partial key per request into the workspace and takes a
+// ticket on a per-snapshot counter; the chunk holding the last ticket reduces
+// the partials and writes the results.  Counters and the queue carry a
+// per-call tag, so the workspace never needs clearing.
 //
 // All arithmetic is unsigned 64-bit integer.  Prefix sums wrap modulo 2^64;
 // differences over a window are exact whenever each run's byte and cost
@@ -104,6 +104,9 @@ constexpr uint32_t kMaxWpr = 4;                  // wavefronts that may share on
 constexpr uint64_t kPartialBudget = 1ull << 23;  // partial keys (32 B each) before chunks grow
 constexpr uint32_t kEpochShift = 24;             // counter = epoch << 24 | tickets
 constexpr uint64_t kEpochMask = (1ull << 40) - 1;
+// Queue word: call tag << 32 | chunks claimed.  A reserve chunk slot holds a
+// chunk index, kQEmpty (nothing claimed yet) or kQDone (the queue ran dry).
+constexpr uint64_t kQEmpty = ~0ull, kQDone = ~0ull - 1;
 
 // DPP controls (GFX9 encoding).
 constexpr int kRowShr1 = 0x111, kRowShr2 = 0x112, kRowShr4 = 0x114, kRowShr8 = 0x118;
@@ -238,14 +241,22 @@ struct Params {
     coop_window_t* out;
     Key* part;             // [num_requests][pc] partial keys
     uint64_t* counters;    // [slices][num_segments] arrival tickets
+    uint64_t* queue;       // chunk queue word
     uint64_t num_blocks;
     uint64_t num_segments;
     uint64_t num_requests;
     uint64_t num_virtual;  // tile ids per slice: floor(num_blocks / kTile) + num_segments
     uint64_t units;        // work units: slices * num_virtual (below 2^32)
-    uint64_t chunk;        // consecutive units per workgroup
-    uint64_t chunk_magic;  // ceil(2^64 / chunk), for division by chunk
+    uint64_t grid;         // workgroups; chunk w < grid is workgroup w's first
+    uint64_t c1, c2;       // units per chunk: first chunks [0, u1), queued chunks after
+                           // (c2 is a lower bound from the host, set by the kernel)
+    uint64_t u1;           // units in the first chunks
+    uint64_t nchunks;      // chunks in all (set by the kernel when there is a queue)
+    uint64_t c1_magic;     // ceil(2^64 / c1), for division by c1
+    uint64_t c2_magic;     // ceil(2^64 / c2) (set by the kernel)
     uint64_t nv_magic;     // ceil(2^64 / num_virtual)
+    uint64_t qtag;         // this call's queue tag (32 bits)
+    uint32_t queue_on;     // units past u1 go through the queue
     uint64_t pc;           // partial slots per request
     uint64_t epoch;
     uint32_t slices_log2;  // request slices (a power of two): slice y takes y, y + slices, ...
@@ -267,6 +278,22 @@ __device__ __forceinline__ uint64_t div_magic(uint64_t n, uint64_t magic) {
     return magic ? __umul64hi(n, magic) : n;
 }
 
+// The chunk holding unit u, and the units of chunk c.
+__device__ __forceinline__ uint64_t chunk_of(const Params& P, uint64_t u) {
+    return u < P.u1 ? div_magic(u, P.c1_magic) : P.grid + div_magic(u - P.u1, P.c2_magic);
+}
+
+__device__ __forceinline__ void chunk_range(const Params& P, uint64_t c, uint64_t& b, uint64_t& e) {
+    if (c < P.grid) {
+        b = c * P.c1;
+        e = b + P.c1 < P.u1 ? b + P.c1 : P.u1;
+    } else {
+        b = P.u1 + (c - P.grid) * P.c2;
+        e = b + P.c2 < P.units ? b + P.c2 : P.units;
+    }
+    if (b > e) b = e;
+}
+
 struct Smem {
     uint64_t x[kXN];    // keys R << 51 | P, or plain P in a tile with a huge block
     uint64_t xc[kXN];   // C
@@ -275,6 +302,7 @@ struct Smem {
     Sums hsum[4];       // per-wavefront totals of the halo
     Key slot[kWaves];   // answers of wavefronts that share a request
     uint64_t slot_s[kWaves];
+    uint64_t claim;     // a chunk claimed from the queue, for every wavefront
 };
 
 __device__ __forceinline__ uint64_t first_id(uint64_t b, uint64_t seg_b) {
@@ -339,9 +367,9 @@ __device__ __forceinline__ void cursor_advance(const Params& P, uint64_t v, Curs
 }
 
 // One tile to search: tile p of snapshot b, for the requests of slice y.
-// The workgroups whose chunks hold the tiles of (b, y) are G consecutive
-// ones; this one is the g-th.  `first` / `last`: the first / last tile of
-// (b, y) in this workgroup's chunk.  Offsets are clamped to the array
+// The chunks holding the tiles of (b, y) are G consecutive ones; the
+// current chunk is the g-th.  `first` / `last`: the first / last tile of
+// (b, y) in the current chunk.  Offsets are clamped to the array
 // lengths: malformed offsets give wrong answers, never an out-of-bounds
 // access.
 struct Job {
@@ -353,7 +381,7 @@ struct Job {
 // snapshot with requests in the unit's slice); false if there is none.
 // (y, v) is unit u as (slice, tile id) and moves along with it.
 __device__ bool next_job(const Params& P, Cursor& c, bool& have_cursor, uint64_t u, uint64_t& y,
-                         uint64_t& v, uint64_t u_begin, uint64_t u_end, Job& job) {
+                         uint64_t& v, uint64_t u_begin, uint64_t u_end, uint64_t chunk, Job& job) {
     for (; u < u_end; ++u, ++v) {
         if (v == P.num_virtual) {
             v = 0;
@@ -390,10 +418,11 @@ __device__ bool next_job(const Params& P, Cursor& c, bool& have_cursor, uint64_t
         job.tiles = tiles;
         job.p = p;
         const uint64_t ue = ub + tiles - 1 < P.units ? ub + tiles - 1 : P.units - 1;
-        const uint64_t i_lo = div_magic(ub, P.chunk_magic), i_hi = div_magic(ue, P.chunk_magic);
+        const uint64_t i_lo = chunk_of(P, ub), i_hi = chunk_of(P, ue);
         job.G = i_hi - i_lo + 1;
         if (job.G > P.pc) job.G = P.pc;  // only with malformed offsets
-        job.g = blockIdx.x - i_lo;
+        job.g = chunk - i_lo;
+        if (job.g >= job.G) job.g = job.G - 1;  // only with malformed offsets
         job.first = u == lo;
         job.last = u + 1 == hi;
         job.direct = job.G == 1;
@@ -845,12 +874,25 @@ __device__ __forceinline__ TileState stage_tile(Smem& sm, const TileGeom& tg, ui
     return ts;
 }
 
-// A Key read with a vector load: the scalar cache does not see this
-// workgroup's earlier stores to the same slot.
-__device__ __forceinline__ Key load_key_vector(const Key* p) {
-    uint32_t z = 0;
-    asm volatile("" : "+v"(z));
-    return p[z];
+// Partial keys are read by whichever workgroup takes a snapshot's last
+// ticket, possibly on another XCD, and the XCDs' L2 caches are not coherent
+// with each other.  They are written and read with device-scope relaxed
+// atomics, which act at the device-coherent level: publishing them then
+// needs only the writes to have completed before the ticket is taken, and
+// no cache write-back or invalidation (which a device-scope fence would
+// cost on every combine, for the whole L2).
+__device__ __forceinline__ void store_key_device(Key* p, const Key& k) {
+    __hip_atomic_store(&p->cost, k.cost, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&p->bytes, k.bytes, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&p->start, k.start, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&p->end, k.end, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ Key load_key_device(Key* p) {
+    return Key{__hip_atomic_load(&p->cost, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT),
+               __hip_atomic_load(&p->bytes, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT),
+               __hip_atomic_load(&p->start, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT),
+               __hip_atomic_load(&p->end, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)};
 }
 
 __device__ __forceinline__ Key readlane_key(const Key& k, uint32_t lane) {
@@ -863,7 +905,7 @@ __device__ __forceinline__ Key readlane_key(const Key& k, uint32_t lane) {
 __device__ __forceinline__ void store_answer(const Params& P, const Job& job, uint64_t q, const Key& k,
                                              uint64_t S) {
     if (job.last && job.direct) P.out[q] = to_window(k, S);
-    else P.part[q * P.pc + job.g] = k;
+    else store_key_device(P.part + q * P.pc + job.g, k);
 }
 
 // This wavefront's answer from per-lane bests: the lexicographic minimum,
@@ -990,7 +1032,7 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
                 }
             }
             Key k = wave_answer(best, best_end, tl, S);
-            if (!job.first) k = min_key(load_key_vector(P.part + q * P.pc + job.g), k);
+            if (!job.first) k = min_key(load_key_device(P.part + q * P.pc + job.g), k);
             if (lane == 0) store_answer(P, job, q, k, S);
         }
     } else {
@@ -1006,11 +1048,15 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
     }
 }
 
-// After the last tile of (b, y) in this workgroup, when other workgroups
+// After the last tile of (b, y) in the current chunk, when other chunks
 // hold tiles of it too: a ticket on the (b, y) counter; the last of the G
-// arrivals reduces the G partial keys of every request of the slice.
+// arrivals reduces the G partial keys of every request of the slice.  The
+// partial keys are device-scope atomics (store_key_device), so the ticket
+// only has to follow the completion of this workgroup's writes.
 __device__ void combine_partials(const Params& P, const Job& job, uint32_t tid, uint32_t& last_flag) {
-    __threadfence();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0);  // every write of this thread has completed
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
     __syncthreads();
     if (tid == 0) {
         uint64_t* ctr = P.counters + job.y * P.num_segments + job.b;
@@ -1018,13 +1064,12 @@ __device__ void combine_partials(const Params& P, const Job& job, uint32_t tid, 
         uint64_t want;
         do {
             want = (old >> kEpochShift) == P.epoch ? old + 1 : (P.epoch << kEpochShift) | 1ull;
-        } while (!__hip_atomic_compare_exchange_strong(ctr, &old, want, __ATOMIC_ACQ_REL,
+        } while (!__hip_atomic_compare_exchange_strong(ctr, &old, want, __ATOMIC_RELAXED,
                                                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
         last_flag = (want & ((1ull << kEpochShift) - 1)) == job.G;
     }
     __syncthreads();
     if (!last_flag) return;
-    __threadfence();
     // tpr threads per request (a power of two within a wavefront), each
     // taking every tpr-th slot; then a shuffle reduction inside the group
     uint32_t tpr = 64;
@@ -1037,7 +1082,7 @@ __device__ void combine_partials(const Params& P, const Job& job, uint32_t tid, 
         Key best = key_none();
         if (act) {
             for (uint64_t gg = sub; gg < job.G; gg += tpr) {
-                const Key o = P.part[q * P.pc + gg];
+                const Key o = load_key_device(P.part + q * P.pc + gg);
                 if (key_less(o, best)) best = o;
             }
         }
@@ -1053,25 +1098,119 @@ __device__ void combine_partials(const Params& P, const Job& job, uint32_t tid, 
     }
 }
 
-__global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params P) {
+// The most tiles of any snapshot (as tile_geom cuts them), over the
+// workgroup: queued chunks must be long enough that no snapshot spans more
+// than pc - 2 of them.  Offsets are clamped as in next_job.
+__device__ uint64_t max_tiles(const Params& P, Smem& sm, uint32_t tid) {
+    uint64_t m = 1;
+    for (uint64_t b = tid; b < P.num_segments; b += kThreads) {
+        const uint64_t s1 = P.seg[b + 1] < P.num_blocks ? P.seg[b + 1] : P.num_blocks;
+        const uint64_t s0 = P.seg[b] < s1 ? P.seg[b] : s1;
+        const uint64_t t = (s1 - (s0 & ~7ull) + kTile - 1) >> kTileLog2;
+        m = t > m ? t : m;
+    }
+    for (int o = 32; o >= 1; o >>= 1) {
+        const uint64_t x = __shfl_xor(m, o, 64);
+        m = x > m ? x : m;
+    }
+    if ((tid & 63u) == 0) sm.slot_s[tid >> 6] = m;
+    __syncthreads();
+    m = sm.slot_s[0];
+    for (uint32_t i = 1; i < kWaves; ++i) m = sm.slot_s[i] > m ? sm.slot_s[i] : m;
+    __syncthreads();
+    return m;
+}
+
+// Claims the next queued chunk for the workgroup (every thread calls this;
+// one atomic, then the result goes out through LDS).  Returns a chunk index,
+// kQDone once the queue has run dry, or kQEmpty if the queue word still
+// holds an earlier call's tag (this call's reset has not landed yet).
+__device__ uint64_t claim_chunk(const Params& P, Smem& sm, uint32_t tid) {
+    if (tid == 0) {
+        const uint64_t old =
+            __hip_atomic_fetch_add(P.queue, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        uint64_t r = kQEmpty;
+        if ((old >> 32) == P.qtag) {
+            const uint64_t c = P.grid + (old & 0xffffffffull);
+            r = c < P.nchunks ? c : kQDone;
+        }
+        sm.claim = r;
+    }
+    __syncthreads();
+    const uint64_t r = sm.claim;
+    __syncthreads();  // sm.claim is written again by the next claim
+    if (r == kQEmpty) __builtin_amdgcn_s_sleep(16);
+    return r;
+}
+
+// Position of the walk over the units: the current chunk and its units, and
+// unit u as (slice y, tile id v).
+struct Walk {
+    uint64_t chunk, u_begin, u_end, y, v;
+};
+
+__device__ __forceinline__ void walk_chunk(const Params& P, uint64_t c, Walk& wk) {
+    wk.chunk = c;
+    chunk_range(P, c, wk.u_begin, wk.u_end);
+    wk.y = div_magic(wk.u_begin, P.nv_magic);
+    wk.v = wk.u_begin - wk.y * P.num_virtual;
+}
+
+// The first job at unit u or later: in the current chunk, else in the
+// reserve chunk (claimed earlier), else in chunks claimed now, until the
+// queue runs dry.  Uniform across the workgroup (claims synchronise it).
+__device__ __forceinline__ bool find_job(const Params& P, Smem& sm, uint32_t tid, Cursor& cur,
+                                         bool& have_cursor, Walk& wk, uint64_t& reserve, uint64_t u,
+                                         Job& job) {
+    for (;;) {
+        if (next_job(P, cur, have_cursor, u, wk.y, wk.v, wk.u_begin, wk.u_end, wk.chunk, job))
+            return true;
+        u = wk.u_end;  // where next_job left (y, v)
+        if (reserve == kQDone) return false;
+        if (reserve == kQEmpty) {
+            reserve = claim_chunk(P, sm, tid);
+            continue;  // (next_job returns at once: u is the chunk end)
+        }
+        walk_chunk(P, reserve, wk);
+        reserve = kQEmpty;
+        have_cursor = false;  // a later chunk: locate from scratch
+        u = wk.u_begin;
+    }
+}
+
+__global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params Pin) {
     __shared__ Smem sm;
     __shared__ uint32_t last_flag;
     const uint32_t tid = threadIdx.x;
     const uint32_t w = uniform(tid >> 6);
-    const uint64_t u_begin = static_cast<uint64_t>(blockIdx.x) * P.chunk;
-    const uint64_t u_end = u_begin + P.chunk < P.units ? u_begin + P.chunk : P.units;
+    Params P = Pin;
+    // The queue, when there is one: workgroup 0 stamps this call's tag; claims
+    // that reach the word before the stamp see an old tag and try again.
+    // Queued chunks are sized from the snapshots' tile counts, the same in
+    // every workgroup.
+    uint64_t reserve = kQDone;
+    if (P.queue_on) {
+        if (blockIdx.x == 0 && tid == 0)
+            __hip_atomic_store(P.queue, P.qtag << 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const uint64_t tmax = max_tiles(P, sm, tid);
+        const uint64_t need = (tmax + P.pc - 3) / (P.pc - 2);
+        P.c2 = need > P.c2 ? need : P.c2;
+        P.c2_magic = P.c2 == 1 ? 0 : ~0ull / P.c2 + 1;
+        P.nchunks = P.grid + (P.units - P.u1 + P.c2 - 1) / P.c2;
+        reserve = kQEmpty;
+    }
+    Walk wk;
+    walk_chunk(P, blockIdx.x, wk);
     Cursor cur;
     bool have_cursor = false;
     Job job;
-    uint64_t uy = div_magic(u_begin, P.nv_magic);  // unit u_begin as (slice, tile id)
-    uint64_t uv = u_begin - uy * P.num_virtual;
-    if (!next_job(P, cur, have_cursor, u_begin, uy, uv, u_begin, u_end, job)) return;
+    if (!find_job(P, sm, tid, cur, have_cursor, wk, reserve, wk.u_begin, job)) return;
     TileGeom tg = tile_geom(job);
     TileRegs regs;
     issue_loads(P, tg, tid, regs);
-    // running keys of the current (snapshot, slice) over this workgroup's
-    // tiles: lane j of wavefront w holds request w + kWaves * j (one
-    // wavefront per request), thread j request j (shared requests)
+    // running keys of the current (snapshot, slice) over the chunk's tiles:
+    // lane j of wavefront w holds request w + kWaves * j (one wavefront per
+    // request), thread j request j (shared requests)
     Key acc = key_none();
     for (;;) {
         // The thread index, opaque to the compiler: values derived from it
@@ -1094,17 +1233,21 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
             const uint64_t rl = wpr == 1 ? w + static_cast<uint64_t>(kWaves) * (t & 63u) : (t & 63u);
             if (rl < job.K) s_lane = P.req_size[job.q0 + job.y + (rl << P.slices_log2)];
         }
-        // The next tile of this workgroup's chunk, found before staging: its
-        // scalar loads (snapshot offsets) then complete during the staging
-        // barriers.  An outstanding scalar load would hold up every LDS wait
-        // of the request phase (they share a counter).
+        // The next tile, found before staging: its scalar loads (snapshot
+        // offsets) then complete during the staging barriers.  An outstanding
+        // scalar load would hold up every LDS wait of the request phase (they
+        // share a counter).  At the end of a chunk this enters the reserve
+        // chunk, or claims one if the reserve is empty.
         Job next;
-        ++uv;
-        const bool has_next = next_job(P, cur, have_cursor, job.u + 1, uy, uv, u_begin, u_end, next);
+        ++wk.v;
+        const bool has_next = find_job(P, sm, t, cur, have_cursor, wk, reserve, job.u + 1, next);
         // ---- 1. stage the tile whose blocks are in (or on their way to) regs
         const TileState ts = stage_tile(sm, tg, t, regs);
         asm volatile("" : "+v"(s_lane));
         if (job.first) acc = key_none();
+        // ---- keep a chunk in reserve (no vector load is in flight here, so
+        // the claim waits only for itself)
+        if (reserve == kQEmpty) reserve = claim_chunk(P, sm, t);
         // ---- prefetch the next tile
         const TileGeom tn = has_next ? tile_geom(next) : TileGeom{tg.t0, 0u, 0u, 0u};
         issue_loads(P, tn, t, regs);
@@ -1127,8 +1270,10 @@ struct Plan {
     uint64_t slices;       // request slices (a power of two)
     uint32_t slices_log2;
     uint64_t units;        // slices * num_virtual
-    uint64_t chunk;        // units per workgroup
     uint64_t grid;         // workgroups
+    uint64_t c1, c2;       // units per first chunk, per queued chunk
+    uint64_t u1;           // units in the first chunks
+    uint64_t nchunks;      // first chunks (one per workgroup) and queued chunks
     uint64_t pc;           // partial slots per request
     size_t part_bytes;     // partial keys
     size_t bytes;          // total workspace
@@ -1140,6 +1285,8 @@ constexpr uint64_t kGridWGs = 512;
 constexpr uint64_t kMaxSlices = 256;
 constexpr uint64_t kSliceRequests = 512;  // requests per snapshot before slicing them
 static_assert(kGridWGs < (1ull << kEpochShift), "tickets fit the counter");
+constexpr uint64_t kQueueMinChunk = 8;         // smaller shares: no queue
+constexpr uint64_t kQueueMaxSegments = 16384;  // every workgroup scans the offsets once
 
 bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests, Plan* pl) {
     if (num_segments > (1ull << 32) || num_blocks > (1ull << 60) || num_requests > (1ull << 40))
@@ -1178,13 +1325,38 @@ bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests
         const uint64_t need = (T + cap - 2) / (cap - 1);
         if (need > chunk) chunk = need;
     }
-    pl->chunk = chunk;
     pl->grid = (pl->units + chunk - 1) / chunk;
+    // A quarter of each workgroup's share goes to the queue, in chunks of at
+    // least a sixteenth of it (and one unit), so that the workgroups finish
+    // together.  The kernel lengthens queued chunks until the largest
+    // snapshot spans at most pc - 2 of them (a span of L units meets at most
+    // ceil(L / c2) + 2 chunks); pc, the partial slots per request, stays
+    // within the budget.
+    uint64_t c1 = chunk, c2 = chunk, u1 = pl->units, nchunks = pl->grid;
     uint64_t pc = (T + chunk - 1) / chunk + 1;
-    if (pc > pl->grid) pc = pl->grid;
+    if (chunk >= kQueueMinChunk && cap >= 4 && num_segments <= kQueueMaxSegments) {
+        const uint64_t q1 = chunk - chunk / 4, q2 = chunk / 16 ? chunk / 16 : 1;
+        const uint64_t qu1 = pl->grid * q1;
+        const uint64_t qn = pl->grid + (pl->units - qu1 + q2 - 1) / q2;
+        uint64_t qpc = (T + q2 - 1) / q2 + 2;
+        if (qpc > cap) qpc = cap;
+        if (qpc > qn) qpc = qn;
+        if (qu1 < pl->units && qpc >= 4) {
+            c1 = q1;
+            c2 = q2;
+            u1 = qu1;
+            nchunks = qn;
+            pc = qpc;
+        }
+    }
+    if (pc > nchunks) pc = nchunks;
+    pl->c1 = c1;
+    pl->c2 = c2;
+    pl->u1 = u1;
+    pl->nchunks = nchunks;
     pl->pc = pc;
     pl->part_bytes = (num_requests * pc * sizeof(Key) + 255) & ~static_cast<size_t>(255);
-    pl->bytes = pl->part_bytes + slices * num_segments * sizeof(uint64_t);
+    pl->bytes = pl->part_bytes + (slices * num_segments + 1) * sizeof(uint64_t);
     return true;
 }
 
@@ -1219,6 +1391,22 @@ coop_status_t coop_window_search_workspace_size(uint64_t num_blocks, uint64_t nu
     return COOP_OK;
 }
 
+coop_status_t coop_window_search_plan(uint64_t num_blocks, uint64_t num_segments,
+                                      uint64_t num_requests, coop_plan_t* plan_out) {
+    if (!plan_out) return COOP_ERR_INVALID;
+    Plan pl;
+    if (!make_plan(num_blocks, num_segments, num_requests, &pl)) return COOP_ERR_INVALID;
+    plan_out->workgroups = pl.grid;
+    plan_out->slices = pl.slices;
+    plan_out->units = pl.units;
+    plan_out->first_chunk_units = pl.c1;
+    plan_out->first_units = pl.u1;
+    plan_out->queued_chunk_units = pl.c2;
+    plan_out->chunks_max = pl.nchunks;
+    plan_out->partial_slots = pl.pc;
+    return COOP_OK;
+}
+
 coop_status_t coop_window_search(const uint64_t* size, const uint64_t* cost, const uint8_t* kind,
                                  uint64_t num_blocks, const uint64_t* seg_offsets,
                                  uint64_t num_segments, const uint64_t* req_sizes,
@@ -1243,16 +1431,25 @@ coop_status_t coop_window_search(const uint64_t* size, const uint64_t* cost, con
     P.out = out;
     P.part = static_cast<Key*>(workspace);
     P.counters = reinterpret_cast<uint64_t*>(static_cast<char*>(workspace) + pl.part_bytes);
+    P.queue = P.counters + pl.slices * num_segments;
     P.num_blocks = num_blocks;
     P.num_segments = num_segments;
     P.num_requests = num_requests;
     P.num_virtual = pl.num_virtual;
     P.units = pl.units;
-    P.chunk = pl.chunk;
-    P.chunk_magic = magic(pl.chunk);
+    P.grid = pl.grid;
+    P.c1 = pl.c1;
+    P.c2 = pl.c2;
+    P.u1 = pl.u1;
+    P.nchunks = pl.nchunks;
+    P.c1_magic = magic(pl.c1);
+    P.c2_magic = magic(pl.c2);
     P.nv_magic = magic(pl.num_virtual);
     P.pc = pl.pc;
-    P.epoch = g_calls.fetch_add(1, std::memory_order_relaxed) & kEpochMask;
+    const uint64_t call = g_calls.fetch_add(1, std::memory_order_relaxed);
+    P.epoch = call & kEpochMask;
+    P.qtag = call & 0xffffffffull;
+    P.queue_on = pl.nchunks > pl.grid ? 1u : 0u;
     P.slices_log2 = pl.slices_log2;
     P.inv_slope = static_cast<double>(num_segments) /
                   (static_cast<double>(num_blocks) / kTile + static_cast<double>(num_segments));

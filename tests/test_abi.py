@@ -42,8 +42,9 @@ def test_workspace_size_depends_on_counts_only():
     a = coop.workspace_size(4096 * 1024, 1024, 1024)
     assert a == coop.workspace_size(4096 * 1024, 1024, 1024) > 0
     assert coop.workspace_size(1 << 24, 1, 4096) >= coop.workspace_size(1 << 20, 1, 4096)
-    # partial storage is bounded: 2^22 keys of 32 bytes plus one counter per snapshot
-    assert coop.workspace_size(1 << 30, 1, 1 << 20) <= (1 << 22) * 32 + 8 + 256
+    # partial storage is bounded: 2^23 keys of 32 bytes, one counter per
+    # (request slice, snapshot) -- at most 256 slices -- and the queue word
+    assert coop.workspace_size(1 << 30, 1, 1 << 20) <= (1 << 23) * 32 + 256 * 8 + 8 + 256
     lib = coop.load_library()
     assert lib.coop_window_search_workspace_size(1, 1, 1, None) == -1
     out = ctypes.c_size_t()
@@ -92,3 +93,21 @@ def test_gpu_path_shares_nothing_with_the_oracle():
     assert '#include "coop.h"' not in oracle_src
     pkg = open(os.path.join(ROOT, "paper_2311_00591_amd", "__init__.py")).read()
     assert "import oracle" not in pkg and "from oracle" not in pkg
+
+
+def test_plan_queue_and_partial_slots():
+    # a quarter of the units go through the queue once each workgroup has at
+    # least 8; the first chunks tile [0, first_units) exactly
+    p = coop.plan_info(66_267_909, 4096, 16384)
+    assert p["chunks_max"] > p["workgroups"] and 256 < p["workgroups"] <= 512
+    assert p["first_units"] == p["workgroups"] * p["first_chunk_units"] < p["units"]
+    assert p["queued_chunk_units"] >= 1 and p["partial_slots"] >= 4
+    assert p["partial_slots"] * 16384 <= 1 << 23
+    # two units per workgroup: no queue
+    p = coop.plan_info(4096 * 1024, 1024, 1024)
+    assert p["chunks_max"] == p["workgroups"] and p["first_units"] == p["units"]
+    # too many snapshots for every workgroup to scan their offsets: no queue
+    p = coop.plan_info(1 << 26, 1 << 15, 1 << 15)
+    assert p["chunks_max"] == p["workgroups"]
+    lib = coop.load_library()
+    assert lib.coop_window_search_plan(1, 1, 1, None) == -1

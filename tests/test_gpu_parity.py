@@ -244,3 +244,54 @@ def test_halo_that_would_overflow_the_key_field():
     reqs = [1, 512 * 30, 1 << 46, (1 << 46) + 1, 1 << 50, 1 << 52, 1 << 55]
     pools = _pools([(size, cost, kind)], [reqs])
     assert_parity(pools, gpu_search(pools), "halo overflow")
+
+
+def _queue_plan(pools):
+    import paper_2311_00591_amd as coop
+    return coop.plan_info(pools.num_blocks, pools.num_segments, pools.num_requests)
+
+
+def test_queued_chunks_back_to_back():
+    """Enough tiles that a quarter of the units go through the chunk queue;
+    three launches share one workspace, so each must stamp the queue with
+    its own tag before any claim counts."""
+    _announce("queued chunks, back to back")
+    import paper_2311_00591_amd as coop
+    pools = workloads.make_config(3, 5, num_segments=1200)
+    info = _queue_plan(pools)
+    assert info["chunks_max"] > info["workgroups"], info
+    ws = coop.WindowSearch(*coop.to_device(pools, "cuda"))
+    outs = [ws().clone() for _ in range(3)]
+    torch.cuda.synchronize()
+    want = oracle.window_search(*pools.arrays(), threads=_threads())
+    for o in outs:
+        got = o.cpu().numpy().view(np.uint64)
+        bad = np.flatnonzero((got != want).any(axis=1))
+        assert len(bad) == 0, f"{len(bad)} requests differ, first q={int(bad[0])}"
+
+
+def test_queued_chunks_sized_by_the_largest_snapshot():
+    """Many requests leave few partial slots per request, and one snapshot
+    of 100 tiles among thousands of tiny ones: the kernel must lengthen the
+    queued chunks so that the big snapshot spans no more chunks than slots."""
+    _announce("queued chunks sized on the device")
+    rng = np.random.default_rng(15)
+    n_big = 100 * TILE
+    size = (rng.integers(1, 64, size=n_big) * 512).astype(np.uint64)
+    kind = rng.choice([0, 1, 1, 1, 1, 1, 1, 2], size=n_big).astype(np.uint8)
+    cost = rng.integers(0, 10**9, size=n_big).astype(np.uint64)
+    snaps = [(size, cost, kind)]
+    reqs = [[int(x) for x in rng.integers(1, 1 << 28, size=105)]]
+    for _ in range(5000):
+        s = (rng.integers(1, 64, size=64) * 512).astype(np.uint64)
+        k = rng.choice([0, 1, 1, 1, 2], size=64).astype(np.uint8)
+        c = rng.integers(0, 10**6, size=64).astype(np.uint64)
+        snaps.append((s, c, k))
+        reqs.append([int(x) for x in rng.integers(1, 1 << 22, size=105)])
+    pools = _pools(snaps, reqs)
+    info = _queue_plan(pools)
+    assert info["chunks_max"] > info["workgroups"], info
+    # the host's minimum chunk would let the 101-tile snapshot span more
+    # chunks than there are partial slots
+    assert -(-101 // info["queued_chunk_units"]) + 2 > info["partial_slots"], info
+    assert_parity(pools, gpu_search(pools), "queued chunks sized on the device")
