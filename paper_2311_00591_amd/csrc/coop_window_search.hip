@@ -100,7 +100,7 @@ static_assert(kStage < (1u << (kValBits - 38)), "staged prefixes must fit the ke
 static_assert(kStage < (1u << 16), "pinned counts fit 16 bits");
 constexpr uint64_t kNone = ~0ull;
 constexpr uint32_t kNone32 = ~0u;
-constexpr uint32_t kMaxWpr = 4;                  // wavefronts that may share one request
+constexpr uint32_t kMaxWpr = 8;                  // wavefronts that may share one request
 constexpr uint64_t kPartialBudget = 1ull << 23;  // partial keys (32 B each) before chunks grow
 constexpr uint32_t kEpochShift = 24;             // counter = epoch << 24 | tickets
 constexpr uint64_t kEpochMask = (1ull << 40) - 1;
@@ -632,21 +632,43 @@ __device__ __forceinline__ uint32_t lower_bound(uint32_t lo, uint32_t hi, Pred p
     return lo;
 }
 
+// The same search by a whole wavefront (every lane active, same arguments):
+// 64 evenly spaced probes narrow [lo, hi) to one gap per round, so a tile
+// takes two rounds of LDS reads instead of a dozen dependent ones.
+template <typename Pred>
+__device__ __forceinline__ uint32_t wave_lower_bound(uint32_t lo, uint32_t hi, uint32_t lane,
+                                                     Pred pred) {
+    while (hi - lo > 64) {
+        const uint32_t step = (hi - lo + 63) >> 6;
+        const uint32_t i = lo + lane * step;
+        const uint64_t m = __ballot(i >= hi || pred(i));
+        // pred false at every probe below lane f, true at f (or past hi)
+        const uint32_t f = m ? static_cast<uint32_t>(__builtin_ctzll(m)) : 64u;
+        const uint32_t nhi = f < 64 ? lo + f * step : hi;
+        lo = f ? lo + (f - 1) * step + 1 : lo;
+        hi = nhi < hi ? nhi : hi;
+    }
+    const uint64_t m = __ballot(lo + lane >= hi || pred(lo + lane));
+    return m ? lo + static_cast<uint32_t>(__builtin_ctzll(m)) : hi;
+}
+
 // The first start whose window cannot end inside the staged region [0, end]
 // although its run reaches the region's end: starts i < nA with run id endrun
 // and fewer than S bytes from i to the region end.  Such starts form a suffix.
+// Called by a whole wavefront with the same arguments.
 __device__ __forceinline__ uint32_t pending_start(const Smem& sm, bool packed, uint32_t nA,
                                                   uint64_t xend, uint32_t endrun, uint64_t S,
-                                                  uint64_t Sc) {
+                                                  uint64_t Sc, uint32_t lane) {
     if (packed) {
         // run id endrun and X[i] + Sc > X[end]
         const uint64_t by_run = static_cast<uint64_t>(endrun) << kValBits;
         const uint64_t by_bytes = xend >= Sc ? xend - Sc + 1 : 0;
         const uint64_t thr = by_run > by_bytes ? by_run : by_bytes;
-        return lower_bound(0, nA, [&](uint32_t i) { return sm.x[i] >= thr; });
+        return wave_lower_bound(0, nA, lane, [&](uint32_t i) { return sm.x[i] >= thr; });
     }
-    const uint32_t i0 = lower_bound(0, nA, [&](uint32_t i) { return sm.run[i] == endrun; });
-    return lower_bound(i0, nA, [&](uint32_t i) { return xend - sm.x[i] < S; });
+    const uint32_t i0 =
+        wave_lower_bound(0, nA, lane, [&](uint32_t i) { return sm.run[i] == endrun; });
+    return wave_lower_bound(i0, nA, lane, [&](uint32_t i) { return xend - sm.x[i] < S; });
 }
 
 // Finishes the pending starts [cur, nA): all lie in the staged region's last
@@ -970,7 +992,8 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
             }
             best_end = tl + e32;
             if (open && sl == 0) {
-                const uint32_t cur = pending_start(sm, ts.packed, nt, ts.xend, ts.endrun, S, Sc);
+                const uint32_t cur =
+                    pending_start(sm, ts.packed, nt, ts.xend, ts.endrun, S, Sc, lane);
                 if (lane == n) pend = cur;
             }
         }
@@ -1025,7 +1048,8 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
                 }
                 best_end = tl + e32;
                 if (open) {
-                    const uint32_t cur = pending_start(sm, ts.packed, nt, ts.xend, ts.endrun, S, Sc);
+                    const uint32_t cur =
+                        pending_start(sm, ts.packed, nt, ts.xend, ts.endrun, S, Sc, lane);
                     if (cur < nt)
                         stream_pass(P, sm, lane, cur, nt, tg.t0 + end, job.s0, job.s1, ts.xend & vmask,
                                     ts.xcend, vmask, S, best, best_end);
