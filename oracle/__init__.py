@@ -43,8 +43,10 @@ def _load():
         lib.coop_oracle_window_search.argtypes = common + [ctypes.c_int]
         lib.coop_oracle_brute_windows.argtypes = common
         lib.coop_oracle_brute_eq1.argtypes = common
+        lib.coop_oracle_first_fit.argtypes = [p64, p8, ctypes.c_uint64, p64, ctypes.c_uint64,
+                                              p64, p64, ctypes.c_uint64, p64, ctypes.c_int]
         for f in (lib.coop_oracle_window_search, lib.coop_oracle_brute_windows,
-                  lib.coop_oracle_brute_eq1):
+                  lib.coop_oracle_brute_eq1, lib.coop_oracle_first_fit):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -109,3 +111,25 @@ def search_single(size, cost, kind, requests, threads=1):
     requests = _u64(requests)
     return window_search(size, cost, kind, [0, len(size)], requests, [0, len(requests)],
                          threads=threads)
+
+
+def first_fit(size, kind, seg_offsets, req_sizes, req_offsets, threads=1):
+    """Leftmost free chunk of at least S bytes (section 2.4, Algorithm 1's
+    find_free_block_not_less_than); returns uint64 (Q,) snapshot-local block
+    indices, 2**64-1 where the snapshot has no such chunk."""
+    size, seg_offsets = _u64(size), _u64(seg_offsets)
+    req_sizes, req_offsets = _u64(req_sizes), _u64(req_offsets)
+    kind = np.ascontiguousarray(kind, dtype=np.uint8)
+    if len(size) != len(kind):
+        raise ValueError("size and kind must have the same length")
+    if len(seg_offsets) != len(req_offsets) or len(seg_offsets) < 1:
+        raise ValueError("seg_offsets and req_offsets must both have num_segments + 1 entries")
+    out = np.empty(len(req_sizes), dtype=np.uint64)
+    rc = _load().coop_oracle_first_fit(
+        _ptr(size, ctypes.c_uint64), _ptr(kind, ctypes.c_uint8), len(size),
+        _ptr(seg_offsets, ctypes.c_uint64), len(seg_offsets) - 1,
+        _ptr(req_sizes, ctypes.c_uint64), _ptr(req_offsets, ctypes.c_uint64), len(req_sizes),
+        _ptr(out, ctypes.c_uint64), int(threads))
+    if rc != 0:
+        raise OracleError(rc)
+    return out

@@ -309,3 +309,80 @@ int coop_oracle_brute_eq1(const uint64_t *size, const uint64_t *cost,
     }
     return COOP_ORACLE_OK;
 }
+
+/* ---------------------------------------------------------------------------
+ * First fit (section 2.4, and find_free_block_not_less_than in Algorithm 1):
+ * the allocator places a tensor of S bytes at the left end of a free chunk
+ * of at least S bytes, the leftmost such chunk.  The answer is that chunk's
+ * index in its snapshot, found by walking the list from the left.
+ * ------------------------------------------------------------------------- */
+static uint64_t first_fit_one(const uint64_t *size, const uint8_t *kind, uint64_t n,
+                              uint64_t S) {
+    for (uint64_t k = 0; k < n; ++k)
+        if (kind[k] == KIND_FREE && size[k] >= S) return k;
+    return NONE;
+}
+
+struct fit_job {
+    const uint64_t *size;
+    const uint8_t *kind;
+    const uint64_t *seg_offsets, *req_sizes, *req_offsets;
+    uint64_t num_segments, num_requests;
+    uint64_t *out;
+    _Atomic uint64_t next;
+};
+
+static void *fit_worker(void *arg) {
+    struct fit_job *job = (struct fit_job *)arg;
+    for (;;) {
+        uint64_t q0 = atomic_fetch_add(&job->next, SWEEP_CHUNK);
+        if (q0 >= job->num_requests) break;
+        uint64_t q1 = q0 + SWEEP_CHUNK < job->num_requests ? q0 + SWEEP_CHUNK
+                                                           : job->num_requests;
+        for (uint64_t q = q0; q < q1; ++q) {
+            uint64_t b = owner_segment(job->req_offsets, job->num_segments, q);
+            uint64_t s0 = job->seg_offsets[b], n = job->seg_offsets[b + 1] - s0;
+            job->out[q] = first_fit_one(job->size + s0, job->kind + s0, n, job->req_sizes[q]);
+        }
+    }
+    return NULL;
+}
+
+int coop_oracle_first_fit(const uint64_t *size, const uint8_t *kind, uint64_t num_blocks,
+                          const uint64_t *seg_offsets, uint64_t num_segments,
+                          const uint64_t *req_sizes, const uint64_t *req_offsets,
+                          uint64_t num_requests, uint64_t *out, int num_threads) {
+    if (num_blocks && (!size || !kind)) return COOP_ORACLE_ERR_INVALID;
+    if (num_requests && (!req_sizes || !out)) return COOP_ORACLE_ERR_INVALID;
+    if (num_segments == 0) {
+        if (num_blocks || num_requests) return COOP_ORACLE_ERR_INVALID;
+        return COOP_ORACLE_OK;
+    }
+    if (!offsets_ok(seg_offsets, num_segments, num_blocks) ||
+        !offsets_ok(req_offsets, num_segments, num_requests))
+        return COOP_ORACLE_ERR_INVALID;
+    if (num_requests == 0) return COOP_ORACLE_OK;
+
+    struct fit_job job;
+    job.size = size; job.kind = kind;
+    job.seg_offsets = seg_offsets; job.req_sizes = req_sizes;
+    job.req_offsets = req_offsets; job.num_segments = num_segments;
+    job.num_requests = num_requests; job.out = out;
+    atomic_init(&job.next, 0);
+
+    if (num_threads <= 1) {
+        fit_worker(&job);
+        return COOP_ORACLE_OK;
+    }
+    pthread_t *tid = (pthread_t *)calloc((size_t)num_threads, sizeof(pthread_t));
+    if (!tid) return COOP_ORACLE_ERR_INVALID;
+    int started = 0;
+    for (int t = 0; t < num_threads; ++t) {
+        if (pthread_create(&tid[t], NULL, fit_worker, &job) != 0) break;
+        ++started;
+    }
+    if (started == 0) fit_worker(&job);
+    for (int t = 0; t < started; ++t) pthread_join(tid[t], NULL);
+    free(tid);
+    return COOP_ORACLE_OK;
+}
