@@ -135,6 +135,31 @@ coop_status_t coop_window_search(const uint64_t *size, const uint64_t *cost,
                                  uint64_t num_requests, coop_window_t *out,
                                  void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * First fit (section 2.4; Algorithm 1's find_free_block_not_less_than, the
+ * step before any eviction): for every request of S bytes, the leftmost free
+ * chunk (kind == COOP_FREE) of its snapshot holding at least S bytes, where
+ * a first-fit allocator places the tensor.  Evictable and pinned blocks are
+ * occupied whatever their size.  S == 0 takes the first free chunk.
+ *
+ * Same batch layout as coop_window_search (cost is not needed); out
+ * (device) receives num_requests snapshot-local block indices, ~0 where the
+ * snapshot has no such chunk.  workspace (device, caller-owned, contents
+ * need not be initialised) holds per-group and per-tile summaries of the
+ * free chunk sizes: coop_first_fit_workspace_size() bytes, which depend on
+ * num_blocks only (0 for an empty batch; workspace may then be NULL).  Two
+ * launches are enqueued on `stream`; nothing is allocated or synchronised.
+ * Status codes and unchecked device preconditions as for
+ * coop_window_search.
+ */
+coop_status_t coop_first_fit_workspace_size(uint64_t num_blocks, size_t *bytes_out);
+
+coop_status_t coop_first_fit(const uint64_t *size, const uint8_t *kind, uint64_t num_blocks,
+                             const uint64_t *seg_offsets, uint64_t num_segments,
+                             const uint64_t *req_sizes, const uint64_t *req_offsets,
+                             uint64_t num_requests, uint64_t *out,
+                             void *workspace, size_t workspace_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

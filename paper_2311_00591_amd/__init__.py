@@ -62,6 +62,10 @@ def load_library():
     lib.coop_window_search_plan.argtypes = [u64, u64, u64, ctypes.POINTER(CoopPlan)]
     lib.coop_window_search_plan.restype = ctypes.c_int
     lib.coop_window_search.argtypes = [vp, vp, vp, u64, vp, u64, vp, vp, u64, vp, vp, sz, vp]
+    lib.coop_first_fit_workspace_size.argtypes = [u64, ctypes.POINTER(sz)]
+    lib.coop_first_fit_workspace_size.restype = ctypes.c_int
+    lib.coop_first_fit.argtypes = [vp, vp, u64, vp, u64, vp, vp, u64, vp, vp, sz, vp]
+    lib.coop_first_fit.restype = ctypes.c_int
     lib.coop_window_search.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -169,6 +173,72 @@ def window_search(size, cost, kind, seg_offsets, req_sizes, req_offsets, *,
     return ws(stream)
 
 
+def first_fit_workspace_size(num_blocks: int) -> int:
+    """Device workspace bytes coop_first_fit needs for num_blocks blocks."""
+    out = ctypes.c_size_t(0)
+    _check(load_library().coop_first_fit_workspace_size(int(num_blocks), ctypes.byref(out)))
+    return out.value
+
+
+class FirstFit:
+    """A prepared first-fit call (coop_first_fit) for fixed device tensors:
+    for every request, the snapshot-local index of the leftmost free chunk of
+    at least S bytes, -1 (2**64-1 as uint64) where there is none."""
+
+    def __init__(self, size, kind, seg_offsets, req_sizes, req_offsets,
+                 out: Optional[torch.Tensor] = None,
+                 workspace: Optional[torch.Tensor] = None):
+        device = size.device
+        if device.type != "cuda":
+            raise ValueError("coop first fit runs on the GPU; tensors are on "
+                             f"{device} (there is no CPU fallback)")
+        lib = load_library()
+        self.size = _u64_tensor(size, "size", device)
+        if kind.dtype != torch.uint8 or kind.device != device or not kind.is_contiguous():
+            raise TypeError("kind must be a contiguous uint8 tensor on the same device")
+        self.kind = kind
+        self.seg_offsets = _u64_tensor(seg_offsets, "seg_offsets", device)
+        self.req_sizes = _u64_tensor(req_sizes, "req_sizes", device)
+        self.req_offsets = _u64_tensor(req_offsets, "req_offsets", device)
+        n, b1, q = size.numel(), seg_offsets.numel(), req_sizes.numel()
+        if kind.numel() != n:
+            raise ValueError("size and kind must have the same length")
+        if b1 < 1 or req_offsets.numel() != b1:
+            raise ValueError("seg_offsets and req_offsets need num_segments + 1 entries")
+        if out is None:
+            out = torch.empty(q, dtype=torch.int64, device=device)
+        if out.shape != (q,) or out.dtype != torch.int64 or not out.is_contiguous():
+            raise ValueError("out must be a contiguous int64 (Q,) tensor")
+        self.out = out
+        need = first_fit_workspace_size(n)
+        if workspace is None:
+            workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+        if workspace.numel() * workspace.element_size() < need:
+            raise ValueError(f"workspace holds {workspace.numel()} bytes, needs {need}")
+        self.workspace = workspace
+        self._fn = lib.coop_first_fit
+        self._args = (_ptr(self.size), _ptr(self.kind), n, _ptr(self.seg_offsets), b1 - 1,
+                      _ptr(self.req_sizes), _ptr(self.req_offsets), q, _ptr(self.out),
+                      _ptr(self.workspace), workspace.numel() * workspace.element_size())
+
+    def launch(self, stream: Optional[int] = None) -> None:
+        if stream is None:
+            stream = torch.cuda.current_stream(self.size.device).cuda_stream
+        _check(self._fn(*self._args, stream))
+
+    def __call__(self, stream: Optional[int] = None) -> torch.Tensor:
+        self.launch(stream)
+        return self.out
+
+
+def first_fit(size, kind, seg_offsets, req_sizes, req_offsets, *,
+              out: Optional[torch.Tensor] = None,
+              workspace: Optional[torch.Tensor] = None,
+              stream: Optional[int] = None) -> torch.Tensor:
+    """One batched first fit on device tensors; returns int64 (Q,)."""
+    return FirstFit(size, kind, seg_offsets, req_sizes, req_offsets, out, workspace)(stream)
+
+
 def to_device(pools, device="cuda"):
     """Moves a host batch (numpy arrays, e.g. workloads.Pools) to the GPU as
     the tensors window_search takes."""
@@ -182,6 +252,6 @@ def to_device(pools, device="cuda"):
             u64(pools.seg_offsets), u64(pools.req_sizes), u64(pools.req_offsets))
 
 
-__all__ = ["COOP_EVICTABLE", "COOP_FREE", "COOP_PINNED", "CoopError", "INFEASIBLE",
-           "LIBRARY", "WindowSearch", "load_library", "to_device", "window_search",
-           "workspace_size"]
+__all__ = ["COOP_EVICTABLE", "COOP_FREE", "COOP_PINNED", "CoopError", "FirstFit",
+           "INFEASIBLE", "LIBRARY", "WindowSearch", "first_fit", "first_fit_workspace_size",
+           "load_library", "plan_info", "to_device", "window_search", "workspace_size"]
