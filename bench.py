@@ -1,7 +1,8 @@
 """Benchmark of the batched sliding-window eviction search on one MI355X.
 
 A step is one coop_window_search call: every request of one batch of
-synthetic pool snapshots, inputs already resident in HBM.  The default
+synthetic pool snapshots, inputs already resident in HBM (--op first_fit:
+one coop_first_fit call on the same batch instead).  The default
 workload is the batched mid-pool batch (1024 snapshots x 4096 blocks, one
 request each).  To measure HBM rather than the 256 MB Infinity Cache, the
 batch is replicated into enough distinct device buffers that consecutive
@@ -27,6 +28,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "eviction-window queries/sec and blocks scanned/sec; % of HBM roofline"
+FIT_METRIC = "first-fit queries/sec; % of HBM roofline"
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E, published
 INFINITY_CACHE_BYTES = 256 << 20
 KERNEL = "coop_window_search_kernel"
@@ -45,6 +47,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=5.0,
                     help="target duration of the CPU-oracle baseline (0 disables it)")
     ap.add_argument("--no-parity", action="store_true")
+    ap.add_argument("--op", choices=["window", "first_fit"], default="window",
+                    help="window: the eviction-window search; first_fit: the free-chunk "
+                         "lookup that precedes it")
     return ap.parse_args()
 
 
@@ -59,9 +64,19 @@ def workload_bytes(pools):
         17 * pools.num_blocks + 32 * pools.num_requests
 
 
-def source_digest():
+FIT_SOURCE = os.path.join(ROOT, "paper_2311_00591_amd", "csrc", "coop_first_fit.hip")
+
+
+def fit_bytes(pools):
+    """Algorithmic bytes of one batched first fit: size (8 B) and kind (1 B)
+    of every block once, whatever the number of requests, plus S (8 B) and
+    the 8-byte result per request."""
+    return 9 * pools.num_blocks + 16 * pools.num_requests
+
+
+def source_digest(source=None):
     h = hashlib.sha256()
-    for p in (KERNEL_SOURCE, os.path.join(ROOT, "include", "coop.h")):
+    for p in (source or KERNEL_SOURCE, os.path.join(ROOT, "include", "coop.h")):
         with open(p, "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -81,26 +96,31 @@ def measured_traffic(workload_name):
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(pools, target_s):
+def cpu_baseline(pools, target_s, op="window"):
     import oracle
     try:
         threads = len(os.sched_getaffinity(0))
     except AttributeError:
         threads = os.cpu_count() or 1
     threads = max(1, min(threads, 64))
-    args = pools.arrays()
+    if op == "window":
+        args = pools.arrays()
+        fn, what = oracle.window_search, "two-pointer sweep"
+    else:
+        args = (pools.size, pools.kind, pools.seg_offsets, pools.req_sizes, pools.req_offsets)
+        fn, what = oracle.first_fit, "left-to-right walk per request"
     t0 = time.perf_counter()
-    oracle.window_search(*args, threads=threads)
+    fn(*args, threads=threads)
     one = time.perf_counter() - t0
     reps = max(1, min(1000, int(target_s / max(one, 1e-6))))
     t0 = time.perf_counter()
     for _ in range(reps):
-        oracle.window_search(*args, threads=threads)
+        fn(*args, threads=threads)
     dt = time.perf_counter() - t0
     return {"value": reps * pools.num_requests / dt, "unit": "queries/s", "cores": threads,
             "kind": "oracle",
             "sample": f"whole workload ({pools.num_requests} requests) x {reps} passes, "
-                      f"{dt:.1f} s, two-pointer sweep, {threads} threads"}
+                      f"{dt:.1f} s, {what}, {threads} threads"}
 
 
 def main():
@@ -123,6 +143,8 @@ def main():
 
     spec = workloads.CONFIGS[args.config]
     pools = workloads.make_config(args.config, args.seed)
+    if args.op == "first_fit":
+        return bench_first_fit(args, pools, spec, dev)
     block_queries, alg_bytes, unique_bytes = workload_bytes(pools)
     batch_dev_bytes = 17 * pools.num_blocks + 16 * pools.num_segments + 8 * pools.num_requests
     copies = args.copies or max(1, -(-2 * INFINITY_CACHE_BYTES // batch_dev_bytes) + 1)
@@ -209,6 +231,94 @@ def main():
         "parity_vs_oracle": parity,
         "wall_s_timed_region": wall,
         "kernel_source": source_digest(),
+    }
+    print(json.dumps(rec), flush=True)
+
+
+def bench_first_fit(args, pools, spec, dev):
+    import torch
+
+    import paper_2311_00591_amd as coop
+
+    alg_bytes = fit_bytes(pools)
+    batch_dev_bytes = 9 * pools.num_blocks + 16 * pools.num_segments + 8 * pools.num_requests
+    copies = args.copies or max(1, -(-2 * INFINITY_CACHE_BYTES // batch_dev_bytes) + 1)
+    size, _, kind, seg, req, roff = coop.to_device(pools, dev)
+    out = torch.empty(pools.num_requests, dtype=torch.int64, device=dev)
+    workspace = torch.empty(max(coop.first_fit_workspace_size(pools.num_blocks), 1),
+                            dtype=torch.uint8, device=dev)
+    calls = []
+    for c in range(copies):
+        t = (size, kind) if c == 0 else (size.clone(), kind.clone())
+        calls.append(coop.FirstFit(*t, seg, req, roff, out=out, workspace=workspace))
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    sh = stream.cuda_stream
+    parity = None
+    if not args.no_parity:
+        import oracle
+        calls[0].launch(sh)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy().view(np.uint64)
+        want = oracle.first_fit(pools.size, pools.kind, pools.seg_offsets, pools.req_sizes,
+                                pools.req_offsets, threads=16)
+        parity = bool(np.array_equal(got, want))
+    for i in range(args.warmup):
+        calls[i % copies].launch(sh)
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    w0 = time.perf_counter()
+    start.record(stream)
+    for i in range(args.steps):
+        calls[i % copies].launch(sh)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms = start.elapsed_time(stop) / args.steps
+    t = ms / 1e3
+    achieved = alg_bytes / t / 1e9
+    cpu = cpu_baseline(pools, args.cpu_seconds, "first_fit") if args.cpu_seconds > 0 else None
+    nb = np.diff(pools.seg_offsets.astype(np.int64))
+    rec = {
+        "metric": FIT_METRIC,
+        "value": pools.num_requests / t,
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u64",
+        "data": "synthetic",
+        "config": {
+            "workload": f"first fit on {spec.name}: B={pools.num_segments} snapshots, "
+                        f"N_b={int(nb.min())}..{int(nb.max())} blocks, "
+                        f"{pools.num_requests} requests (standard workload {args.config})",
+            "num_segments": pools.num_segments,
+            "num_blocks": pools.num_blocks,
+            "num_requests": pools.num_requests,
+            "seed": args.seed,
+            "input_sha256": pools.digest()[:16],
+            "resident_copies": copies,
+            "cache": "cold" if copies > 1 else "warm",
+        },
+        "hbm_roofline_pct": 100.0 * achieved / PEAK_HBM_GBS,
+        "roofline": {
+            "kernel": "first_fit_summary_kernel + first_fit_search_kernel (one call)",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": achieved / PEAK_HBM_GBS,
+            "traffic": None,
+            "algorithmic_bytes_per_launch": alg_bytes,
+        },
+        "cpu_baseline": cpu,
+        "parity_vs_oracle": parity,
+        "wall_s_timed_region": wall,
+        "kernel_source": source_digest(FIT_SOURCE),
     }
     print(json.dumps(rec), flush=True)
 

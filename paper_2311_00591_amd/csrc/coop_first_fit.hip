@@ -14,13 +14,14 @@
 //     chunk).  Groups and tiles are aligned to the array, not to snapshots.
 //  2. Search: one wavefront per request walks its snapshot from the left.
 //     Where whole tiles (then whole groups) fit inside what is left of the
-//     snapshot, 64 of their keys are tested at once against key(S); the
-//     first one that passes is entered one level down, and inside a group
-//     the 64 blocks are tested exactly.  A key passes whenever its entry
-//     holds a fit; the saturation lets it pass without a fit only for
-//     S = 2^64 - 1 and a chunk of 2^64 - 2 bytes, and then the walk simply
-//     continues after that entry.  Everything left of the walk's position
-//     is known to hold no fit, so the first exact hit is the answer.
+//     snapshot, 512 tile keys (64 group keys) are tested at once against
+//     key(S); the first one that passes is entered one level down, and
+//     inside a group the 64 blocks are tested exactly.  A key passes
+//     whenever its entry holds a fit; the saturation lets it pass without a
+//     fit only for S = 2^64 - 1 and a chunk of 2^64 - 2 bytes, and then the
+//     walk simply continues after that entry.  Everything left of the walk's
+//     position is known to hold no fit, so the first exact hit is the
+//     answer.
 
 #include <hip/hip_runtime.h>
 
@@ -39,6 +40,7 @@ constexpr uint64_t kTile = 1ull << kTileLog2;
 static_assert(kTile == kThreads * kItems, "a tile is one workgroup's blocks");
 static_assert(kGroup == 8 * kItems, "a group is eight threads' blocks");
 constexpr uint32_t kSearchWaves = 4;      // requests per search workgroup
+constexpr uint32_t kTilesPerLane = 8;     // tile summaries one lane tests per step
 constexpr uint64_t kMaxSummaryWGs = 1ull << 20;
 constexpr uint64_t kMaxSearchWGs = 1ull << 18;
 constexpr uint64_t kNone = ~0ull;
@@ -62,7 +64,8 @@ __global__ __launch_bounds__(kThreads) void first_fit_summary_kernel(
     __shared__ uint64_t wave_max[kThreads / 64];
     const uint32_t tid = threadIdx.x, lane = tid & 63u, w = tid >> 6;
     const uint64_t tiles = (n + kTile - 1) >> kTileLog2;
-    const bool aligned = ((reinterpret_cast<uintptr_t>(size) & 15u) | (reinterpret_cast<uintptr_t>(kind) & 7u)) == 0;
+    const bool aligned =
+        ((reinterpret_cast<uintptr_t>(size) & 15u) | (reinterpret_cast<uintptr_t>(kind) & 7u)) == 0;
     for (uint64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
         const uint64_t k0 = (tile << kTileLog2) + tid * kItems;
         uint64_t m = 0;
@@ -145,12 +148,21 @@ __global__ __launch_bounds__(64 * kSearchWaves) void first_fit_search_kernel(
                 top = 2;
             }
             if (top == 2 && (pos & (kTile - 1)) == 0 && pos + kTile <= lim) {
+                // kTilesPerLane consecutive tiles per lane: a long run of
+                // tiles without a fit goes by 512 tiles a step
                 const uint64_t t0 = pos >> kTileLog2;
-                const uint64_t tl = lim >> kTileLog2, tn = tl < t0 + 64 ? tl : t0 + 64;
-                const uint64_t t = t0 + lane;
-                const uint64_t m = __ballot(t < tn && g2[t] >= T);
+                const uint64_t span = 64 * kTilesPerLane;
+                const uint64_t tl = lim >> kTileLog2, tn = tl < t0 + span ? tl : t0 + span;
+                const uint64_t tb = t0 + lane * kTilesPerLane;
+                uint32_t jf = kTilesPerLane;
+#pragma unroll
+                for (uint32_t j = kTilesPerLane; j-- > 0;)
+                    if (tb + j < tn && g2[tb + j] >= T) jf = j;
+                const uint64_t m = __ballot(jf < kTilesPerLane);
                 if (m) {
-                    pos = (t0 + __builtin_ctzll(m)) << kTileLog2;
+                    const uint32_t f = static_cast<uint32_t>(__builtin_ctzll(m));
+                    const uint32_t j = __builtin_amdgcn_readlane(jf, f);
+                    pos = (t0 + f * kTilesPerLane + j) << kTileLog2;
                     lim = pos + kTile;
                     top = 1;
                 } else {
