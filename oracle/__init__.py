@@ -133,3 +133,52 @@ def first_fit(size, kind, seg_offsets, req_sizes, req_offsets, threads=1):
     if rc != 0:
         raise OracleError(rc)
     return out
+
+
+def replay(state, trace, threads=1):
+    """Algorithm 1 replayed on independent pools (see coop_oracle.h).
+
+    state: dict of numpy arrays size/cost (uint64, num_pools * capacity),
+    kind (uint8), id (uint32), len (uint64, num_pools), and 'capacity';
+    trace: dict op (uint8), op_id (uint32), op_size/op_cost (uint64),
+    op_flags (uint8), each num_pools * num_ops.  Returns (new_state,
+    outputs) with outputs block (uint64, P x T), window (P x T x 2), cost,
+    free (P x T)."""
+    cap = int(state["capacity"])
+    P = len(state["len"])
+    T = len(trace["op"]) // max(P, 1)
+    st = {k: np.array(state[k], copy=True) for k in ("size", "cost", "kind", "id", "len")}
+    st["size"] = _u64(st["size"]); st["cost"] = _u64(st["cost"]); st["len"] = _u64(st["len"])
+    st["kind"] = np.ascontiguousarray(st["kind"], dtype=np.uint8)
+    st["id"] = np.ascontiguousarray(st["id"], dtype=np.uint32)
+    st["capacity"] = cap
+    tr = {"op": np.ascontiguousarray(trace["op"], dtype=np.uint8),
+          "op_id": np.ascontiguousarray(trace["op_id"], dtype=np.uint32),
+          "op_size": _u64(trace["op_size"]), "op_cost": _u64(trace["op_cost"]),
+          "op_flags": np.ascontiguousarray(trace["op_flags"], dtype=np.uint8)}
+    if any(len(v) != P * T for v in tr.values()) or len(st["size"]) != P * cap:
+        raise ValueError("inconsistent replay array lengths")
+    out_block = np.empty(P * T, dtype=np.uint64)
+    out_window = np.empty(2 * P * T, dtype=np.uint64)
+    out_cost = np.empty(P * T, dtype=np.uint64)
+    out_free = np.empty(P * T, dtype=np.uint64)
+    lib = _load()
+    p64, p8, p32 = (ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_uint8),
+                    ctypes.POINTER(ctypes.c_uint32))
+    lib.coop_oracle_replay.argtypes = [p64, p64, p8, p32, p64, ctypes.c_uint64, ctypes.c_uint64,
+                                       p8, p32, p64, p64, p8, ctypes.c_uint64, p64, p64, p64, p64,
+                                       ctypes.c_int]
+    lib.coop_oracle_replay.restype = ctypes.c_int
+    rc = lib.coop_oracle_replay(
+        _ptr(st["size"], ctypes.c_uint64), _ptr(st["cost"], ctypes.c_uint64),
+        _ptr(st["kind"], ctypes.c_uint8), _ptr(st["id"], ctypes.c_uint32),
+        _ptr(st["len"], ctypes.c_uint64), P, cap, _ptr(tr["op"], ctypes.c_uint8),
+        _ptr(tr["op_id"], ctypes.c_uint32), _ptr(tr["op_size"], ctypes.c_uint64),
+        _ptr(tr["op_cost"], ctypes.c_uint64), _ptr(tr["op_flags"], ctypes.c_uint8), T,
+        _ptr(out_block, ctypes.c_uint64), _ptr(out_window, ctypes.c_uint64),
+        _ptr(out_cost, ctypes.c_uint64), _ptr(out_free, ctypes.c_uint64), int(threads))
+    if rc != 0:
+        raise OracleError(rc)
+    outs = {"block": out_block.reshape(P, T), "window": out_window.reshape(P, T, 2),
+            "cost": out_cost.reshape(P, T), "free": out_free.reshape(P, T)}
+    return st, outs

@@ -386,3 +386,202 @@ int coop_oracle_first_fit(const uint64_t *size, const uint8_t *kind, uint64_t nu
     free(tid);
     return COOP_ORACLE_OK;
 }
+
+/* ---------------------------------------------------------------------------
+ * Replay of Algorithm 1 on independent pools.  A pool is its address-sorted
+ * block list, holding a fixed number of bytes; no two free chunks are ever
+ * adjacent (section 2.4: a released chunk merges with its free neighbours).
+ * Each operation of a pool's trace is applied in order:
+ *
+ *   allocate(id, S, flags): first fit; if no free chunk holds S bytes, the
+ *     sliding-window search for S (section 3.3), the window's evictable
+ *     tensors are evicted and the whole window becomes one free chunk, merged
+ *     with free neighbours, and first fit runs again (Algorithm 1).  The
+ *     tensor goes to the left end of the chunk when the operation is
+ *     expensive and to the right end otherwise (section 3.4, applied to
+ *     every placement).  No window: the allocation fails and nothing
+ *     changes.
+ *   release(id): the tensor's block becomes free and merges with free
+ *     neighbours; a tensor that was evicted is already gone (no-op).
+ *
+ * Per operation the replay records the block the tensor went to (or the
+ * merged free chunk of a release; ~0 for a failure or a no-op), the evicted
+ * window [start, end) in pre-eviction indices (~0 when nothing was evicted),
+ * its eviction cost, and, for an eviction, the free bytes of the pool just
+ * before it (the fragmentation-rate sample of section 4.1: free memory over
+ * the memory the allocator holds).
+ * ------------------------------------------------------------------------- */
+#define OP_ALLOC 0
+#define OP_FREE 1
+#define FLAG_LEFT 1u   /* an expensive operation: placed at the left end */
+#define FLAG_PINNED 2u /* an unevictable tensor */
+
+struct replay_pool {
+    uint64_t *size, *cost;
+    uint8_t *kind;
+    uint32_t *id;
+    uint64_t len, cap;
+};
+
+/* Replaces blocks [lo, hi) by the m blocks given (m <= 2). */
+static void pool_replace(struct replay_pool *p, uint64_t lo, uint64_t hi, uint64_t m,
+                         const uint64_t *ns, const uint64_t *nc, const uint8_t *nk,
+                         const uint32_t *ni) {
+    uint64_t tail = p->len - hi;
+    memmove(p->size + lo + m, p->size + hi, tail * sizeof(uint64_t));
+    memmove(p->cost + lo + m, p->cost + hi, tail * sizeof(uint64_t));
+    memmove(p->kind + lo + m, p->kind + hi, tail * sizeof(uint8_t));
+    memmove(p->id + lo + m, p->id + hi, tail * sizeof(uint32_t));
+    for (uint64_t j = 0; j < m; ++j) {
+        p->size[lo + j] = ns[j]; p->cost[lo + j] = nc[j];
+        p->kind[lo + j] = nk[j]; p->id[lo + j] = ni[j];
+    }
+    p->len = p->len - (hi - lo) + m;
+}
+
+/* Turns blocks [lo, hi) into one free chunk merged with free neighbours;
+ * returns its index. */
+static uint64_t pool_free_range(struct replay_pool *p, uint64_t lo, uint64_t hi) {
+    while (lo > 0 && p->kind[lo - 1] == KIND_FREE) --lo;
+    while (hi < p->len && p->kind[hi] == KIND_FREE) ++hi;
+    uint64_t total = 0;
+    for (uint64_t k = lo; k < hi; ++k) total += p->size[k];
+    uint64_t s = total, c = 0;
+    uint8_t kd = KIND_FREE;
+    uint32_t i = 0;
+    pool_replace(p, lo, hi, 1, &s, &c, &kd, &i);
+    return lo;
+}
+
+static int replay_one(struct replay_pool *p, const uint8_t *op, const uint32_t *op_id,
+                      const uint64_t *op_size, const uint64_t *op_cost, const uint8_t *op_flags,
+                      uint64_t num_ops, uint64_t *out_block, uint64_t *out_window,
+                      uint64_t *out_cost, uint64_t *out_free) {
+    for (uint64_t t = 0; t < num_ops; ++t) {
+        out_block[t] = NONE;
+        out_window[2 * t] = out_window[2 * t + 1] = NONE;
+        out_cost[t] = 0;
+        out_free[t] = NONE;
+        if (op[t] == OP_FREE) {
+            for (uint64_t k = 0; k < p->len; ++k) {
+                if (p->kind[k] != KIND_FREE && p->id[k] == op_id[t]) {
+                    out_block[t] = pool_free_range(p, k, k + 1);
+                    break;
+                }
+            }
+            continue;
+        }
+        if (op[t] != OP_ALLOC || op_size[t] == 0 || op_id[t] == 0)
+            return COOP_ORACLE_ERR_INVALID;
+        const uint64_t S = op_size[t];
+        uint64_t k = first_fit_one(p->size, p->kind, p->len, S);
+        if (k == NONE) {
+            uint64_t win[3];
+            if (!runs_fit(p->size, p->cost, p->kind, p->len)) return COOP_ORACLE_ERR_OVERFLOW;
+            sweep_one(p->size, p->cost, p->kind, p->len, S, win);
+            if (win[0] == NONE) continue; /* the allocation fails */
+            uint64_t free_bytes = 0;
+            for (uint64_t j = 0; j < p->len; ++j)
+                if (p->kind[j] == KIND_FREE) free_bytes += p->size[j];
+            out_free[t] = free_bytes;
+            out_window[2 * t] = win[0];
+            out_window[2 * t + 1] = win[1];
+            out_cost[t] = win[2];
+            pool_free_range(p, win[0], win[1]);
+            k = first_fit_one(p->size, p->kind, p->len, S);
+            if (k == NONE) return COOP_ORACLE_ERR_INVALID; /* cannot happen */
+        }
+        if (p->len + 1 > p->cap) return COOP_ORACLE_ERR_TOO_LARGE;
+        const uint64_t F = p->size[k];
+        const uint8_t tk = (op_flags[t] & FLAG_PINNED) ? 2 : KIND_EVICTABLE;
+        uint64_t ns[2], nc[2];
+        uint8_t nk[2];
+        uint32_t ni[2];
+        uint64_t m = 1, at = k;
+        if (F == S) {
+            ns[0] = S; nc[0] = op_cost[t]; nk[0] = tk; ni[0] = op_id[t];
+        } else if (op_flags[t] & FLAG_LEFT) {
+            ns[0] = S; nc[0] = op_cost[t]; nk[0] = tk; ni[0] = op_id[t];
+            ns[1] = F - S; nc[1] = 0; nk[1] = KIND_FREE; ni[1] = 0;
+            m = 2;
+        } else {
+            ns[0] = F - S; nc[0] = 0; nk[0] = KIND_FREE; ni[0] = 0;
+            ns[1] = S; nc[1] = op_cost[t]; nk[1] = tk; ni[1] = op_id[t];
+            m = 2;
+            at = k + 1;
+        }
+        pool_replace(p, k, k + 1, m, ns, nc, nk, ni);
+        out_block[t] = at;
+    }
+    return COOP_ORACLE_OK;
+}
+
+struct replay_job {
+    uint64_t *size, *cost;
+    uint8_t *kind;
+    uint32_t *id;
+    uint64_t *len;
+    uint64_t cap, num_pools, num_ops;
+    const uint8_t *op;
+    const uint32_t *op_id;
+    const uint64_t *op_size, *op_cost;
+    const uint8_t *op_flags;
+    uint64_t *out_block, *out_window, *out_cost, *out_free;
+    _Atomic uint64_t next;
+    _Atomic int status;
+};
+
+static void *replay_worker(void *arg) {
+    struct replay_job *j = (struct replay_job *)arg;
+    for (;;) {
+        uint64_t b = atomic_fetch_add(&j->next, 1);
+        if (b >= j->num_pools) break;
+        struct replay_pool p = {j->size + b * j->cap, j->cost + b * j->cap, j->kind + b * j->cap,
+                                j->id + b * j->cap, j->len[b], j->cap};
+        const uint64_t o = b * j->num_ops;
+        int rc = replay_one(&p, j->op + o, j->op_id + o, j->op_size + o, j->op_cost + o,
+                            j->op_flags + o, j->num_ops, j->out_block + o, j->out_window + 2 * o,
+                            j->out_cost + o, j->out_free + o);
+        j->len[b] = p.len;
+        if (rc != COOP_ORACLE_OK) atomic_store(&j->status, rc);
+    }
+    return NULL;
+}
+
+int coop_oracle_replay(uint64_t *size, uint64_t *cost, uint8_t *kind, uint32_t *id, uint64_t *len,
+                       uint64_t num_pools, uint64_t capacity, const uint8_t *op,
+                       const uint32_t *op_id, const uint64_t *op_size, const uint64_t *op_cost,
+                       const uint8_t *op_flags, uint64_t num_ops, uint64_t *out_block,
+                       uint64_t *out_window, uint64_t *out_cost, uint64_t *out_free,
+                       int num_threads) {
+    if (num_pools == 0) return COOP_ORACLE_OK;
+    if (!size || !cost || !kind || !id || !len || capacity == 0) return COOP_ORACLE_ERR_INVALID;
+    if (num_ops && (!op || !op_id || !op_size || !op_cost || !op_flags || !out_block ||
+                    !out_window || !out_cost || !out_free))
+        return COOP_ORACLE_ERR_INVALID;
+    for (uint64_t b = 0; b < num_pools; ++b)
+        if (len[b] > capacity) return COOP_ORACLE_ERR_INVALID;
+    struct replay_job job;
+    job.size = size; job.cost = cost; job.kind = kind; job.id = id; job.len = len;
+    job.cap = capacity; job.num_pools = num_pools; job.num_ops = num_ops;
+    job.op = op; job.op_id = op_id; job.op_size = op_size; job.op_cost = op_cost;
+    job.op_flags = op_flags; job.out_block = out_block; job.out_window = out_window;
+    job.out_cost = out_cost; job.out_free = out_free;
+    atomic_init(&job.next, 0);
+    atomic_init(&job.status, COOP_ORACLE_OK);
+    if (num_threads <= 1) {
+        replay_worker(&job);
+        return atomic_load(&job.status);
+    }
+    pthread_t *tid = (pthread_t *)calloc((size_t)num_threads, sizeof(pthread_t));
+    if (!tid) return COOP_ORACLE_ERR_INVALID;
+    int started = 0;
+    for (int t = 0; t < num_threads; ++t) {
+        if (pthread_create(&tid[t], NULL, replay_worker, &job) != 0) break;
+        ++started;
+    }
+    if (started == 0) replay_worker(&job);
+    for (int t = 0; t < started; ++t) pthread_join(tid[t], NULL);
+    free(tid);
+    return atomic_load(&job.status);
+}

@@ -92,6 +92,27 @@ int coop_oracle_first_fit(const uint64_t *size, const uint8_t *kind, uint64_t nu
                           const uint64_t *req_sizes, const uint64_t *req_offsets,
                           uint64_t num_requests, uint64_t *out, int num_threads);
 
+/* Replay of Algorithm 1 (allocate: first fit, else evict the sliding
+ * window's tensors, merge the window into one free chunk and fit again;
+ * expensive operations placed at the left end of the chunk, others at the
+ * right end as in section 3.4) and of releases, on num_pools independent
+ * pools.  Pool b occupies slots [b * capacity, (b + 1) * capacity) of
+ * size/cost/kind/id (tensor ids, 0 for free chunks); len[b] blocks are in
+ * use.  All are updated in place.  Operations: num_ops per pool, pool b's at
+ * [b * num_ops, (b + 1) * num_ops): op 0 = allocate(op_id, op_size,
+ * op_cost, op_flags: 1 expensive, 2 unevictable), op 1 = release(op_id).
+ * Outputs per operation: out_block (the tensor's block, the merged free
+ * chunk of a release, ~0 for a failed allocation or a release of an evicted
+ * tensor), out_window[2] (evicted window, pre-eviction indices, or ~0),
+ * out_cost (its eviction cost), out_free (free bytes just before an
+ * eviction, else ~0).  Returns -5 if a pool would exceed its capacity. */
+int coop_oracle_replay(uint64_t *size, uint64_t *cost, uint8_t *kind, uint32_t *id, uint64_t *len,
+                       uint64_t num_pools, uint64_t capacity, const uint8_t *op,
+                       const uint32_t *op_id, const uint64_t *op_size, const uint64_t *op_cost,
+                       const uint8_t *op_flags, uint64_t num_ops, uint64_t *out_block,
+                       uint64_t *out_window, uint64_t *out_cost, uint64_t *out_free,
+                       int num_threads);
+
 #ifdef __cplusplus
 }
 #endif
