@@ -160,6 +160,48 @@ coop_status_t coop_first_fit(const uint64_t *size, const uint8_t *kind, uint64_t
                              uint64_t num_requests, uint64_t *out,
                              void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * Replay of Algorithm 1 on num_pools independent pools, all in lockstep.
+ * For every operation of a pool's trace, in order: an allocation runs first
+ * fit; when no free chunk holds S bytes, the sliding-window search for S,
+ * evicts the window's tensors, merges the window and its free neighbours
+ * into one free chunk and fits again; the tensor goes to the chunk's left
+ * end when the operation is expensive and to its right end otherwise
+ * (section 3.4).  With no window the allocation fails and nothing changes.
+ * A release frees the tensor's block and merges it with free neighbours; a
+ * tensor already evicted is skipped.
+ *
+ * Pools (device, updated in place): pool b occupies slots
+ *   [b * capacity, (b + 1) * capacity) of size, cost (u64), kind (u8) and id
+ *   (u32 tensor ids, 0 for free chunks); len[b] (u64) blocks are in use,
+ *   never two free chunks side by side, and unused slots must hold empty
+ *   pinned blocks (size 0, kind COOP_PINNED), which the replay keeps so.
+ * Operations (device): num_ops per pool, pool b's at [b * num_ops, +num_ops):
+ *   op 0 allocate (op_id != 0, op_size > 0, op_cost, op_flags bit 0
+ *   expensive, bit 1 unevictable tensor), op 1 release op_id.
+ * Outputs (device), per operation: out_block (the tensor's block, or the
+ *   merged free chunk of a release; ~0 for a failed allocation or a
+ *   skipped release), out_window[2] (the evicted window, indices before the
+ *   eviction, or ~0), out_cost (its eviction cost), out_free (free bytes
+ *   just before an eviction, else ~0: the fragmentation-rate sample of
+ *   section 4.1, free memory over the memory the allocator holds).
+ * status (device u32): set to 0, then bit 0 if a pool ran out of slots (that
+ *   allocation is skipped), bit 1 for an invalid operation.
+ * workspace: coop_replay_workspace_size() bytes (device, caller-owned).
+ * Enqueues 4 + 5 * num_ops launches on `stream`; nothing is allocated or
+ * synchronised.
+ */
+coop_status_t coop_replay_workspace_size(uint64_t num_pools, uint64_t capacity,
+                                         size_t *bytes_out);
+
+coop_status_t coop_replay(uint64_t *size, uint64_t *cost, uint8_t *kind, uint32_t *id,
+                          uint64_t *len, uint64_t num_pools, uint64_t capacity,
+                          const uint8_t *op, const uint32_t *op_id, const uint64_t *op_size,
+                          const uint64_t *op_cost, const uint8_t *op_flags, uint64_t num_ops,
+                          uint64_t *out_block, uint64_t *out_window, uint64_t *out_cost,
+                          uint64_t *out_free, uint32_t *status, void *workspace,
+                          size_t workspace_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

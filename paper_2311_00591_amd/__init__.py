@@ -66,6 +66,11 @@ def load_library():
     lib.coop_first_fit_workspace_size.restype = ctypes.c_int
     lib.coop_first_fit.argtypes = [vp, vp, u64, vp, u64, vp, vp, u64, vp, vp, sz, vp]
     lib.coop_first_fit.restype = ctypes.c_int
+    lib.coop_replay_workspace_size.argtypes = [u64, u64, ctypes.POINTER(sz)]
+    lib.coop_replay_workspace_size.restype = ctypes.c_int
+    lib.coop_replay.argtypes = [vp, vp, vp, vp, vp, u64, u64, vp, vp, vp, vp, vp, u64, vp, vp,
+                                vp, vp, vp, vp, sz, vp]
+    lib.coop_replay.restype = ctypes.c_int
     lib.coop_window_search.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -239,6 +244,89 @@ def first_fit(size, kind, seg_offsets, req_sizes, req_offsets, *,
     return FirstFit(size, kind, seg_offsets, req_sizes, req_offsets, out, workspace)(stream)
 
 
+def replay_workspace_size(num_pools: int, capacity: int) -> int:
+    """Device workspace bytes coop_replay needs."""
+    out = ctypes.c_size_t(0)
+    _check(load_library().coop_replay_workspace_size(int(num_pools), int(capacity),
+                                                     ctypes.byref(out)))
+    return out.value
+
+
+class Replay:
+    """A prepared coop_replay call: Algorithm 1 replayed on independent pools
+    held in device tensors (updated in place by every launch).
+
+    state: dict of device tensors size/cost (int64 holding u64, P*cap),
+    kind (uint8), id (int32 holding u32), len (int64, P) and int capacity;
+    trace: dict of device tensors op (uint8), op_id (int32), op_size/op_cost
+    (int64), op_flags (uint8), each P*T.  Outputs: block, cost, free (int64,
+    P*T), window (int64, P*T*2), status (int32, 1)."""
+
+    def __init__(self, state, trace, workspace: Optional[torch.Tensor] = None):
+        dev = state["size"].device
+        if dev.type != "cuda":
+            raise ValueError("coop replay runs on the GPU (there is no CPU fallback)")
+        lib = load_library()
+        self.state, self.trace = state, trace
+        P = state["len"].numel()
+        cap = int(state["capacity"])
+        T = trace["op"].numel() // max(P, 1)
+        for k, dt in (("size", torch.int64), ("cost", torch.int64), ("kind", torch.uint8),
+                      ("id", torch.int32)):
+            t = state[k]
+            if t.dtype != dt or t.numel() != P * cap or not t.is_contiguous() or t.device != dev:
+                raise ValueError(f"state[{k!r}] must be a contiguous {dt} tensor of {P * cap}")
+        for k, dt in (("op", torch.uint8), ("op_id", torch.int32), ("op_size", torch.int64),
+                      ("op_cost", torch.int64), ("op_flags", torch.uint8)):
+            t = trace[k]
+            if t.dtype != dt or t.numel() != P * T or not t.is_contiguous() or t.device != dev:
+                raise ValueError(f"trace[{k!r}] must be a contiguous {dt} tensor of {P * T}")
+        self.num_pools, self.capacity, self.num_ops = P, cap, T
+        self.block = torch.empty(P * T, dtype=torch.int64, device=dev)
+        self.window = torch.empty(P * T * 2, dtype=torch.int64, device=dev)
+        self.cost = torch.empty(P * T, dtype=torch.int64, device=dev)
+        self.free = torch.empty(P * T, dtype=torch.int64, device=dev)
+        self.status = torch.zeros(1, dtype=torch.int32, device=dev)
+        need = replay_workspace_size(P, cap)
+        if workspace is None:
+            workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+        if workspace.numel() * workspace.element_size() < need:
+            raise ValueError(f"workspace holds {workspace.numel()} bytes, needs {need}")
+        self.workspace = workspace
+        self._fn = lib.coop_replay
+        self._args = (state["size"].data_ptr(), state["cost"].data_ptr(), state["kind"].data_ptr(),
+                      state["id"].data_ptr(), state["len"].data_ptr(), P, cap,
+                      trace["op"].data_ptr(), trace["op_id"].data_ptr(),
+                      trace["op_size"].data_ptr(), trace["op_cost"].data_ptr(),
+                      trace["op_flags"].data_ptr(), T, self.block.data_ptr(),
+                      self.window.data_ptr(), self.cost.data_ptr(), self.free.data_ptr(),
+                      self.status.data_ptr(), workspace.data_ptr(),
+                      workspace.numel() * workspace.element_size())
+
+    def launch(self, stream: Optional[int] = None) -> None:
+        if stream is None:
+            stream = torch.cuda.current_stream(self.status.device).cuda_stream
+        _check(self._fn(*self._args, stream))
+
+
+def replay_to_device(state, trace, device="cuda"):
+    """Moves a host replay (numpy, as workloads.traces.generate returns) to the GPU."""
+    import numpy as np
+
+    def t(a, dt, view=None):
+        a = np.ascontiguousarray(a, dtype=dt)
+        return torch.from_numpy(a.view(view) if view else a).to(device)
+
+    st = {"size": t(state["size"], np.uint64, np.int64), "cost": t(state["cost"], np.uint64, np.int64),
+          "kind": t(state["kind"], np.uint8), "id": t(state["id"], np.uint32, np.int32),
+          "len": t(state["len"], np.uint64, np.int64), "capacity": int(state["capacity"])}
+    tr = {"op": t(trace["op"], np.uint8), "op_id": t(trace["op_id"], np.uint32, np.int32),
+          "op_size": t(trace["op_size"], np.uint64, np.int64),
+          "op_cost": t(trace["op_cost"], np.uint64, np.int64),
+          "op_flags": t(trace["op_flags"], np.uint8)}
+    return st, tr
+
+
 def to_device(pools, device="cuda"):
     """Moves a host batch (numpy arrays, e.g. workloads.Pools) to the GPU as
     the tensors window_search takes."""
@@ -253,5 +341,6 @@ def to_device(pools, device="cuda"):
 
 
 __all__ = ["COOP_EVICTABLE", "COOP_FREE", "COOP_PINNED", "CoopError", "FirstFit",
-           "INFEASIBLE", "LIBRARY", "WindowSearch", "first_fit", "first_fit_workspace_size",
-           "load_library", "plan_info", "to_device", "window_search", "workspace_size"]
+           "INFEASIBLE", "LIBRARY", "Replay", "WindowSearch", "first_fit",
+           "first_fit_workspace_size", "load_library", "plan_info", "replay_to_device",
+           "replay_workspace_size", "to_device", "window_search", "workspace_size"]

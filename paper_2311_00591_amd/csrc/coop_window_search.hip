@@ -32,7 +32,7 @@
 //     and cost are P[k] - P[i] and C[k] - C[i]; no reset at pinned blocks is
 //     needed.  The sums run per thread, per wavefront (DPP row shifts and
 //     broadcasts) and across the wavefronts (one barrier).  LDS receives, per
-//     staged boundary k, the key X[k] = R[k] << 51 | P[k] and C[k].  Keys
+//     staged boundary k, the key X[k] = R[k] << 50 | P[k] and C[k].  Keys
 //     increase with k, and for a start i the first end k with X[k] >= X[i] + S
 //     is its shortest window when R[k] == R[i], while no window from i exists
 //     inside the staged region otherwise.
@@ -48,8 +48,8 @@
 //     goes on) are a suffix of the tile, found by one search; the request's
 //     wavefront finishes them by walking the rest of the run 64 blocks at a
 //     time.
-// A tile that holds a block of 2^38 bytes or more keeps plain 64-bit
-// prefixes (P could outgrow the 51-bit field) with the run ids in a separate
+// A tile that holds a block of 2^37 bytes or more keeps plain 64-bit
+// prefixes (P could outgrow the 50-bit field) with the run ids in a separate
 // array, stages no halo, and bisects per start.
 //
 // Combining tiles
@@ -90,13 +90,18 @@ constexpr uint32_t kMaxSteps = ((kTile + kStage + 63) / 64 + 1) / 4 * 4 + 2;
 // positions a lane reads past the starts once they are used up.
 constexpr uint32_t kXN = ((kStage + 2 > kTile + kMaxSteps + 1 ? kStage + 2 : kTile + kMaxSteps + 1) +
                           7) / 8 * 8;
-constexpr uint32_t kValBits = 51;
+constexpr uint32_t kValBits = 50;
 constexpr uint64_t kValMask = (1ull << kValBits) - 1;
-constexpr uint32_t kRunShift = kValBits - 32;  // run id position in the high word of a key
-// With every block below 2^38 bytes, any staged prefix (at most kStage < 2^13
-// blocks) fits the 51-bit field, and no prefix wraps.
-constexpr uint32_t kBigHiLog2 = 38 - 32;
-static_assert(kStage < (1u << (kValBits - 38)), "staged prefixes must fit the key field");
+// With every block below 2^37 bytes, any staged prefix (at most kStage < 2^13
+// blocks) fits the 50-bit field, and no prefix wraps.  Keys then stay below
+// (kStage + 1) << 50 < 2^63, so the difference of two keys is exact as a
+// signed 64-bit number (the merge relies on it).
+constexpr uint32_t kBigHiLog2 = 37 - 32;
+static_assert(kStage < (1u << (kValBits - 37)), "staged prefixes must fit the key field");
+static_assert(kStage + 2 < (1u << (63 - kValBits)), "keys stay below 2^63");
+// The end key after a staged region: above every key and target, and
+// positive as a signed number.
+constexpr uint64_t kEndKey = (1ull << 63) - 1;
 static_assert(kStage < (1u << 16), "pinned counts fit 16 bits");
 constexpr uint64_t kNone = ~0ull;
 constexpr uint32_t kNone32 = ~0u;
@@ -295,7 +300,7 @@ __device__ __forceinline__ void chunk_range(const Params& P, uint64_t c, uint64_
 }
 
 struct Smem {
-    uint64_t x[kXN];    // keys R << 51 | P, or plain P in a tile with a huge block
+    uint64_t x[kXN];    // keys R << 50 | P, or plain P in a tile with a huge block
     uint64_t xc[kXN];   // C
     uint16_t run[kXN];  // R, kept only in a tile with a huge block
     Sums wsum[kWaves];  // per-wavefront totals of the tile
@@ -541,10 +546,13 @@ __device__ __forceinline__ uint32_t merge_steps(uint32_t total, uint32_t lanes) 
 // (starts i < nA) with the end keys X[1..nB]: merge steps [d, d + L).  Ties
 // take the start first, so a start is taken when the head end key is the
 // first one at or above its target: the shortest window from that start that
-// reaches S bytes, valid when both ends have the same run id.  Steps past the
-// lane's slice repeat work of the next lane (harmless: equal windows), and
-// starts past nA are ignored.  X[nB + 1] must be all-ones, which no target
-// exceeds: the end index never passes it.
+// reaches S bytes.  With D = X[k] - X[i] (exact as a signed number, keys
+// being below 2^63), the start is taken iff D >= Sc, and the window is valid
+// iff D < 2^50, i.e. both ends have the same run id; D is then its byte
+// count.  Windows are ranked by (cost, D), which orders them as (cost,
+// bytes - S).  Steps past the lane's slice repeat work of the next lane
+// (harmless: equal windows), and starts past nA are ignored.  X[nB + 1] must
+// be kEndKey, which every target is below: the end index never passes it.
 __device__ __forceinline__ void merge_pass(const Smem& sm, uint32_t nA, uint32_t nB, uint32_t d,
                                            uint32_t L, uint64_t Sc, Cand& best,
                                            uint32_t& best_end) {
@@ -559,22 +567,21 @@ __device__ __forceinline__ void merge_pass(const Smem& sm, uint32_t nA, uint32_t
     }
     uint32_t pA = lo * 8u, pB = (d - lo + 1) * 8u;  // byte offsets of X[a] and of X[b + 1]
     const uint32_t endA = nA * 8u;
-    uint64_t bc = kNone, bx = kNone;
+    const int64_t sc = static_cast<int64_t>(Sc);
+    uint64_t bc = kNone, bd = kNone;
     uint32_t bpa = kNone32, bpb = 0;
     for (uint32_t k = 0; k < L; k += 2) {
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
             const uint64_t xa = lds_u64(sm.x, pA), kb = lds_u64(sm.x, pB);
             const uint64_t ca = lds_u64(sm.xc, pA), cb = lds_u64(sm.xc, pB);
-            const uint64_t ta = xa + Sc;
-            const bool takeA = ta <= kb;
-            const bool same = (static_cast<uint32_t>(xa >> 32) ^ static_cast<uint32_t>(kb >> 32)) <
-                              (1u << kRunShift);
-            const bool valid = takeA & (pA < endA) & same;
-            const uint64_t cost = cb - ca, ex = kb - ta;  // ex = bytes - S
-            const bool better = valid & ((cost < bc) | ((cost == bc) & (ex < bx)));
+            const uint64_t D = kb - xa;
+            const bool takeA = static_cast<int64_t>(D) >= sc;
+            const bool valid = takeA & (pA < endA) & (D < (1ull << kValBits));
+            const uint64_t cost = cb - ca;
+            const bool better = valid & ((cost < bc) | ((cost == bc) & (D < bd)));
             bc = better ? cost : bc;
-            bx = better ? ex : bx;
+            bd = better ? D : bd;
             bpa = better ? pA : bpa;
             bpb = better ? pB : bpb;
             pA += takeA ? 8u : 0u;
@@ -583,7 +590,7 @@ __device__ __forceinline__ void merge_pass(const Smem& sm, uint32_t nA, uint32_t
     }
     // Within a lane starts are met in increasing order, so strict comparison
     // kept the lowest start among equal (cost, bytes).
-    const Cand c{bc, bx, bpa == kNone32 ? kNone32 : bpa / 8u};
+    const Cand c{bc, bpa == kNone32 ? kNone : bd - Sc, bpa == kNone32 ? kNone32 : bpa / 8u};
     if (cand_less(c, best)) {
         best = c;
         best_end = bpb / 8u;
@@ -739,7 +746,7 @@ __device__ void stream_pass(const Params& P, const Smem& sm, uint32_t lane, uint
 
 // What staging left in LDS.
 struct TileState {
-    bool packed;     // keys R << 51 | P; otherwise plain P with R in sm.run
+    bool packed;     // keys R << 50 | P; otherwise plain P with R in sm.run
     uint32_t end;    // staged boundaries [0, end]
     uint32_t endrun; // R at the region end
     uint64_t xend;   // X at the region end
@@ -767,12 +774,12 @@ __device__ __forceinline__ void wave_inclusive_sum2(Sums& s) {
 }
 
 // Stages a tile (and its halo) into LDS.  One pass of prefix sums: the key
-// itself, X = sum of (size + 2^51 per pinned block), which is R << 51 | P
-// exactly while P stays below 2^51 (every block below 2^38 bytes), C, and the
+// itself, X = sum of (size + 2^50 per pinned block), which is R << 50 | P
+// exactly while P stays below 2^50 (every block below 2^37 bytes), C, and the
 // pinned count R.  X[k], C[k] for k < end are written by their owners, the
-// region end and the sentinel X[end + 1] = all-ones by the last thread.  A
-// tile holding a block of 2^38 bytes or more is staged plain instead: P =
-// X - 2^51 R (exact modulo 2^64), R in sm.run, no halo.  Two barriers.
+// region end and the sentinel X[end + 1] = kEndKey by the last thread.  A
+// tile holding a block of 2^37 bytes or more is staged plain instead: P =
+// X - 2^50 R (exact modulo 2^64), R in sm.run, no halo.  Two barriers.
 __device__ __forceinline__ TileState stage_tile(Smem& sm, const TileGeom& tg, uint32_t tid,
                                                 TileRegs& r) {
     const uint32_t lane = tid & 63u;
@@ -890,7 +897,7 @@ __device__ __forceinline__ TileState stage_tile(Smem& sm, const TileGeom& tg, ui
         sm.x[ts.end] = ts.xend;
         sm.xc[ts.end] = ts.xcend;
         sm.run[ts.end] = static_cast<uint16_t>(ts.endrun);
-        sm.x[ts.end + 1] = kNone;  // sentinel end key
+        sm.x[ts.end + 1] = kEndKey;  // sentinel end key
     }
     __syncthreads();
     return ts;
