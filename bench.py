@@ -29,6 +29,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "eviction-window queries/sec and blocks scanned/sec; % of HBM roofline"
 FIT_METRIC = "first-fit queries/sec; % of HBM roofline"
+REPLAY_METRIC = "Algorithm 1 replay: allocator operations/sec over independent pools"
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E, published
 INFINITY_CACHE_BYTES = 256 << 20
 KERNEL = "coop_window_search_kernel"
@@ -47,9 +48,10 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=5.0,
                     help="target duration of the CPU-oracle baseline (0 disables it)")
     ap.add_argument("--no-parity", action="store_true")
-    ap.add_argument("--op", choices=["window", "first_fit"], default="window",
+    ap.add_argument("--op", choices=["window", "first_fit", "replay"], default="window",
                     help="window: the eviction-window search; first_fit: the free-chunk "
-                         "lookup that precedes it")
+                         "lookup that precedes it; replay: Algorithm 1 over training traces "
+                         "(--config picks the trace set)")
     return ap.parse_args()
 
 
@@ -141,6 +143,8 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
 
+    if args.op == "replay":
+        return bench_replay(args, dev)
     spec = workloads.CONFIGS[args.config]
     pools = workloads.make_config(args.config, args.seed)
     if args.op == "first_fit":
@@ -319,6 +323,114 @@ def bench_first_fit(args, pools, spec, dev):
         "parity_vs_oracle": parity,
         "wall_s_timed_region": wall,
         "kernel_source": source_digest(FIT_SOURCE),
+    }
+    print(json.dumps(rec), flush=True)
+
+
+def bench_replay(args, dev):
+    import torch
+
+    import paper_2311_00591_amd as coop
+    from workloads import traces
+
+    k = args.config if args.config < len(traces.REPLAY_CONFIGS) else len(traces.REPLAY_CONFIGS) - 1
+    spec = traces.REPLAY_CONFIGS[k]
+    state, trace = traces.make_replay(k, args.seed)
+    P, cap, T = len(state["len"]), state["capacity"], trace["num_ops"]
+    st0, tr = coop.replay_to_device(state, trace, dev)
+    # every step reads size and kind (first fit) and size, cost and kind
+    # (window search) of every slot of the batch
+    alg_bytes = 26 * P * cap * T
+    parity = None
+    frag = None
+    st = {k2: (v.clone() if hasattr(v, "clone") else v) for k2, v in st0.items()}
+    r = coop.Replay(st, tr)
+    stream = torch.cuda.current_stream(dev)
+    sh = stream.cuda_stream
+    r.launch(sh)
+    torch.cuda.synchronize()
+    host_free = r.free.cpu().numpy().view(np.uint64).reshape(P, T)
+    cap_bytes = np.array([int(state["size"][b * cap:(b + 1) * cap].sum()) for b in range(P)],
+                         dtype=np.float64)
+    sampled = host_free != np.uint64(2**64 - 1)
+    if sampled.any():
+        frag = float(np.mean((host_free.astype(np.float64) / cap_bytes[:, None])[sampled]))
+    evictions = int(sampled.sum())
+    if not args.no_parity:
+        import oracle
+        _, want = oracle.replay(state, trace, threads=16)
+        got_block = r.block.cpu().numpy().view(np.uint64).reshape(P, T)
+        parity = bool(np.array_equal(got_block, want["block"]) and
+                      np.array_equal(host_free, want["free"]))
+    times = []
+    for i in range(args.warmup + args.steps):
+        for k2 in ("size", "cost", "kind", "id", "len"):
+            st[k2].copy_(st0[k2])
+        torch.cuda.synchronize()
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record(stream)
+        r.launch(sh)
+        stop.record(stream)
+        torch.cuda.synchronize()
+        if i >= args.warmup:
+            times.append(start.elapsed_time(stop))
+    ms = float(np.median(times))
+    t = ms / 1e3
+    achieved = alg_bytes / t / 1e9
+    cpu = None
+    if args.cpu_seconds > 0:
+        import oracle
+        try:
+            threads = len(os.sched_getaffinity(0))
+        except AttributeError:
+            threads = os.cpu_count() or 1
+        threads = max(1, min(threads, 64))
+        t0 = time.perf_counter()
+        oracle.replay(state, trace, threads=threads)
+        one = time.perf_counter() - t0
+        reps = max(1, min(100, int(args.cpu_seconds / max(one, 1e-6))))
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            oracle.replay(state, trace, threads=threads)
+        dt = time.perf_counter() - t0
+        cpu = {"value": reps * P * T / dt, "unit": "operations/s", "cores": threads,
+               "kind": "oracle", "sample": f"whole replay ({P} pools x {T} operations) x {reps}, "
+                                           f"{dt:.1f} s, {threads} threads"}
+    rec = {
+        "metric": REPLAY_METRIC,
+        "value": P * T / t,
+        "unit": "operations/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u64",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{spec.name}: {P} pools x {T} operations ({spec.layers} layers, "
+                        f"{spec.iterations} iteration(s), {spec.pattern} pattern), "
+                        f"{cap} slots per pool",
+            "num_pools": P, "num_ops": T, "capacity": cap, "seed": args.seed,
+        },
+        "evictions": evictions,
+        "fragmentation_rate_mean": frag,
+        "roofline": {
+            "kernel": "replay step: first fit + gate + window search + update",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": achieved / PEAK_HBM_GBS,
+            "traffic": None,
+            "algorithmic_bytes_per_launch": alg_bytes,
+        },
+        "cpu_baseline": cpu,
+        "parity_vs_oracle": parity,
+        "kernel_source": source_digest(os.path.join(ROOT, "paper_2311_00591_amd", "csrc",
+                                                    "coop_replay.hip")),
     }
     print(json.dumps(rec), flush=True)
 

@@ -52,6 +52,10 @@ __global__ void replay_init_kernel(uint64_t num_pools, uint64_t cap, uint64_t* s
     if (i == 0) *status = 0;
 }
 
+// Clears the status word (a kernel rather than a memset, so that the call
+// can be captured in a graph).
+__global__ void replay_status_kernel(uint32_t* status) { *status = 0; }
+
 // Step 2: a window is wanted only where an allocation found no chunk.
 __global__ void replay_gate_kernel(uint64_t num_pools, const uint64_t* req_ff, const uint64_t* ff,
                                    uint64_t* req_win) {
@@ -250,6 +254,353 @@ __global__ __launch_bounds__(kThreads) void replay_update_kernel(
     }
 }
 
+// ---------------------------------------------------------------------------
+// Resident replay: one workgroup per pool keeps the pool in LDS and applies
+// all of its operations itself, with no launch per step.  Used when a pool's
+// slots fit in LDS; the same operations as above, in the same order, with
+// the searches done by the workgroup:
+//   first fit  the lowest free slot of at least S bytes (a workgroup min);
+//   window     plain prefix sums P (bytes), C (eviction cost) and R (pinned
+//              count) over the pool; for each start i the first end k with
+//              P[k] - P[i] >= S, valid iff R[k] == R[i] (no pinned block in
+//              between); each thread takes a run of consecutive starts, finds
+//              the first end by bisection and the later ones by walking on
+//              (ends never move left); then the lexicographic minimum of
+//              (cost, bytes, start) over the workgroup.
+// ---------------------------------------------------------------------------
+constexpr uint32_t kResThreads = 256;
+constexpr uint32_t kResWaves = kResThreads / 64;
+
+// LDS bytes per pool slot: size, cost, prefix bytes and cost (u64), tensor id
+// (u32), pinned-count prefix (u16), kind (u8); plus one prefix entry.
+constexpr size_t kResSlotBytes = 8 + 8 + 8 + 8 + 4 + 2 + 1;
+__host__ __device__ constexpr size_t resident_lds_bytes(uint64_t cap) {
+    return ((cap * 8 + 7) & ~7ull) * 2 + ((cap + 1) * 8) * 2 + ((cap * 4 + 7) & ~7ull) +
+           (((cap + 1) * 2 + 7) & ~7ull) + ((cap + 7) & ~7ull);
+}
+
+struct Lds {
+    uint64_t* sz;
+    uint64_t* co;
+    uint64_t* P;
+    uint64_t* C;
+    uint32_t* id;
+    uint16_t* R;
+    uint8_t* kd;
+};
+
+__device__ Lds lds_layout(char* base, uint64_t cap) {
+    Lds l;
+    size_t at = 0;
+    l.sz = reinterpret_cast<uint64_t*>(base + at); at += (cap * 8 + 7) & ~7ull;
+    l.co = reinterpret_cast<uint64_t*>(base + at); at += (cap * 8 + 7) & ~7ull;
+    l.P = reinterpret_cast<uint64_t*>(base + at); at += (cap + 1) * 8;
+    l.C = reinterpret_cast<uint64_t*>(base + at); at += (cap + 1) * 8;
+    l.id = reinterpret_cast<uint32_t*>(base + at); at += (cap * 4 + 7) & ~7ull;
+    l.R = reinterpret_cast<uint16_t*>(base + at); at += ((cap + 1) * 2 + 7) & ~7ull;
+    l.kd = reinterpret_cast<uint8_t*>(base + at);
+    return l;
+}
+
+struct WinKey {
+    uint64_t cost, bytes, start, end;
+};
+
+__device__ __forceinline__ bool win_less(const WinKey& a, const WinKey& b) {
+    if (a.cost != b.cost) return a.cost < b.cost;
+    if (a.bytes != b.bytes) return a.bytes < b.bytes;
+    return a.start < b.start;
+}
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
+    const uint32_t lo = __shfl_xor(static_cast<uint32_t>(v), m, 64);
+    const uint32_t hi = __shfl_xor(static_cast<uint32_t>(v >> 32), m, 64);
+    return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t shfl_up_u64(uint64_t v, int d) {
+    const uint32_t lo = __shfl_up(static_cast<uint32_t>(v), d, 64);
+    const uint32_t hi = __shfl_up(static_cast<uint32_t>(v >> 32), d, 64);
+    return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+// Workgroup sum and minimum (every thread calls them; `red` holds kResWaves).
+__device__ uint64_t res_sum(uint64_t v, uint64_t* red) {
+    for (int o = 32; o >= 1; o >>= 1) v += shfl_xor_u64(v, o);
+    if ((threadIdx.x & 63u) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    uint64_t s = 0;
+    for (uint32_t w = 0; w < kResWaves; ++w) s += red[w];
+    __syncthreads();
+    return s;
+}
+
+__device__ uint64_t res_min(uint64_t v, uint64_t* red) {
+    for (int o = 32; o >= 1; o >>= 1) {
+        const uint64_t x = shfl_xor_u64(v, o);
+        v = x < v ? x : v;
+    }
+    if ((threadIdx.x & 63u) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    uint64_t m = red[0];
+    for (uint32_t w = 1; w < kResWaves; ++w) m = red[w] < m ? red[w] : m;
+    __syncthreads();
+    return m;
+}
+
+// Replaces slots [lo, hi) of a pool of n blocks by m <= 2 new blocks (uniform
+// values), moving the tail in LDS.  Every thread calls it.
+__device__ void res_replace(const Lds& l, uint64_t n, uint64_t lo, uint64_t hi, uint32_t m,
+                            const uint64_t* ns, const uint64_t* nc, const uint8_t* nk,
+                            const uint32_t* ni) {
+    const uint32_t tid = threadIdx.x;
+    const uint64_t tail = n - hi, dst = lo + m;
+    if (dst != hi) {
+        const bool right = dst > hi;
+        for (uint64_t c0 = 0; c0 < tail; c0 += kResThreads) {
+            // moving right, the chunks go from the end
+            const uint64_t base = right ? (tail - c0 > kResThreads ? tail - c0 - kResThreads : 0) : c0;
+            const uint64_t cend = right ? tail - c0 : (c0 + kResThreads < tail ? c0 + kResThreads : tail);
+            const uint64_t k = base + tid;
+            const bool act = k < cend;
+            uint64_t s = 0, c = 0;
+            uint32_t i = 0;
+            uint8_t kd = 0;
+            if (act) {
+                s = l.sz[hi + k]; c = l.co[hi + k]; i = l.id[hi + k]; kd = l.kd[hi + k];
+            }
+            __syncthreads();
+            if (act) {
+                l.sz[dst + k] = s; l.co[dst + k] = c; l.id[dst + k] = i; l.kd[dst + k] = kd;
+            }
+            __syncthreads();
+        }
+    }
+    if (tid < m) {
+        l.sz[lo + tid] = ns[tid]; l.co[lo + tid] = nc[tid];
+        l.id[lo + tid] = ni[tid]; l.kd[lo + tid] = nk[tid];
+    }
+    __syncthreads();
+}
+
+// The window search for S > 0 over a pool of n blocks held in LDS.
+__device__ WinKey res_window(const Lds& l, uint64_t n, uint64_t S, uint64_t* red, WinKey* wred) {
+    const uint32_t tid = threadIdx.x, lane = tid & 63u, w = tid >> 6;
+    // each thread owns blocks [a, a1): local sums, then a workgroup scan
+    const uint64_t per = (n + kResThreads - 1) / kResThreads;
+    const uint64_t a = tid * per < n ? tid * per : n;
+    const uint64_t a1 = a + per < n ? a + per : n;
+    uint64_t ps = 0, pc = 0, pr = 0;
+    for (uint64_t k = a; k < a1; ++k) {
+        ps += l.sz[k];
+        pc += l.kd[k] == COOP_EVICTABLE ? l.co[k] : 0;
+        pr += l.kd[k] >= COOP_PINNED ? 1 : 0;
+    }
+    // inclusive scans over the wavefront
+    uint64_t is = ps, ic = pc, ir = pr;
+    for (int d = 1; d < 64; d <<= 1) {
+        const uint64_t xs = shfl_up_u64(is, d), xc = shfl_up_u64(ic, d), xr = shfl_up_u64(ir, d);
+        if (lane >= static_cast<uint32_t>(d)) {
+            is += xs; ic += xc; ir += xr;
+        }
+    }
+    if (lane == 63) {
+        red[w] = is;
+        wred[w] = WinKey{ic, ir, 0, 0};
+    }
+    __syncthreads();
+    uint64_t bs = 0, bc = 0, br = 0;
+    for (uint32_t v = 0; v < w; ++v) {
+        bs += red[v]; bc += wred[v].cost; br += wred[v].bytes;
+    }
+    __syncthreads();
+    uint64_t xs = bs + is - ps, xc = bc + ic - pc, xr = br + ir - pr;
+    for (uint64_t k = a; k < a1; ++k) {
+        l.P[k] = xs; l.C[k] = xc; l.R[k] = static_cast<uint16_t>(xr);
+        xs += l.sz[k];
+        xc += l.kd[k] == COOP_EVICTABLE ? l.co[k] : 0;
+        xr += l.kd[k] >= COOP_PINNED ? 1 : 0;
+    }
+    if (a1 == n && a < a1) {
+        l.P[n] = xs; l.C[n] = xc; l.R[n] = static_cast<uint16_t>(xr);
+    }
+    if (n == 0 && tid == 0) {
+        l.P[0] = 0; l.C[0] = 0; l.R[0] = 0;
+    }
+    __syncthreads();
+    // starts [a, a1): the first end by bisection, later ends by walking on
+    WinKey best{kNone, kNone, kNone, kNone};
+    uint64_t k = 0;
+    for (uint64_t i = a; i < a1; ++i) {
+        const uint64_t pi = l.P[i];
+        if (i == a) {
+            uint64_t lo = i + 1, hi = n + 1;  // first k in [i + 1, n] with P[k] - P[i] >= S, or n + 1
+            while (lo < hi) {
+                const uint64_t mid = (lo + hi) >> 1;
+                if (l.P[mid] - pi >= S) hi = mid; else lo = mid + 1;
+            }
+            k = lo;
+        } else {
+            if (k < i + 1) k = i + 1;
+            while (k <= n && l.P[k] - pi < S) ++k;
+        }
+        if (k > n) break;  // no later start of this thread reaches S either
+        if (l.R[k] == l.R[i]) {
+            const WinKey c{l.C[k] - l.C[i], l.P[k] - pi, i, k};
+            if (win_less(c, best)) best = c;
+        }
+    }
+    // workgroup lexicographic minimum
+    for (int o = 32; o >= 1; o >>= 1) {
+        WinKey x{shfl_xor_u64(best.cost, o), shfl_xor_u64(best.bytes, o), shfl_xor_u64(best.start, o),
+                 shfl_xor_u64(best.end, o)};
+        if (win_less(x, best)) best = x;
+    }
+    if (lane == 0) wred[w] = best;
+    __syncthreads();
+    WinKey m = wred[0];
+    for (uint32_t v = 1; v < kResWaves; ++v)
+        if (win_less(wred[v], m)) m = wred[v];
+    __syncthreads();
+    return m;
+}
+
+__global__ __launch_bounds__(kResThreads) void replay_resident_kernel(
+    uint64_t* size, uint64_t* cost, uint8_t* kind, uint32_t* id, uint64_t* len, uint64_t cap,
+    const uint8_t* op, const uint32_t* op_id, const uint64_t* op_size, const uint64_t* op_cost,
+    const uint8_t* op_flags, uint64_t num_ops, uint64_t* out_block, uint64_t* out_window,
+    uint64_t* out_cost, uint64_t* out_free, uint32_t* status) {
+    extern __shared__ __align__(16) char lds_raw[];
+    __shared__ uint64_t red[kResWaves];
+    __shared__ WinKey wred[kResWaves];
+    __shared__ uint32_t hit;
+    const uint32_t tid = threadIdx.x;
+    const uint64_t b = blockIdx.x;
+    const Lds l = lds_layout(lds_raw, cap);
+    const uint64_t g = b * cap;
+    uint64_t n = len[b];
+    if (n > cap) n = cap;
+    for (uint64_t k = tid; k < n; k += kResThreads) {
+        l.sz[k] = size[g + k]; l.co[k] = cost[g + k]; l.id[k] = id[g + k]; l.kd[k] = kind[g + k];
+    }
+    __syncthreads();
+    for (uint64_t t = 0; t < num_ops; ++t) {
+        const uint64_t o = b * num_ops + t;
+        const uint8_t kop = op[o];
+        const uint32_t oid = op_id[o];
+        uint64_t r_block = kNone, r_w0 = kNone, r_w1 = kNone, r_cost = 0, r_free = kNone;
+        if (kop == kOpFree) {
+            if (tid == 0) hit = ~0u;
+            __syncthreads();
+            for (uint64_t k = tid; k < n; k += kResThreads)
+                if (l.kd[k] != COOP_FREE && l.id[k] == oid) hit = static_cast<uint32_t>(k);
+            __syncthreads();
+            const uint32_t j = hit;
+            if (j != ~0u) {
+                const uint64_t lo = j > 0 && l.kd[j - 1] == COOP_FREE ? j - 1 : j;
+                const uint64_t hi = j + 1 < n && l.kd[j + 1] == COOP_FREE ? j + 2 : j + 1;
+                uint64_t total = 0;
+                for (uint64_t k = lo; k < hi; ++k) total += l.sz[k];
+                __syncthreads();
+                const uint64_t ns[1] = {total}, nc[1] = {0};
+                const uint8_t nk[1] = {COOP_FREE};
+                const uint32_t ni[1] = {0};
+                res_replace(l, n, lo, hi, 1, ns, nc, nk, ni);
+                n = n - (hi - lo) + 1;
+                r_block = lo;
+            }
+        } else if (kop == kOpAlloc && op_size[o] != 0 && oid != 0) {
+            const uint64_t S = op_size[o];
+            uint64_t mine = kNone;
+            for (uint64_t k = tid; k < n; k += kResThreads) {
+                if (l.kd[k] == COOP_FREE && l.sz[k] >= S) {
+                    mine = k;
+                    break;
+                }
+            }
+            uint64_t k = res_min(mine, red);
+            bool ok = true;
+            if (k == kNone) {
+                const WinKey wk = res_window(l, n, S, red, wred);
+                if (wk.start == kNone) {
+                    ok = false;  // no window: the allocation fails, nothing changes
+                } else {
+                    uint64_t fb = 0;
+                    for (uint64_t j = tid; j < n; j += kResThreads)
+                        if (l.kd[j] == COOP_FREE) fb += l.sz[j];
+                    r_free = res_sum(fb, red);
+                    r_w0 = wk.start;
+                    r_w1 = wk.end;
+                    r_cost = wk.cost;
+                    uint64_t lo = wk.start, hi = wk.end;
+                    if (lo > 0 && l.kd[lo - 1] == COOP_FREE) --lo;
+                    if (hi < n && l.kd[hi] == COOP_FREE) ++hi;
+                    uint64_t tot = 0;
+                    for (uint64_t j = lo + tid; j < hi; j += kResThreads) tot += l.sz[j];
+                    const uint64_t total = res_sum(tot, red);
+                    const uint64_t ns[1] = {total}, nc[1] = {0};
+                    const uint8_t nk[1] = {COOP_FREE};
+                    const uint32_t ni[1] = {0};
+                    res_replace(l, n, lo, hi, 1, ns, nc, nk, ni);
+                    n = n - (hi - lo) + 1;
+                    k = lo;  // the only free chunk of at least S bytes
+                }
+            }
+            if (ok && n + 1 > cap) {
+                if (tid == 0) atomicOr(status, kErrCapacity);
+                ok = false;
+            }
+            if (ok) {
+                const uint64_t F = l.sz[k];
+                const uint8_t fl = op_flags[o];
+                const uint8_t tk = (fl & kFlagPinned) ? COOP_PINNED : COOP_EVICTABLE;
+                uint64_t ns[2], nc[2];
+                uint8_t nk[2];
+                uint32_t ni[2];
+                uint32_t m = 1;
+                uint64_t at = k;
+                if (F == S) {
+                    ns[0] = S; nc[0] = op_cost[o]; nk[0] = tk; ni[0] = oid;
+                } else if (fl & kFlagLeft) {
+                    ns[0] = S; nc[0] = op_cost[o]; nk[0] = tk; ni[0] = oid;
+                    ns[1] = F - S; nc[1] = 0; nk[1] = COOP_FREE; ni[1] = 0;
+                    m = 2;
+                } else {
+                    ns[0] = F - S; nc[0] = 0; nk[0] = COOP_FREE; ni[0] = 0;
+                    ns[1] = S; nc[1] = op_cost[o]; nk[1] = tk; ni[1] = oid;
+                    m = 2;
+                    at = k + 1;
+                }
+                __syncthreads();
+                res_replace(l, n, k, k + 1, m, ns, nc, nk, ni);
+                n = n + m - 1;
+                r_block = at;
+            }
+        } else if (kop == kOpAlloc) {
+            if (tid == 0) atomicOr(status, kErrOperation);
+        }
+        if (tid == 0) {
+            out_block[o] = r_block;
+            out_window[2 * o] = r_w0;
+            out_window[2 * o + 1] = r_w1;
+            out_cost[o] = r_cost;
+            out_free[o] = r_free;
+        }
+    }
+    // the pool back to its slots; unused slots empty pinned blocks
+    for (uint64_t k = tid; k < cap; k += kResThreads) {
+        const bool in = k < n;
+        size[g + k] = in ? l.sz[k] : 0;
+        cost[g + k] = in ? l.co[k] : 0;
+        id[g + k] = in ? l.id[k] : 0;
+        kind[g + k] = in ? l.kd[k] : static_cast<uint8_t>(COOP_PINNED);
+    }
+    if (tid == 0) len[b] = n;
+}
+
+constexpr size_t kLdsLimit = 160 * 1024;
+constexpr size_t kStaticResLds = 1024;  // red, wred, hit (generous)
+
 struct ReplayLayout {
     size_t seg, req_off, req_ff, req_win, ff, win, status, ff_ws, win_ws, bytes;
     size_t ff_ws_bytes, win_ws_bytes;
@@ -305,6 +656,24 @@ coop_status_t coop_replay(uint64_t* size, uint64_t* cost, uint8_t* kind, uint32_
     ReplayLayout l;
     if (!replay_layout(num_pools, capacity, &l)) return COOP_ERR_INVALID;
     if (!workspace || workspace_bytes < l.bytes) return COOP_ERR_WORKSPACE;
+    hipStream_t s0 = static_cast<hipStream_t>(stream);
+    // Pools that fit in LDS: one resident workgroup per pool, one launch.
+    const size_t res_lds = resident_lds_bytes(capacity);
+    if (capacity < 65536 && res_lds + kStaticResLds <= kLdsLimit) {
+        hipLaunchKernelGGL(replay_status_kernel, dim3(1), dim3(1), 0, s0, status_out);
+        if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
+        if (res_lds > 64 * 1024 &&
+            hipFuncSetAttribute(reinterpret_cast<const void*>(replay_resident_kernel),
+                                hipFuncAttributeMaxDynamicSharedMemorySize,
+                                static_cast<int>(res_lds)) != hipSuccess)
+            return COOP_ERR_HIP;
+        hipLaunchKernelGGL(replay_resident_kernel, dim3(static_cast<uint32_t>(num_pools)),
+                           dim3(kResThreads), res_lds, s0, size, cost, kind, id, len, capacity, op,
+                           op_id, op_size, op_cost, op_flags, num_ops, out_block, out_window,
+                           out_cost, out_free, status_out);
+        if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
+        return COOP_OK;
+    }
     char* w = static_cast<char*>(workspace);
     uint64_t* seg = reinterpret_cast<uint64_t*>(w + l.seg);
     uint64_t* req_off = reinterpret_cast<uint64_t*>(w + l.req_off);

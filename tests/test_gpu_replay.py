@@ -113,3 +113,15 @@ def test_out_of_slots_is_reported():
     assert status & 1
     assert got["block"][0].tolist()[:2] == [1, 1] and got["block"][0, 2] == U64MAX
     assert int(got_state["len"][0]) == 3
+
+
+def test_pools_too_large_for_lds_take_the_stepwise_path():
+    """Capacity beyond what one workgroup's LDS holds: the replay runs one
+    step per operation with the batched first-fit and window kernels."""
+    _announce("stepwise path")
+    import paper_2311_00591_amd as coop
+    state, trace = traces.make_replay(1, 7, layers=2200, num_pools=6, iterations=1,
+                                      budget_frac=0.9)
+    # 39 bytes of LDS per slot (pool, prefix sums, ids, run counts): above 160 KiB
+    assert state["capacity"] * 39 > 160 * 1024
+    assert_same(state, trace, "stepwise")
