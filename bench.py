@@ -338,9 +338,11 @@ def bench_replay(args, dev):
     state, trace = traces.make_replay(k, args.seed)
     P, cap, T = len(state["len"]), state["capacity"], trace["num_ops"]
     st0, tr = coop.replay_to_device(state, trace, dev)
-    # every step reads size and kind (first fit) and size, cost and kind
-    # (window search) of every slot of the batch
-    alg_bytes = 26 * P * cap * T
+    # compulsory bytes: each pool's slots read and written once (size, cost,
+    # kind, id: 21 B), each operation read once (op, id, size, cost, flags:
+    # 22 B) and its outcome written (block, window, cost, free: 40 B); the
+    # replay is bound by its chain of dependent operations, not by these
+    alg_bytes = 2 * 21 * P * cap + (22 + 40) * P * T
     parity = None
     frag = None
     st = {k2: (v.clone() if hasattr(v, "clone") else v) for k2, v in st0.items()}
@@ -418,7 +420,7 @@ def bench_replay(args, dev):
         "evictions": evictions,
         "fragmentation_rate_mean": frag,
         "roofline": {
-            "kernel": "replay step: first fit + gate + window search + update",
+            "kernel": "replay_resident_kernel (pools held in LDS)",
             "bound": "hbm",
             "achieved": achieved,
             "peak": PEAK_HBM_GBS,
