@@ -135,8 +135,9 @@ def first_fit(size, kind, seg_offsets, req_sizes, req_offsets, threads=1):
     return out
 
 
-def replay(state, trace, threads=1):
-    """Algorithm 1 replayed on independent pools (see coop_oracle.h).
+def replay(state, trace, threads=1, policy=0):
+    """Algorithm 1 replayed on independent pools (see coop_oracle.h);
+    policy 0 evicts the sliding window, policy 1 the DTR-style greedy choice.
 
     state: dict of numpy arrays size/cost (uint64, num_pools * capacity),
     kind (uint8), id (uint32), len (uint64, num_pools), and 'capacity';
@@ -167,7 +168,7 @@ def replay(state, trace, threads=1):
                     ctypes.POINTER(ctypes.c_uint32))
     lib.coop_oracle_replay.argtypes = [p64, p64, p8, p32, p64, ctypes.c_uint64, ctypes.c_uint64,
                                        p8, p32, p64, p64, p8, ctypes.c_uint64, p64, p64, p64, p64,
-                                       ctypes.c_int]
+                                       ctypes.c_int, ctypes.c_int]
     lib.coop_oracle_replay.restype = ctypes.c_int
     rc = lib.coop_oracle_replay(
         _ptr(st["size"], ctypes.c_uint64), _ptr(st["cost"], ctypes.c_uint64),
@@ -176,7 +177,8 @@ def replay(state, trace, threads=1):
         _ptr(tr["op_id"], ctypes.c_uint32), _ptr(tr["op_size"], ctypes.c_uint64),
         _ptr(tr["op_cost"], ctypes.c_uint64), _ptr(tr["op_flags"], ctypes.c_uint8), T,
         _ptr(out_block, ctypes.c_uint64), _ptr(out_window, ctypes.c_uint64),
-        _ptr(out_cost, ctypes.c_uint64), _ptr(out_free, ctypes.c_uint64), int(threads))
+        _ptr(out_cost, ctypes.c_uint64), _ptr(out_free, ctypes.c_uint64), int(policy),
+        int(threads))
     if rc != 0:
         raise OracleError(rc)
     outs = {"block": out_block.reshape(P, T), "window": out_window.reshape(P, T, 2),

@@ -415,6 +415,42 @@ int coop_oracle_first_fit(const uint64_t *size, const uint8_t *kind, uint64_t nu
 #define OP_FREE 1
 #define FLAG_LEFT 1u   /* an expensive operation: placed at the left end */
 #define FLAG_PINNED 2u /* an unevictable tensor */
+#define POLICY_WINDOW 0 /* Coop: evict the sliding window (section 3.3) */
+#define POLICY_GREEDY 1 /* DTR-style: evict the least h = c / (m * s), one by one */
+
+/* 160-bit products c * m * s for the greedy comparison (c, m < 2^64,
+ * s < 2^32), as (hi, lo) with hi holding bits 128 and up. */
+struct u160 { uint64_t hi; unsigned __int128 lo; };
+
+static struct u160 mul3(uint64_t c, uint64_t m, uint32_t st) {
+    unsigned __int128 cm = (unsigned __int128)c * m;
+    unsigned __int128 lo64 = (unsigned __int128)(uint64_t)cm * st;
+    unsigned __int128 hi64 = (unsigned __int128)(uint64_t)(cm >> 64) * st;
+    /* cm * st = hi64 * 2^64 + lo64 */
+    unsigned __int128 mid = (lo64 >> 64) + (uint64_t)hi64;
+    struct u160 r;
+    r.lo = (mid << 64) | (uint64_t)lo64;
+    r.hi = (uint64_t)(hi64 >> 64) + (uint64_t)(mid >> 64);
+    return r;
+}
+
+static int u160_less(struct u160 a, struct u160 b) {
+    return a.hi != b.hi ? a.hi < b.hi : a.lo < b.lo;
+}
+
+/* DTR's heuristic h = c / (m * s) (section 3.3 restates it): cost over
+ * size times staleness.  Staleness counts allocations since the tensor's
+ * own, read off the trace's tensor ids, which are issued in allocation
+ * order (op_id - id, modulo 2^32).  A zero size or staleness counts as 1, so
+ * that h is always a finite ratio.  h_a < h_b iff
+ * c_a * m_b * s_b < c_b * m_a * s_a, compared exactly; ties go to the lower
+ * block index. */
+static int greedy_less(uint64_t ca, uint64_t ma, uint32_t sa, uint64_t cb, uint64_t mb,
+                       uint32_t sb) {
+    ma = ma ? ma : 1; mb = mb ? mb : 1;
+    sa = sa ? sa : 1; sb = sb ? sb : 1;
+    return u160_less(mul3(ca, mb, sb), mul3(cb, ma, sa));
+}
 
 struct replay_pool {
     uint64_t *size, *cost;
@@ -456,7 +492,7 @@ static uint64_t pool_free_range(struct replay_pool *p, uint64_t lo, uint64_t hi)
 static int replay_one(struct replay_pool *p, const uint8_t *op, const uint32_t *op_id,
                       const uint64_t *op_size, const uint64_t *op_cost, const uint8_t *op_flags,
                       uint64_t num_ops, uint64_t *out_block, uint64_t *out_window,
-                      uint64_t *out_cost, uint64_t *out_free) {
+                      uint64_t *out_cost, uint64_t *out_free, int policy) {
     for (uint64_t t = 0; t < num_ops; ++t) {
         out_block[t] = NONE;
         out_window[2 * t] = out_window[2 * t + 1] = NONE;
@@ -475,6 +511,33 @@ static int replay_one(struct replay_pool *p, const uint8_t *op, const uint32_t *
             return COOP_ORACLE_ERR_INVALID;
         const uint64_t S = op_size[t];
         uint64_t k = first_fit_one(p->size, p->kind, p->len, S);
+        if (k == NONE && policy == POLICY_GREEDY) {
+            /* evict the least-h tensor until a chunk fits or none is left */
+            uint64_t free_bytes = 0, count = 0, evcost = 0;
+            for (uint64_t j = 0; j < p->len; ++j)
+                if (p->kind[j] == KIND_FREE) free_bytes += p->size[j];
+            while (k == NONE) {
+                uint64_t v = NONE;
+                for (uint64_t j = 0; j < p->len; ++j) {
+                    if (p->kind[j] != KIND_EVICTABLE) continue;
+                    const uint32_t st = op_id[t] - p->id[j];
+                    if (v == NONE || greedy_less(p->cost[j], p->size[j], st, p->cost[v],
+                                                 p->size[v], op_id[t] - p->id[v]))
+                        v = j;
+                }
+                if (v == NONE) break;
+                ++count;
+                evcost += p->cost[v];
+                pool_free_range(p, v, v + 1);
+                k = first_fit_one(p->size, p->kind, p->len, S);
+            }
+            if (count) {
+                out_free[t] = free_bytes;
+                out_window[2 * t] = count;
+                out_cost[t] = evcost;
+            }
+            if (k == NONE) continue; /* the allocation fails (evictions stay done) */
+        }
         if (k == NONE) {
             uint64_t win[3];
             if (!runs_fit(p->size, p->cost, p->kind, p->len)) return COOP_ORACLE_ERR_OVERFLOW;
@@ -527,6 +590,7 @@ struct replay_job {
     const uint64_t *op_size, *op_cost;
     const uint8_t *op_flags;
     uint64_t *out_block, *out_window, *out_cost, *out_free;
+    int policy;
     _Atomic uint64_t next;
     _Atomic int status;
 };
@@ -541,7 +605,7 @@ static void *replay_worker(void *arg) {
         const uint64_t o = b * j->num_ops;
         int rc = replay_one(&p, j->op + o, j->op_id + o, j->op_size + o, j->op_cost + o,
                             j->op_flags + o, j->num_ops, j->out_block + o, j->out_window + 2 * o,
-                            j->out_cost + o, j->out_free + o);
+                            j->out_cost + o, j->out_free + o, j->policy);
         j->len[b] = p.len;
         if (rc != COOP_ORACLE_OK) atomic_store(&j->status, rc);
     }
@@ -553,8 +617,9 @@ int coop_oracle_replay(uint64_t *size, uint64_t *cost, uint8_t *kind, uint32_t *
                        const uint32_t *op_id, const uint64_t *op_size, const uint64_t *op_cost,
                        const uint8_t *op_flags, uint64_t num_ops, uint64_t *out_block,
                        uint64_t *out_window, uint64_t *out_cost, uint64_t *out_free,
-                       int num_threads) {
+                       int policy, int num_threads) {
     if (num_pools == 0) return COOP_ORACLE_OK;
+    if (policy != POLICY_WINDOW && policy != POLICY_GREEDY) return COOP_ORACLE_ERR_INVALID;
     if (!size || !cost || !kind || !id || !len || capacity == 0) return COOP_ORACLE_ERR_INVALID;
     if (num_ops && (!op || !op_id || !op_size || !op_cost || !op_flags || !out_block ||
                     !out_window || !out_cost || !out_free))
@@ -566,7 +631,7 @@ int coop_oracle_replay(uint64_t *size, uint64_t *cost, uint8_t *kind, uint32_t *
     job.cap = capacity; job.num_pools = num_pools; job.num_ops = num_ops;
     job.op = op; job.op_id = op_id; job.op_size = op_size; job.op_cost = op_cost;
     job.op_flags = op_flags; job.out_block = out_block; job.out_window = out_window;
-    job.out_cost = out_cost; job.out_free = out_free;
+    job.out_cost = out_cost; job.out_free = out_free; job.policy = policy;
     atomic_init(&job.next, 0);
     atomic_init(&job.status, COOP_ORACLE_OK);
     if (num_threads <= 1) {

@@ -105,13 +105,23 @@ int coop_oracle_first_fit(const uint64_t *size, const uint8_t *kind, uint64_t nu
  * chunk of a release, ~0 for a failed allocation or a release of an evicted
  * tensor), out_window[2] (evicted window, pre-eviction indices, or ~0),
  * out_cost (its eviction cost), out_free (free bytes just before an
- * eviction, else ~0).  Returns -5 if a pool would exceed its capacity. */
+ * eviction, else ~0).  Returns -5 if a pool would exceed its capacity.
+ *
+ * policy 0 is Coop's (the sliding window).  policy 1 is the DTR-style greedy
+ * baseline: while no chunk fits, evict the evictable tensor of least
+ * h = cost / (size * staleness), staleness being op_id minus the tensor's
+ * id (ids are issued in allocation order), ties to the lower index; each
+ * eviction frees and merges one block.  out_window[0] then holds the number
+ * of tensors evicted for the operation (out_window[1] ~0), out_cost their
+ * summed cost, out_free the free bytes before the first of them.  If the
+ * pool runs out of evictable tensors the allocation fails, the evictions
+ * staying done. */
 int coop_oracle_replay(uint64_t *size, uint64_t *cost, uint8_t *kind, uint32_t *id, uint64_t *len,
                        uint64_t num_pools, uint64_t capacity, const uint8_t *op,
                        const uint32_t *op_id, const uint64_t *op_size, const uint64_t *op_cost,
                        const uint8_t *op_flags, uint64_t num_ops, uint64_t *out_block,
                        uint64_t *out_window, uint64_t *out_cost, uint64_t *out_free,
-                       int num_threads);
+                       int policy, int num_threads);
 
 #ifdef __cplusplus
 }
