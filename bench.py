@@ -48,6 +48,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=5.0,
                     help="target duration of the CPU-oracle baseline (0 disables it)")
     ap.add_argument("--no-parity", action="store_true")
+    ap.add_argument("--policy", choices=["window", "greedy"], default="window",
+                    help="replay eviction policy timed by --op replay: Coop's sliding window "
+                         "or the DTR-style greedy baseline")
     ap.add_argument("--op", choices=["window", "first_fit", "replay"], default="window",
                     help="window: the eviction-window search; first_fit: the free-chunk "
                          "lookup that precedes it; replay: Algorithm 1 over training traces "
@@ -77,11 +80,9 @@ def fit_bytes(pools):
 
 
 def source_digest(source=None):
-    h = hashlib.sha256()
-    for p in (source or KERNEL_SOURCE, os.path.join(ROOT, "include", "coop.h")):
-        with open(p, "rb") as f:
-            h.update(f.read())
-    return h.hexdigest()[:16]
+    """First 16 hex digits of the sha256 of a kernel's source file."""
+    with open(source or KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
 def measured_traffic(workload_name):
@@ -343,27 +344,47 @@ def bench_replay(args, dev):
     # 22 B) and its outcome written (block, window, cost, free: 40 B); the
     # replay is bound by its chain of dependent operations, not by these
     alg_bytes = 2 * 21 * P * cap + (22 + 40) * P * T
-    parity = None
-    frag = None
-    st = {k2: (v.clone() if hasattr(v, "clone") else v) for k2, v in st0.items()}
-    r = coop.Replay(st, tr)
+    policy = {"window": coop.POLICY_WINDOW, "greedy": coop.POLICY_GREEDY}[args.policy]
     stream = torch.cuda.current_stream(dev)
     sh = stream.cuda_stream
-    r.launch(sh)
-    torch.cuda.synchronize()
-    host_free = r.free.cpu().numpy().view(np.uint64).reshape(P, T)
     cap_bytes = np.array([int(state["size"][b * cap:(b + 1) * cap].sum()) for b in range(P)],
                          dtype=np.float64)
-    sampled = host_free != np.uint64(2**64 - 1)
-    if sampled.any():
-        frag = float(np.mean((host_free.astype(np.float64) / cap_bytes[:, None])[sampled]))
-    evictions = int(sampled.sum())
+    none = np.uint64(2**64 - 1)
+
+    def run_once(pol):
+        """One untimed replay under policy pol: its host outputs and summary."""
+        s1 = {k2: (v.clone() if hasattr(v, "clone") else v) for k2, v in st0.items()}
+        r1 = coop.Replay(s1, tr, policy=pol)
+        r1.launch(sh)
+        torch.cuda.synchronize()
+        out = {"block": r1.block.cpu().numpy().view(np.uint64).reshape(P, T),
+               "free": r1.free.cpu().numpy().view(np.uint64).reshape(P, T),
+               "cost": r1.cost.cpu().numpy().view(np.uint64).reshape(P, T)}
+        sampled = out["free"] != none
+        failed = (out["block"] == none) & (np.asarray(trace["op"]).reshape(P, T) == 0)
+        summary = {
+            "eviction_events": int(sampled.sum()),
+            "fragmentation_rate_mean": (float(np.mean(
+                (out["free"].astype(np.float64) / cap_bytes[:, None])[sampled]))
+                if sampled.any() else None),
+            "evicted_cost_total": float(out["cost"].astype(np.float64).sum()),
+            "failed_allocations": int(failed.sum()),
+            "status": int(r1.status.item()),
+        }
+        return out, summary
+
+    host, summary = run_once(policy)
+    other = coop.POLICY_GREEDY if policy == coop.POLICY_WINDOW else coop.POLICY_WINDOW
+    _, other_summary = run_once(other)
+    by_policy = {args.policy: summary,
+                 ("greedy" if other == coop.POLICY_GREEDY else "window"): other_summary}
+    parity = None
     if not args.no_parity:
         import oracle
-        _, want = oracle.replay(state, trace, threads=16)
-        got_block = r.block.cpu().numpy().view(np.uint64).reshape(P, T)
-        parity = bool(np.array_equal(got_block, want["block"]) and
-                      np.array_equal(host_free, want["free"]))
+        _, want = oracle.replay(state, trace, threads=16, policy=policy)
+        parity = bool(all(np.array_equal(host[k2], want[k2]) for k2 in ("block", "free", "cost")))
+    st = {k2: (v.clone() if hasattr(v, "clone") else v) for k2, v in st0.items()}
+    r = coop.Replay(st, tr, policy=policy)
     times = []
     for i in range(args.warmup + args.steps):
         for k2 in ("size", "cost", "kind", "id", "len"):
@@ -388,12 +409,12 @@ def bench_replay(args, dev):
             threads = os.cpu_count() or 1
         threads = max(1, min(threads, 64))
         t0 = time.perf_counter()
-        oracle.replay(state, trace, threads=threads)
+        oracle.replay(state, trace, threads=threads, policy=policy)
         one = time.perf_counter() - t0
         reps = max(1, min(100, int(args.cpu_seconds / max(one, 1e-6))))
         t0 = time.perf_counter()
         for _ in range(reps):
-            oracle.replay(state, trace, threads=threads)
+            oracle.replay(state, trace, threads=threads, policy=policy)
         dt = time.perf_counter() - t0
         cpu = {"value": reps * P * T / dt, "unit": "operations/s", "cores": threads,
                "kind": "oracle", "sample": f"whole replay ({P} pools x {T} operations) x {reps}, "
@@ -416,9 +437,11 @@ def bench_replay(args, dev):
                         f"{spec.iterations} iteration(s), {spec.pattern} pattern), "
                         f"{cap} slots per pool",
             "num_pools": P, "num_ops": T, "capacity": cap, "seed": args.seed,
+            "policy": args.policy,
         },
-        "evictions": evictions,
-        "fragmentation_rate_mean": frag,
+        "evictions": summary["eviction_events"],
+        "fragmentation_rate_mean": summary["fragmentation_rate_mean"],
+        "policies": by_policy,
         "roofline": {
             "kernel": "replay_resident_kernel (pools held in LDS)",
             "bound": "hbm",

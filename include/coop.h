@@ -53,7 +53,7 @@ typedef enum {
 } coop_status_t;
 
 /* Version of this ABI; bumped on any incompatible change. */
-#define COOP_ABI_VERSION 1
+#define COOP_ABI_VERSION 2
 int coop_abi_version(void);
 
 /* Human-readable text for a status code (static storage, never NULL). */
@@ -160,6 +160,12 @@ coop_status_t coop_first_fit(const uint64_t *size, const uint8_t *kind, uint64_t
                              uint64_t num_requests, uint64_t *out,
                              void *workspace, size_t workspace_bytes, void *stream);
 
+/* Eviction policies of coop_replay. */
+typedef enum {
+    COOP_POLICY_WINDOW = 0, /* Coop: the sliding window (section 3.3) */
+    COOP_POLICY_GREEDY = 1  /* DTR's heuristic, one tensor at a time (section 3.3) */
+} coop_policy_t;
+
 /*
  * Replay of Algorithm 1 on num_pools independent pools, all in lockstep.
  * For every operation of a pool's trace, in order: an allocation runs first
@@ -170,6 +176,15 @@ coop_status_t coop_first_fit(const uint64_t *size, const uint8_t *kind, uint64_t
  * (section 3.4).  With no window the allocation fails and nothing changes.
  * A release frees the tensor's block and merges it with free neighbours; a
  * tensor already evicted is skipped.
+ *
+ * policy COOP_POLICY_WINDOW is the above.  COOP_POLICY_GREEDY is the
+ * baseline Coop is compared against: while first fit finds no chunk, evict
+ * the evictable tensor of least h = c / (m * s), cost over size times
+ * staleness (op_id minus the tensor's id, modulo 2^32; ids are issued in
+ * allocation order), a zero size or staleness counting as 1, ties to the
+ * lower block index, comparing exactly; each eviction frees and merges one
+ * block.  Placement is the same.  With nothing left to evict the allocation
+ * fails and the evictions stay done.  Any other value: COOP_ERR_INVALID.
  *
  * Pools (device, updated in place): pool b occupies slots
  *   [b * capacity, (b + 1) * capacity) of size, cost (u64), kind (u8) and id
@@ -182,14 +197,18 @@ coop_status_t coop_first_fit(const uint64_t *size, const uint8_t *kind, uint64_t
  * Outputs (device), per operation: out_block (the tensor's block, or the
  *   merged free chunk of a release; ~0 for a failed allocation or a
  *   skipped release), out_window[2] (the evicted window, indices before the
- *   eviction, or ~0), out_cost (its eviction cost), out_free (free bytes
- *   just before an eviction, else ~0: the fragmentation-rate sample of
- *   section 4.1, free memory over the memory the allocator holds).
+ *   eviction, or ~0; greedy: {number of tensors evicted, ~0}), out_cost (the
+ *   evicted cost, modulo 2^64), out_free (free bytes just before an
+ *   eviction, else ~0: the fragmentation-rate sample of section 4.1, free
+ *   memory over the memory the allocator holds).
  * status (device u32): set to 0, then bit 0 if a pool ran out of slots (that
  *   allocation is skipped), bit 1 for an invalid operation.
  * workspace: coop_replay_workspace_size() bytes (device, caller-owned).
- * Enqueues 4 + 5 * num_ops launches on `stream`; nothing is allocated or
- * synchronised.
+ * Pools of up to about 4170 slots (39 bytes of LDS a slot, within 160 KiB)
+ * are replayed by two launches, a workgroup per pool holding the pool in
+ * LDS; larger ones step by step, about five launches per operation (the
+ * greedy policy skips the window search's).  Either way everything is enqueued on `stream`; nothing is
+ * allocated or synchronised.
  */
 coop_status_t coop_replay_workspace_size(uint64_t num_pools, uint64_t capacity,
                                          size_t *bytes_out);
@@ -198,9 +217,9 @@ coop_status_t coop_replay(uint64_t *size, uint64_t *cost, uint8_t *kind, uint32_
                           uint64_t *len, uint64_t num_pools, uint64_t capacity,
                           const uint8_t *op, const uint32_t *op_id, const uint64_t *op_size,
                           const uint64_t *op_cost, const uint8_t *op_flags, uint64_t num_ops,
-                          uint64_t *out_block, uint64_t *out_window, uint64_t *out_cost,
-                          uint64_t *out_free, uint32_t *status, void *workspace,
-                          size_t workspace_bytes, void *stream);
+                          int32_t policy, uint64_t *out_block, uint64_t *out_window,
+                          uint64_t *out_cost, uint64_t *out_free, uint32_t *status,
+                          void *workspace, size_t workspace_bytes, void *stream);
 
 #ifdef __cplusplus
 }

@@ -23,6 +23,7 @@ LIBRARY = os.path.join(_PKG, "libcoop.so")
 
 COOP_FREE, COOP_EVICTABLE, COOP_PINNED = 0, 1, 2
 INFEASIBLE = -1  # int64 view of the all-ones sentinel
+POLICY_WINDOW, POLICY_GREEDY = 0, 1  # coop_replay's eviction policies
 
 _STATUS = {0: "ok", -1: "invalid argument", -2: "workspace missing or too small",
            -3: "HIP launch failed"}
@@ -68,8 +69,8 @@ def load_library():
     lib.coop_first_fit.restype = ctypes.c_int
     lib.coop_replay_workspace_size.argtypes = [u64, u64, ctypes.POINTER(sz)]
     lib.coop_replay_workspace_size.restype = ctypes.c_int
-    lib.coop_replay.argtypes = [vp, vp, vp, vp, vp, u64, u64, vp, vp, vp, vp, vp, u64, vp, vp,
-                                vp, vp, vp, vp, sz, vp]
+    lib.coop_replay.argtypes = [vp, vp, vp, vp, vp, u64, u64, vp, vp, vp, vp, vp, u64,
+                                ctypes.c_int32, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.coop_replay.restype = ctypes.c_int
     lib.coop_window_search.restype = ctypes.c_int
     _lib = lib
@@ -260,9 +261,12 @@ class Replay:
     kind (uint8), id (int32 holding u32), len (int64, P) and int capacity;
     trace: dict of device tensors op (uint8), op_id (int32), op_size/op_cost
     (int64), op_flags (uint8), each P*T.  Outputs: block, cost, free (int64,
-    P*T), window (int64, P*T*2), status (int32, 1)."""
+    P*T), window (int64, P*T*2), status (int32, 1).  policy: POLICY_WINDOW
+    (Coop's sliding window) or POLICY_GREEDY (DTR's heuristic, one tensor at
+    a time)."""
 
-    def __init__(self, state, trace, workspace: Optional[torch.Tensor] = None):
+    def __init__(self, state, trace, workspace: Optional[torch.Tensor] = None,
+                 policy: int = 0):
         dev = state["size"].device
         if dev.type != "cuda":
             raise ValueError("coop replay runs on the GPU (there is no CPU fallback)")
@@ -281,7 +285,9 @@ class Replay:
             t = trace[k]
             if t.dtype != dt or t.numel() != P * T or not t.is_contiguous() or t.device != dev:
                 raise ValueError(f"trace[{k!r}] must be a contiguous {dt} tensor of {P * T}")
-        self.num_pools, self.capacity, self.num_ops = P, cap, T
+        if policy not in (POLICY_WINDOW, POLICY_GREEDY):
+            raise ValueError(f"unknown policy {policy}")
+        self.num_pools, self.capacity, self.num_ops, self.policy = P, cap, T, policy
         self.block = torch.empty(P * T, dtype=torch.int64, device=dev)
         self.window = torch.empty(P * T * 2, dtype=torch.int64, device=dev)
         self.cost = torch.empty(P * T, dtype=torch.int64, device=dev)
@@ -298,7 +304,7 @@ class Replay:
                       state["id"].data_ptr(), state["len"].data_ptr(), P, cap,
                       trace["op"].data_ptr(), trace["op_id"].data_ptr(),
                       trace["op_size"].data_ptr(), trace["op_cost"].data_ptr(),
-                      trace["op_flags"].data_ptr(), T, self.block.data_ptr(),
+                      trace["op_flags"].data_ptr(), T, policy, self.block.data_ptr(),
                       self.window.data_ptr(), self.cost.data_ptr(), self.free.data_ptr(),
                       self.status.data_ptr(), workspace.data_ptr(),
                       workspace.numel() * workspace.element_size())
@@ -341,6 +347,7 @@ def to_device(pools, device="cuda"):
 
 
 __all__ = ["COOP_EVICTABLE", "COOP_FREE", "COOP_PINNED", "CoopError", "FirstFit",
-           "INFEASIBLE", "LIBRARY", "Replay", "WindowSearch", "first_fit",
-           "first_fit_workspace_size", "load_library", "plan_info", "replay_to_device",
-           "replay_workspace_size", "to_device", "window_search", "workspace_size"]
+           "INFEASIBLE", "LIBRARY", "POLICY_GREEDY", "POLICY_WINDOW", "Replay", "WindowSearch",
+           "first_fit", "first_fit_workspace_size", "load_library", "plan_info",
+           "replay_to_device", "replay_workspace_size", "to_device", "window_search",
+           "workspace_size"]

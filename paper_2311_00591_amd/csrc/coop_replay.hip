@@ -23,6 +23,13 @@
 // evicted window and its cost, and for an eviction the pool's free bytes
 // just before it (the fragmentation-rate sample: free memory over the
 // memory the allocator holds).
+//
+// The greedy policy replaces steps 2-3 and the window eviction by the
+// baseline Coop is measured against (DTR's heuristic, restated in section
+// 3.3): while no chunk fits, evict the evictable tensor of least
+// h = c / (m * s) (cost over size times staleness) and merge its block with
+// free neighbours.  The update then records the number of tensors evicted
+// and their summed cost instead of a window.
 
 #include <hip/hip_runtime.h>
 
@@ -37,6 +44,86 @@ constexpr uint64_t kNone = ~0ull;
 constexpr uint8_t kOpAlloc = 0, kOpFree = 1;
 constexpr uint8_t kFlagLeft = 1, kFlagPinned = 2;
 constexpr uint32_t kErrCapacity = 1, kErrOperation = 2;
+
+// ---------------------------------------------------------------------------
+// Greedy victim choice.  h_a < h_b iff c_a * m_b * s_b < c_b * m_a * s_a;
+// both sides are products of two u64 and a u32 (below 2^160), compared
+// exactly in three words.  A zero size or staleness counts as 1.  Ties go to
+// the lower block index, which makes the choice unique, so any reduction
+// order gives the same victim.
+// ---------------------------------------------------------------------------
+struct Prod {
+    uint64_t lo, mid, hi;
+};
+
+__device__ __forceinline__ Prod mul3(uint64_t c, uint64_t m, uint32_t st) {
+    const uint64_t cm_lo = c * m, cm_hi = __umul64hi(c, m);
+    // (cm_hi * 2^64 + cm_lo) * st
+    const uint64_t a_lo = cm_lo * st, a_hi = __umul64hi(cm_lo, st);
+    const uint64_t b_lo = cm_hi * st, b_hi = __umul64hi(cm_hi, st);
+    const uint64_t mid = a_hi + b_lo;
+    return Prod{a_lo, mid, b_hi + (mid < a_hi ? 1u : 0u)};
+}
+
+__device__ __forceinline__ bool prod_less(const Prod& a, const Prod& b) {
+    if (a.hi != b.hi) return a.hi < b.hi;
+    if (a.mid != b.mid) return a.mid < b.mid;
+    return a.lo < b.lo;
+}
+
+struct Victim {
+    uint64_t c, m;  // cost, size (at least 1)
+    uint32_t s, j;  // staleness (at least 1), block index; j == ~0u: none
+};
+
+__device__ __forceinline__ bool victim_less(const Victim& a, const Victim& b) {
+    if (b.j == ~0u) return a.j != ~0u;
+    if (a.j == ~0u) return false;
+    const Prod pa = mul3(a.c, b.m, b.s), pb = mul3(b.c, a.m, a.s);
+    if (prod_less(pa, pb)) return true;
+    if (prod_less(pb, pa)) return false;
+    return a.j < b.j;
+}
+
+__device__ __forceinline__ Victim shfl_xor_victim(const Victim& v, int o) {
+    Victim x;
+    x.c = (static_cast<uint64_t>(__shfl_xor(static_cast<uint32_t>(v.c >> 32), o, 64)) << 32) |
+          __shfl_xor(static_cast<uint32_t>(v.c), o, 64);
+    x.m = (static_cast<uint64_t>(__shfl_xor(static_cast<uint32_t>(v.m >> 32), o, 64)) << 32) |
+          __shfl_xor(static_cast<uint32_t>(v.m), o, 64);
+    x.s = __shfl_xor(v.s, o, 64);
+    x.j = __shfl_xor(v.j, o, 64);
+    return x;
+}
+
+// The evictable block of least h among blocks [0, n) for operation id oid
+// (staleness oid - id, modulo 2^32), or ~0u.  The arrays may live in LDS or
+// global memory; every thread of the 256-thread workgroup calls it and gets
+// the same answer.  vred holds 4 entries.
+__device__ __forceinline__ uint32_t greedy_victim(const uint64_t* sz, const uint64_t* co,
+                                                  const uint8_t* kd, const uint32_t* id,
+                                                  uint64_t n, uint32_t oid, Victim* vred) {
+    const uint32_t tid = threadIdx.x;
+    Victim best{0, 1, 1, ~0u};
+    for (uint64_t k = tid; k < n; k += 256) {
+        if (kd[k] != COOP_EVICTABLE) continue;
+        const uint64_t m = sz[k];
+        const uint32_t st = oid - id[k];
+        const Victim v{co[k], m ? m : 1, st ? st : 1u, static_cast<uint32_t>(k)};
+        if (victim_less(v, best)) best = v;
+    }
+    for (int o = 32; o >= 1; o >>= 1) {
+        const Victim x = shfl_xor_victim(best, o);
+        if (victim_less(x, best)) best = x;
+    }
+    if ((tid & 63u) == 0) vred[tid >> 6] = best;
+    __syncthreads();
+    Victim m = vred[0];
+    for (uint32_t w = 1; w < 4; ++w)
+        if (victim_less(vred[w], m)) m = vred[w];
+    __syncthreads();
+    return m.j;
+}
 
 // Sets the fixed batch layout (pool b is slots [b * cap, (b + 1) * cap) and
 // owns request b) and the requests of the first operation.
@@ -144,10 +231,11 @@ __device__ void pool_replace(Pool p, uint64_t len, uint64_t lo, uint64_t hi, uin
 __global__ __launch_bounds__(kThreads) void replay_update_kernel(
     uint64_t* size, uint64_t* cost, uint8_t* kind, uint32_t* id, uint64_t* len, uint64_t cap,
     const uint8_t* op, const uint32_t* op_id, const uint64_t* op_size, const uint64_t* op_cost,
-    const uint8_t* op_flags, uint64_t num_ops, uint64_t t, const uint64_t* ff,
+    const uint8_t* op_flags, uint64_t num_ops, uint64_t t, int32_t policy, const uint64_t* ff,
     const coop_window_t* win, uint64_t* req_ff, uint64_t* out_block, uint64_t* out_window,
     uint64_t* out_cost, uint64_t* out_free, uint32_t* status) {
     __shared__ uint64_t red[kThreads / 64];
+    __shared__ Victim vred[kThreads / 64];
     __shared__ uint64_t found;
     const uint32_t tid = threadIdx.x;
     const uint64_t b = blockIdx.x;
@@ -182,7 +270,37 @@ __global__ __launch_bounds__(kThreads) void replay_update_kernel(
         const uint64_t S = op_size[o];
         uint64_t k = ff[b];
         bool ok = true;
-        if (k == kNone) {
+        if (k == kNone && policy == COOP_POLICY_GREEDY) {
+            uint64_t fb = 0;
+            for (uint64_t j = tid; j < n; j += kThreads)
+                if (p.kind[j] == COOP_FREE) fb += p.size[j];
+            const uint64_t free0 = block_sum(fb, red);
+            uint64_t count = 0, evc = 0;
+            while (k == kNone) {
+                const uint32_t v = greedy_victim(p.size, p.cost, p.kind, p.id, nl, op_id[o], vred);
+                if (v == ~0u) break;
+                ++count;
+                evc += p.cost[v];
+                const uint64_t lo = v > 0 && p.kind[v - 1] == COOP_FREE ? v - 1 : v;
+                const uint64_t hi = v + 1 < nl && p.kind[v + 1] == COOP_FREE ? v + 2 : v + 1;
+                uint64_t total = 0;
+                for (uint64_t j = lo; j < hi; ++j) total += p.size[j];
+                __syncthreads();
+                const uint64_t ns[1] = {total}, nc[1] = {0};
+                const uint8_t nk[1] = {COOP_FREE};
+                const uint32_t ni[1] = {0};
+                pool_replace(p, nl, lo, hi, 1, ns, nc, nk, ni);
+                nl = nl - (hi - lo) + 1;
+                // no chunk held S bytes before, so only the merged one can now
+                if (total >= S) k = lo;
+            }
+            if (count) {
+                r_free = free0;
+                r_w0 = count;
+                r_cost = evc;
+            }
+            ok = k != kNone;  // out of evictable tensors: fails, evictions stay
+        } else if (k == kNone) {
             const coop_window_t w = win[b];
             if (w.start == kNone) {
                 ok = false;  // no window: the allocation fails, nothing changes
@@ -271,9 +389,9 @@ __global__ __launch_bounds__(kThreads) void replay_update_kernel(
 constexpr uint32_t kResThreads = 256;
 constexpr uint32_t kResWaves = kResThreads / 64;
 
-// LDS bytes per pool slot: size, cost, prefix bytes and cost (u64), tensor id
-// (u32), pinned-count prefix (u16), kind (u8); plus one prefix entry.
-constexpr size_t kResSlotBytes = 8 + 8 + 8 + 8 + 4 + 2 + 1;
+// LDS bytes for a pool of cap slots, 39 a slot: size, cost, prefix bytes and
+// cost (u64), tensor id (u32), pinned-count prefix (u16), kind (u8); plus one
+// prefix entry and padding to 8 bytes.
 __host__ __device__ constexpr size_t resident_lds_bytes(uint64_t cap) {
     return ((cap * 8 + 7) & ~7ull) * 2 + ((cap + 1) * 8) * 2 + ((cap * 4 + 7) & ~7ull) +
            (((cap + 1) * 2 + 7) & ~7ull) + ((cap + 7) & ~7ull);
@@ -468,11 +586,12 @@ __device__ WinKey res_window(const Lds& l, uint64_t n, uint64_t S, uint64_t* red
 __global__ __launch_bounds__(kResThreads) void replay_resident_kernel(
     uint64_t* size, uint64_t* cost, uint8_t* kind, uint32_t* id, uint64_t* len, uint64_t cap,
     const uint8_t* op, const uint32_t* op_id, const uint64_t* op_size, const uint64_t* op_cost,
-    const uint8_t* op_flags, uint64_t num_ops, uint64_t* out_block, uint64_t* out_window,
-    uint64_t* out_cost, uint64_t* out_free, uint32_t* status) {
+    const uint8_t* op_flags, uint64_t num_ops, int32_t policy, uint64_t* out_block,
+    uint64_t* out_window, uint64_t* out_cost, uint64_t* out_free, uint32_t* status) {
     extern __shared__ __align__(16) char lds_raw[];
     __shared__ uint64_t red[kResWaves];
     __shared__ WinKey wred[kResWaves];
+    __shared__ Victim vred[kResWaves];
     __shared__ uint32_t hit;
     const uint32_t tid = threadIdx.x;
     const uint64_t b = blockIdx.x;
@@ -520,7 +639,37 @@ __global__ __launch_bounds__(kResThreads) void replay_resident_kernel(
             }
             uint64_t k = res_min(mine, red);
             bool ok = true;
-            if (k == kNone) {
+            if (k == kNone && policy == COOP_POLICY_GREEDY) {
+                uint64_t fb = 0;
+                for (uint64_t j = tid; j < n; j += kResThreads)
+                    if (l.kd[j] == COOP_FREE) fb += l.sz[j];
+                const uint64_t free0 = res_sum(fb, red);
+                uint64_t count = 0, evc = 0;
+                while (k == kNone) {
+                    const uint32_t v = greedy_victim(l.sz, l.co, l.kd, l.id, n, oid, vred);
+                    if (v == ~0u) break;
+                    ++count;
+                    evc += l.co[v];
+                    const uint64_t lo = v > 0 && l.kd[v - 1] == COOP_FREE ? v - 1 : v;
+                    const uint64_t hi = v + 1 < n && l.kd[v + 1] == COOP_FREE ? v + 2 : v + 1;
+                    uint64_t total = 0;
+                    for (uint64_t j = lo; j < hi; ++j) total += l.sz[j];
+                    __syncthreads();
+                    const uint64_t ns[1] = {total}, nc[1] = {0};
+                    const uint8_t nk[1] = {COOP_FREE};
+                    const uint32_t ni[1] = {0};
+                    res_replace(l, n, lo, hi, 1, ns, nc, nk, ni);
+                    n = n - (hi - lo) + 1;
+                    // no chunk held S bytes before, so only the merged one can now
+                    if (total >= S) k = lo;
+                }
+                if (count) {
+                    r_free = free0;
+                    r_w0 = count;
+                    r_cost = evc;
+                }
+                ok = k != kNone;  // out of evictable tensors: fails, evictions stay
+            } else if (k == kNone) {
                 const WinKey wk = res_window(l, n, S, red, wred);
                 if (wk.start == kNone) {
                     ok = false;  // no window: the allocation fails, nothing changes
@@ -645,10 +794,11 @@ coop_status_t coop_replay_workspace_size(uint64_t num_pools, uint64_t capacity, 
 coop_status_t coop_replay(uint64_t* size, uint64_t* cost, uint8_t* kind, uint32_t* id,
                           uint64_t* len, uint64_t num_pools, uint64_t capacity, const uint8_t* op,
                           const uint32_t* op_id, const uint64_t* op_size, const uint64_t* op_cost,
-                          const uint8_t* op_flags, uint64_t num_ops, uint64_t* out_block,
-                          uint64_t* out_window, uint64_t* out_cost, uint64_t* out_free,
-                          uint32_t* status_out, void* workspace, size_t workspace_bytes,
-                          void* stream) {
+                          const uint8_t* op_flags, uint64_t num_ops, int32_t policy,
+                          uint64_t* out_block, uint64_t* out_window, uint64_t* out_cost,
+                          uint64_t* out_free, uint32_t* status_out, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+    if (policy != COOP_POLICY_WINDOW && policy != COOP_POLICY_GREEDY) return COOP_ERR_INVALID;
     if (num_pools == 0 || num_ops == 0) return COOP_OK;
     if (!size || !cost || !kind || !id || !len || !op || !op_id || !op_size || !op_cost ||
         !op_flags || !out_block || !out_window || !out_cost || !out_free || !status_out)
@@ -669,8 +819,8 @@ coop_status_t coop_replay(uint64_t* size, uint64_t* cost, uint8_t* kind, uint32_
             return COOP_ERR_HIP;
         hipLaunchKernelGGL(replay_resident_kernel, dim3(static_cast<uint32_t>(num_pools)),
                            dim3(kResThreads), res_lds, s0, size, cost, kind, id, len, capacity, op,
-                           op_id, op_size, op_cost, op_flags, num_ops, out_block, out_window,
-                           out_cost, out_free, status_out);
+                           op_id, op_size, op_cost, op_flags, num_ops, policy, out_block,
+                           out_window, out_cost, out_free, status_out);
         if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
         return COOP_OK;
     }
@@ -692,16 +842,18 @@ coop_status_t coop_replay(uint64_t* size, uint64_t* cost, uint8_t* kind, uint32_
         coop_status_t rc = coop_first_fit(size, kind, nb, seg, num_pools, req_ff, req_off, num_pools,
                                           ff, w + l.ff_ws, l.ff_ws_bytes, stream);
         if (rc != COOP_OK) return rc;
-        hipLaunchKernelGGL(replay_gate_kernel, dim3(small), dim3(256), 0, s, num_pools, req_ff, ff,
-                           req_win);
-        if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
-        rc = coop_window_search(size, cost, kind, nb, seg, num_pools, req_win, req_off, num_pools,
-                                win, w + l.win_ws, l.win_ws_bytes, stream);
-        if (rc != COOP_OK) return rc;
+        if (policy == COOP_POLICY_WINDOW) {
+            hipLaunchKernelGGL(replay_gate_kernel, dim3(small), dim3(256), 0, s, num_pools, req_ff,
+                               ff, req_win);
+            if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
+            rc = coop_window_search(size, cost, kind, nb, seg, num_pools, req_win, req_off,
+                                    num_pools, win, w + l.win_ws, l.win_ws_bytes, stream);
+            if (rc != COOP_OK) return rc;
+        }
         hipLaunchKernelGGL(replay_update_kernel, dim3(static_cast<uint32_t>(num_pools)),
                            dim3(kThreads), 0, s, size, cost, kind, id, len, capacity, op, op_id,
-                           op_size, op_cost, op_flags, num_ops, t, ff, win, req_ff, out_block,
-                           out_window, out_cost, out_free, status);
+                           op_size, op_cost, op_flags, num_ops, t, policy, ff, win, req_ff,
+                           out_block, out_window, out_cost, out_free, status);
         if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
     }
     return COOP_OK;

@@ -54,3 +54,31 @@ def parse_golden(path):
 @pytest.fixture(scope="session")
 def golden_examples():
     return parse_golden(os.path.join(GOLDEN, "window_examples.txt"))
+
+
+def parse_greedy_golden(path):
+    """Parses tests/golden/greedy_examples.txt into a list of cases
+    {"name", "pool": [(kind, bytes, id, cost)], "steps": [{"op", "expect",
+    "after": [(kind, bytes, id)]}]}; sizes in the file are MiB."""
+    kinds, mib = {"F": 0, "E": 1, "P": 2}, 1 << 20
+    cases, cur, step = [], None, None
+    with open(path) as f:
+        for raw in f:
+            line = raw.split("#", 1)[0].strip()
+            if not line:
+                continue
+            tok = line.split()
+            if tok[0] == "case":
+                cur = {"name": tok[1], "pool": [], "steps": []}
+                cases.append(cur)
+            elif tok[0] == "pool":
+                cur["pool"].append((kinds[tok[1]], int(tok[2]) * mib, int(tok[3]), int(tok[4])))
+            elif tok[0] == "op":
+                step = {"op": tok[1:]}
+                cur["steps"].append(step)
+            elif tok[0] == "expect":
+                step["expect"] = tok[1:]
+            elif tok[0] == "after":
+                step["after"] = [(kinds[k], int(s) * mib, int(i)) for k, s, i in
+                                 (p.split() for p in line[len("after"):].split("|"))]
+    return cases

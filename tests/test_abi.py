@@ -111,3 +111,23 @@ def test_plan_queue_and_partial_slots():
     assert p["chunks_max"] == p["workgroups"]
     lib = coop.load_library()
     assert lib.coop_window_search_plan(1, 1, 1, None) == -1
+
+
+def test_replay_rejects_unknown_policy_and_null_buffers():
+    # validation happens before any launch, so no GPU is touched
+    lib = coop.load_library()
+    nz = 16  # non-null, never dereferenced
+    bufs = [nz] * 5
+
+    def call(policy, P=1, T=1, ptr=nz):
+        return lib.coop_replay(*bufs, P, 8, ptr, nz, nz, nz, nz, T, policy, nz, nz, nz, nz, nz,
+                               nz, 1 << 20, None)
+
+    assert call(2) == -1
+    assert call(-1) == -1
+    assert call(2, P=0) == -1          # the policy is checked even for an empty batch
+    assert call(coop.POLICY_GREEDY, P=0) == 0
+    assert call(coop.POLICY_WINDOW, T=0) == 0
+    assert call(coop.POLICY_GREEDY, ptr=None) == -1
+    assert lib.coop_replay(*bufs, 1, 8, nz, nz, nz, nz, nz, 1, 1, nz, nz, nz, nz, nz, nz, 1,
+                           None) == -2  # workspace too small

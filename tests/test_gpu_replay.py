@@ -1,12 +1,14 @@
 """GPU replay of Algorithm 1 (coop_replay) equals the CPU oracle's replay:
 every operation's outcome (block, evicted window, its cost, the free-bytes
-sample) and the final pools, slot for slot, through the C ABI."""
+sample) and the final pools, slot for slot, through the C ABI -- under
+Coop's sliding-window eviction and under the DTR-style greedy baseline."""
 import sys
 
 import numpy as np
 import pytest
 
 import oracle
+from conftest import GOLDEN, parse_greedy_golden
 from workloads import traces
 
 torch = pytest.importorskip("torch")
@@ -14,6 +16,7 @@ pytestmark = pytest.mark.gpu
 
 U64MAX = (1 << 64) - 1
 MiB = 1 << 20
+WINDOW, GREEDY = 0, 1
 
 
 def _announce(label):
@@ -21,10 +24,10 @@ def _announce(label):
     sys.stdout.flush()
 
 
-def gpu_replay(state, trace):
+def gpu_replay(state, trace, policy=WINDOW):
     import paper_2311_00591_amd as coop
     st, tr = coop.replay_to_device(state, trace)
-    r = coop.Replay(st, tr)
+    r = coop.Replay(st, tr, policy=policy)
     r.launch()
     torch.cuda.synchronize()
     P, T = r.num_pools, r.num_ops
@@ -39,9 +42,9 @@ def gpu_replay(state, trace):
     return state_after, outs, int(r.status.item())
 
 
-def assert_same(state, trace, label):
-    want_state, want = oracle.replay(state, trace, threads=8)
-    got_state, got, status = gpu_replay(state, trace)
+def assert_same(state, trace, label, policy=WINDOW):
+    want_state, want = oracle.replay(state, trace, threads=8, policy=policy)
+    got_state, got, status = gpu_replay(state, trace, policy)
     assert status == 0, f"{label}: status {status}"
     for k in ("block", "window", "cost", "free"):
         bad = np.argwhere(got[k] != want[k])
@@ -61,11 +64,62 @@ def assert_same(state, trace, label):
         assert (got_state["size"][rest] == 0).all() and (got_state["kind"][rest] == 2).all()
 
 
+@pytest.mark.parametrize("policy", [WINDOW, GREEDY])
 @pytest.mark.parametrize("k,seed", [(0, 0), (0, 1), (1, 0), (1, 2)])
-def test_generated_traces(k, seed):
-    _announce(f"config {k} seed {seed}")
+def test_generated_traces(k, seed, policy):
+    _announce(f"config {k} seed {seed} policy {policy}")
     state, trace = traces.make_replay(k, seed)
-    assert_same(state, trace, f"config {k} seed {seed}")
+    assert_same(state, trace, f"config {k} seed {seed} policy {policy}", policy)
+
+
+@pytest.mark.parametrize("policy", [WINDOW, GREEDY])
+def test_training_replay_full_size(policy):
+    """The training-replay workload the benchmark times (512 pools of 1024
+    operations), whole."""
+    _announce(f"training replay, policy {policy}")
+    state, trace = traces.make_replay(2, 0)
+    assert_same(state, trace, f"training policy {policy}", policy)
+
+
+def test_greedy_worked_replays():
+    """The hand-derived cases of tests/golden/greedy_examples.txt, each pool
+    replayed on the GPU."""
+    import os
+    cases = parse_greedy_golden(os.path.join(GOLDEN, "greedy_examples.txt"))
+    for case in cases:
+        _announce(f"greedy worked case {case['name']}")
+        cap = 16
+        state = {"size": np.zeros(cap, np.uint64), "cost": np.zeros(cap, np.uint64),
+                 "kind": np.full(cap, 2, np.uint8), "id": np.zeros(cap, np.uint32),
+                 "len": np.array([len(case["pool"])], np.uint64), "capacity": cap}
+        for j, (kd, sz, i, c) in enumerate(case["pool"]):
+            state["kind"][j], state["size"][j], state["id"][j], state["cost"][j] = kd, sz, i, c
+        for stp in case["steps"]:
+            o = stp["op"]
+            trace = {"op": np.zeros(1, np.uint8), "op_id": np.array([int(o[1])]),
+                     "op_size": np.array([int(o[2]) * MiB], np.uint64),
+                     "op_cost": np.array([int(o[3])], np.uint64),
+                     "op_flags": np.array([1 if o[4] == "left" else 0], np.uint8)}
+            new_state, got, status = gpu_replay(state, trace, GREEDY)
+            assert status == 0
+            e = stp["expect"]
+            assert int(got["block"][0, 0]) == (U64MAX if e[0] == "none" else int(e[0])), o
+            assert got["window"][0, 0].tolist() == [int(e[2]), U64MAX], o
+            assert int(got["cost"][0, 0]) == int(e[3]), o
+            assert int(got["free"][0, 0]) == int(e[4]) * MiB, o
+            n = int(new_state["len"][0])
+            blocks = [(int(new_state["kind"][j]), int(new_state["size"][j]),
+                       int(new_state["id"][j])) for j in range(n)]
+            assert blocks == stp["after"], (case["name"], o, blocks)
+            state = new_state
+
+
+def test_unknown_policy_is_rejected():
+    import paper_2311_00591_amd as coop
+    state, trace = traces.make_replay(0, 0)
+    st, tr = coop.replay_to_device(state, trace)
+    with pytest.raises(ValueError):
+        coop.Replay(st, tr, policy=2)
 
 
 def test_resnet_pattern_tight_budget():
@@ -115,13 +169,14 @@ def test_out_of_slots_is_reported():
     assert int(got_state["len"][0]) == 3
 
 
-def test_pools_too_large_for_lds_take_the_stepwise_path():
+@pytest.mark.parametrize("policy", [WINDOW, GREEDY])
+def test_pools_too_large_for_lds_take_the_stepwise_path(policy):
     """Capacity beyond what one workgroup's LDS holds: the replay runs one
     step per operation with the batched first-fit and window kernels."""
-    _announce("stepwise path")
+    _announce(f"stepwise path, policy {policy}")
     import paper_2311_00591_amd as coop
     state, trace = traces.make_replay(1, 7, layers=2200, num_pools=6, iterations=1,
                                       budget_frac=0.9)
     # 39 bytes of LDS per slot (pool, prefix sums, ids, run counts): above 160 KiB
     assert state["capacity"] * 39 > 160 * 1024
-    assert_same(state, trace, "stepwise")
+    assert_same(state, trace, f"stepwise policy {policy}", policy)

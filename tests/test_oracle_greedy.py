@@ -17,13 +17,13 @@ import numpy as np
 import pytest
 
 import oracle
+from conftest import parse_greedy_golden
 from workloads import traces
 
 U64MAX = (1 << 64) - 1
 MiB = 1 << 20
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
                       "greedy_examples.txt")
-KIND = {"F": 0, "E": 1, "P": 2}
 GREEDY = 1
 
 
@@ -44,31 +44,8 @@ def _blocks(st):
             for j in range(n)]
 
 
-def _cases():
-    cases, cur, step = [], None, None
-    for raw in open(GOLDEN):
-        line = raw.split("#", 1)[0].strip()
-        if not line:
-            continue
-        tok = line.split()
-        if tok[0] == "case":
-            cur = {"name": tok[1], "pool": [], "steps": []}
-            cases.append(cur)
-        elif tok[0] == "pool":
-            cur["pool"].append((KIND[tok[1]], int(tok[2]) * MiB, int(tok[3]), int(tok[4])))
-        elif tok[0] == "op":
-            step = {"op": tok[1:]}
-            cur["steps"].append(step)
-        elif tok[0] == "expect":
-            step["expect"] = tok[1:]
-        elif tok[0] == "after":
-            step["after"] = [(KIND[k], int(s) * MiB, int(i)) for k, s, i in
-                             (p.split() for p in line[len("after"):].split("|"))]
-    return cases
-
-
 def test_golden_greedy():
-    cases = _cases()
+    cases = parse_greedy_golden(GOLDEN)
     assert len(cases) >= 6
     for case in cases:
         st = _state(case["pool"], 16)
