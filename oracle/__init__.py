@@ -19,7 +19,8 @@ from . import build as _build
 INFEASIBLE = np.uint64(0xFFFFFFFFFFFFFFFF)
 
 _ERRORS = {-1: "invalid arguments", -4: "a run total overflows 64 bits",
-           -5: "input too large for brute force"}
+           -5: "input too large for brute force",
+           -6: "a heuristic value is NaN, negative or at least 2^64"}
 
 _lib = None
 
@@ -45,8 +46,13 @@ def _load():
         lib.coop_oracle_brute_eq1.argtypes = common
         lib.coop_oracle_first_fit.argtypes = [p64, p8, ctypes.c_uint64, p64, ctypes.c_uint64,
                                               p64, p64, ctypes.c_uint64, p64, ctypes.c_int]
+        pd = ctypes.POINTER(ctypes.c_double)
+        lib.coop_oracle_window_search_real.argtypes = [p64, pd, p8, ctypes.c_uint64, p64,
+                                                       ctypes.c_uint64, p64, p64,
+                                                       ctypes.c_uint64, p64, pd, ctypes.c_int]
         for f in (lib.coop_oracle_window_search, lib.coop_oracle_brute_windows,
-                  lib.coop_oracle_brute_eq1, lib.coop_oracle_first_fit):
+                  lib.coop_oracle_brute_eq1, lib.coop_oracle_first_fit,
+                  lib.coop_oracle_window_search_real):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -84,6 +90,23 @@ def window_search(size, cost, kind, seg_offsets, req_sizes, req_offsets, threads
     if rc != 0:
         raise OracleError(rc)
     return out
+
+
+def window_search_real(size, h, kind, seg_offsets, req_sizes, req_offsets, threads=1):
+    """The search with real-valued heuristics h (float64, see coop_oracle.h).
+    Returns (uint64 (Q, 4) = (start, end, exact cost low, high words in units
+    of 2^-64), float64 (Q,) = the exact cost rounded to nearest)."""
+    h = np.ascontiguousarray(h, dtype=np.float64)
+    keep, cargs = _args(size, np.zeros(len(h), np.uint64), kind, seg_offsets, req_sizes,
+                        req_offsets)
+    cargs[1] = _ptr(h, ctypes.c_double)
+    out = np.empty((len(keep[4]), 4), dtype=np.uint64)
+    cost = np.empty(len(keep[4]), dtype=np.float64)
+    rc = _load().coop_oracle_window_search_real(*cargs, _ptr(out, ctypes.c_uint64),
+                                                _ptr(cost, ctypes.c_double), int(threads))
+    if rc != 0:
+        raise OracleError(rc)
+    return out, cost
 
 
 def brute_windows(size, cost, kind, seg_offsets, req_sizes, req_offsets):

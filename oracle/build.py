@@ -16,7 +16,7 @@ def build(verbose: bool = False) -> str:
     """Always recompiles; returns the path of the shared library."""
     tmp = LIBRARY + ".tmp"
     cmd = ["gcc", "-std=c11", "-O2", "-Wall", "-Wextra", "-Werror", "-fPIC", "-shared",
-           "-pthread", "-o", tmp, SOURCE]
+           "-pthread", "-o", tmp, SOURCE, "-lm"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)

@@ -10,6 +10,7 @@
  */
 #include "coop_oracle.h"
 
+#include <math.h>
 #include <pthread.h>
 #include <stdatomic.h>
 #include <stdlib.h>
@@ -189,6 +190,174 @@ int coop_oracle_window_search(const uint64_t *size, const uint64_t *cost,
     if (started == 0) sweep_worker(&job);
     for (int t = 0; t < started; ++t) pthread_join(tid[t], NULL);
     free(tid);
+    return COOP_ORACLE_OK;
+}
+
+/* ---------------------------------------------------------------------------
+ * Real-valued heuristic.  Section 3.3 defines a tensor's heuristic as
+ * h(t) = c(t) / s(t), projected cost over staleness: a real number.  Here
+ * each evictable block carries h as a binary64 value and a window costs the
+ * exact real sum of its h values, so that no summation order can change
+ * which window wins.  To add exactly, each h becomes a 128-bit fixed-point
+ * number with 64 fraction bits (Q64.64), rounded to the nearest multiple of
+ * 2^-64, ties to even.  That rounding is exact for every h >= 2^-12, whose
+ * binary64 spacing is at least 2^-64.  h must be finite, >= 0 and < 2^64;
+ * the stored h of free and pinned blocks is ignored.  Each run's total must
+ * stay below 2^64 (its fixed-point sum fits 128 bits).
+ * ------------------------------------------------------------------------- */
+typedef unsigned __int128 u128;
+
+#define U128_NONE (~(u128)0)
+
+/* h to Q64.64: 2^64 * h is exact in binary64 (a power-of-two scaling well
+ * inside the exponent range); nearbyint rounds it to an integer under the
+ * default rounding mode, to nearest with ties to even; that integer (below
+ * 2^128, at most 53 significant bits) is split into two exact halves. */
+static int real_to_q(double h, u128 *q) {
+    if (!(h >= 0.0) || !(h < 0x1p64)) return 0;
+    const double x = nearbyint(ldexp(h, 64));
+    const double hi = floor(ldexp(x, -64));
+    const double lo = x - ldexp(hi, 64);
+    *q = ((u128)(uint64_t)hi << 64) | (u128)(uint64_t)lo;
+    return 1;
+}
+
+/* Q64.64 to the nearest binary64, ties to even: the compiler's unsigned
+ * 128-bit conversion rounds to nearest, and the scaling by 2^-64 is exact. */
+static double q_to_real(u128 q) { return ldexp((double)q, -64); }
+
+static u128 real_cost(uint8_t k, u128 q) { return k == KIND_EVICTABLE ? q : 0; }
+
+static int key_less_real(u128 c1, uint64_t b1, uint64_t s1, u128 c2, uint64_t b2,
+                         uint64_t s2) {
+    if (c1 != c2) return c1 < c2;
+    if (b1 != b2) return b1 < b2;
+    return s1 < s2;
+}
+
+/* The same linear sweep as above, on fixed-point costs. */
+static void sweep_one_real(const uint64_t *size, const u128 *q, const uint8_t *kind,
+                           uint64_t n, uint64_t S, uint64_t res[4], double *res_cost) {
+    res[0] = res[1] = res[2] = res[3] = NONE;
+    *res_cost = INFINITY;
+    if (S == 0) {
+        res[0] = res[1] = res[2] = res[3] = 0;
+        *res_cost = 0.0;
+        return;
+    }
+    int found = 0;
+    u128 best_c = 0;
+    uint64_t best_b = 0, best_s = 0, best_e = 0;
+    uint64_t i = 0;
+    while (i < n) {
+        if (is_pinned(kind[i])) { ++i; continue; }
+        uint64_t r = i;
+        while (r < n && !is_pinned(kind[r])) ++r;
+        uint64_t e = i, bytes = 0;
+        u128 c = 0;
+        for (uint64_t st = i; st < r; ++st) {
+            while (e < r && bytes < S) {
+                bytes += size[e];
+                c += real_cost(kind[e], q[e]);
+                ++e;
+            }
+            if (bytes < S) break;
+            if (!found || key_less_real(c, bytes, st, best_c, best_b, best_s)) {
+                found = 1;
+                best_c = c; best_b = bytes; best_s = st; best_e = e;
+            }
+            bytes -= size[st];
+            c -= real_cost(kind[st], q[st]);
+        }
+        i = r;
+    }
+    if (found) {
+        res[0] = best_s;
+        res[1] = best_e;
+        res[2] = (uint64_t)best_c;
+        res[3] = (uint64_t)(best_c >> 64);
+        *res_cost = q_to_real(best_c);
+    }
+}
+
+struct real_job {
+    const uint64_t *size;
+    const u128 *q;
+    const uint8_t *kind;
+    const uint64_t *seg_offsets, *req_sizes, *req_offsets;
+    uint64_t num_segments, num_requests;
+    uint64_t *out;
+    double *out_cost;
+    _Atomic uint64_t next;
+};
+
+static void *real_worker(void *arg) {
+    struct real_job *job = (struct real_job *)arg;
+    for (;;) {
+        uint64_t q0 = atomic_fetch_add(&job->next, SWEEP_CHUNK);
+        if (q0 >= job->num_requests) break;
+        uint64_t q1 = q0 + SWEEP_CHUNK < job->num_requests ? q0 + SWEEP_CHUNK
+                                                           : job->num_requests;
+        for (uint64_t r = q0; r < q1; ++r) {
+            uint64_t b = owner_segment(job->req_offsets, job->num_segments, r);
+            uint64_t s0 = job->seg_offsets[b], n = job->seg_offsets[b + 1] - s0;
+            sweep_one_real(job->size + s0, job->q + s0, job->kind + s0, n, job->req_sizes[r],
+                           job->out + 4 * r, job->out_cost + r);
+        }
+    }
+    return NULL;
+}
+
+int coop_oracle_window_search_real(const uint64_t *size, const double *h, const uint8_t *kind,
+                                   uint64_t num_blocks, const uint64_t *seg_offsets,
+                                   uint64_t num_segments, const uint64_t *req_sizes,
+                                   const uint64_t *req_offsets, uint64_t num_requests,
+                                   uint64_t *out, double *out_cost, int num_threads) {
+    if (!batch_ok(size, (const uint64_t *)h, kind, num_blocks, seg_offsets, num_segments,
+                  req_sizes, req_offsets, num_requests, out) ||
+        (num_requests && !out_cost))
+        return COOP_ORACLE_ERR_INVALID;
+    u128 *q = (u128 *)malloc((num_blocks ? num_blocks : 1) * sizeof(u128));
+    if (!q) return COOP_ORACLE_ERR_INVALID;
+    int rc = COOP_ORACLE_OK;
+    for (uint64_t k = 0; k < num_blocks && rc == COOP_ORACLE_OK; ++k) {
+        q[k] = 0;
+        if (kind[k] == KIND_EVICTABLE && !real_to_q(h[k], &q[k])) rc = COOP_ORACLE_ERR_VALUE;
+    }
+    /* every run's byte total below 2^64, its h total below 2^64 */
+    for (uint64_t b = 0; b < num_segments && rc == COOP_ORACLE_OK; ++b) {
+        uint64_t bytes = 0;
+        u128 c = 0;
+        for (uint64_t k = seg_offsets[b]; k < seg_offsets[b + 1]; ++k) {
+            if (is_pinned(kind[k])) { bytes = 0; c = 0; continue; }
+            if (__builtin_add_overflow(bytes, size[k], &bytes) ||
+                __builtin_add_overflow(c, q[k], &c)) {
+                rc = COOP_ORACLE_ERR_OVERFLOW;
+                break;
+            }
+        }
+    }
+    if (rc != COOP_ORACLE_OK || num_requests == 0) {
+        free(q);
+        return rc;
+    }
+    struct real_job job;
+    job.size = size; job.q = q; job.kind = kind;
+    job.seg_offsets = seg_offsets; job.req_sizes = req_sizes;
+    job.req_offsets = req_offsets; job.num_segments = num_segments;
+    job.num_requests = num_requests; job.out = out; job.out_cost = out_cost;
+    atomic_init(&job.next, 0);
+    pthread_t *tid = num_threads > 1 ? (pthread_t *)calloc((size_t)num_threads,
+                                                           sizeof(pthread_t)) : NULL;
+    int started = 0;
+    for (int t = 0; tid && t < num_threads; ++t) {
+        if (pthread_create(&tid[t], NULL, real_worker, &job) != 0) break;
+        ++started;
+    }
+    if (started == 0) real_worker(&job);
+    for (int t = 0; t < started; ++t) pthread_join(tid[t], NULL);
+    free(tid);
+    free(q);
     return COOP_ORACLE_OK;
 }
 

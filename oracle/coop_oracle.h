@@ -38,7 +38,8 @@
  *
  * Return codes: 0 ok, -1 invalid arguments, -4 a run's size or effective-cost
  * total does not fit in 64 bits (the precondition the GPU path relies on),
- * -5 input too large for a brute-force enumerator.
+ * -5 input too large for a brute-force enumerator, -6 an invalid real-valued
+ * heuristic.
  */
 #ifndef COOP_ORACLE_H
 #define COOP_ORACLE_H
@@ -53,6 +54,7 @@ extern "C" {
 #define COOP_ORACLE_ERR_INVALID (-1)
 #define COOP_ORACLE_ERR_OVERFLOW (-4)
 #define COOP_ORACLE_ERR_TOO_LARGE (-5)
+#define COOP_ORACLE_ERR_VALUE (-6)
 
 /* Linear two-pointer sweep per run (section 3.3), one request at a time,
  * requests spread over num_threads POSIX threads (<= 0 means 1). */
@@ -91,6 +93,23 @@ int coop_oracle_first_fit(const uint64_t *size, const uint8_t *kind, uint64_t nu
                           const uint64_t *seg_offsets, uint64_t num_segments,
                           const uint64_t *req_sizes, const uint64_t *req_offsets,
                           uint64_t num_requests, uint64_t *out, int num_threads);
+
+/* The search with real-valued heuristics (section 3.3: h = c / s).  h[k]
+ * (binary64) replaces cost[k]; a window costs the exact sum of its h values:
+ * each h is rounded to a multiple of 2^-64 (to nearest, ties to even; exact
+ * for h >= 2^-12) and summed in 128-bit fixed point, so the answer does not
+ * depend on any summation order.  Ranking and tie-breaks as above.  Per
+ * request out[4] = (start, end, low and high 64 bits of the exact sum in
+ * units of 2^-64) and out_cost = that sum rounded to the nearest binary64
+ * (ties to even).  S == 0: (0, 0, 0, 0) and 0.0; infeasible: all ~0 and
+ * +inf.  Returns -6 if an evictable block's h is NaN, negative or >= 2^64,
+ * -4 if a run's byte total or h total reaches 2^64.  Must run under the
+ * default floating-point rounding mode. */
+int coop_oracle_window_search_real(const uint64_t *size, const double *h, const uint8_t *kind,
+                                   uint64_t num_blocks, const uint64_t *seg_offsets,
+                                   uint64_t num_segments, const uint64_t *req_sizes,
+                                   const uint64_t *req_offsets, uint64_t num_requests,
+                                   uint64_t *out, double *out_cost, int num_threads);
 
 /* Replay of Algorithm 1 (allocate: first fit, else evict the sliding
  * window's tensors, merge the window into one free chunk and fit again;
