@@ -51,7 +51,7 @@ def parse():
     ap.add_argument("--policy", choices=["window", "greedy"], default="window",
                     help="replay eviction policy timed by --op replay: Coop's sliding window "
                          "or the DTR-style greedy baseline")
-    ap.add_argument("--op", choices=["window", "first_fit", "replay"], default="window",
+    ap.add_argument("--op", choices=["window", "first_fit", "replay", "real"], default="window",
                     help="window: the eviction-window search; first_fit: the free-chunk "
                          "lookup that precedes it; replay: Algorithm 1 over training traces "
                          "(--config picks the trace set)")
@@ -99,7 +99,7 @@ def measured_traffic(workload_name):
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(pools, target_s, op="window"):
+def cpu_baseline(pools, target_s, op="window", h=None):
     import oracle
     try:
         threads = len(os.sched_getaffinity(0))
@@ -109,6 +109,9 @@ def cpu_baseline(pools, target_s, op="window"):
     if op == "window":
         args = pools.arrays()
         fn, what = oracle.window_search, "two-pointer sweep"
+    elif op == "real":
+        args = (pools.size, h, pools.kind, pools.seg_offsets, pools.req_sizes, pools.req_offsets)
+        fn, what = oracle.window_search_real, "two-pointer sweep, 128-bit fixed-point costs"
     else:
         args = (pools.size, pools.kind, pools.seg_offsets, pools.req_sizes, pools.req_offsets)
         fn, what = oracle.first_fit, "left-to-right walk per request"
@@ -150,6 +153,8 @@ def main():
     pools = workloads.make_config(args.config, args.seed)
     if args.op == "first_fit":
         return bench_first_fit(args, pools, spec, dev)
+    if args.op == "real":
+        return bench_real(args, pools, spec, dev)
     block_queries, alg_bytes, unique_bytes = workload_bytes(pools)
     batch_dev_bytes = 17 * pools.num_blocks + 16 * pools.num_segments + 8 * pools.num_requests
     copies = args.copies or max(1, -(-2 * INFINITY_CACHE_BYTES // batch_dev_bytes) + 1)
@@ -324,6 +329,113 @@ def bench_first_fit(args, pools, spec, dev):
         "parity_vs_oracle": parity,
         "wall_s_timed_region": wall,
         "kernel_source": source_digest(FIT_SOURCE),
+    }
+    print(json.dumps(rec), flush=True)
+
+
+REAL_SOURCE = os.path.join(ROOT, "paper_2311_00591_amd", "csrc", "coop_window_search_real.hip")
+
+
+def bench_real(args, pools, spec, dev):
+    """The search with real-valued heuristics h = cost / staleness on a
+    standard workload: same metric and byte accounting as the integer
+    search (17 B per block and request: size, h, kind), timed per call."""
+    import torch
+
+    import paper_2311_00591_amd as coop
+    import workloads
+
+    h = workloads.real_costs(pools, args.seed)
+    block_queries, alg_bytes, unique_bytes = workload_bytes(pools)
+    alg_bytes += 8 * pools.num_requests  # the 40-byte result instead of 24 (plus 8 B of S)
+    batch_dev_bytes = 17 * pools.num_blocks + 16 * pools.num_segments + 8 * pools.num_requests
+    copies = args.copies or max(1, -(-2 * INFINITY_CACHE_BYTES // batch_dev_bytes) + 1)
+    size, _, kind, seg, req, roff = coop.to_device(pools, dev)
+    ht = torch.from_numpy(h).to(dev)
+    ws = torch.empty(max(coop.real_workspace_size(pools.num_blocks, pools.num_segments,
+                                                  pools.num_requests), 1),
+                     dtype=torch.uint8, device=dev)
+    calls = []
+    for c in range(copies):
+        t = (size, ht, kind) if c == 0 else (size.clone(), ht.clone(), kind.clone())
+        calls.append(coop.WindowSearchReal(*t, seg, req, roff, workspace=ws))
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    sh = stream.cuda_stream
+    parity = None
+    status = None
+    if not args.no_parity:
+        import oracle
+        calls[0].launch(sh)
+        torch.cuda.synchronize()
+        out = calls[0].out.cpu().numpy()
+        status = int(calls[0].status.item())
+        want, want_cost = oracle.window_search_real(pools.size, h, pools.kind, pools.seg_offsets,
+                                                    pools.req_sizes, pools.req_offsets,
+                                                    threads=16)
+        parity = bool(np.array_equal(out[:, :4].view(np.uint64), want) and
+                      np.array_equal(out[:, 4].copy().view(np.uint64), want_cost.view(np.uint64))
+                      and status == 0)
+    for i in range(args.warmup):
+        calls[i % copies].launch(sh)
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    w0 = time.perf_counter()
+    start.record(stream)
+    for i in range(args.steps):
+        calls[i % copies].launch(sh)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms = start.elapsed_time(stop) / args.steps
+    t = ms / 1e3
+    achieved = alg_bytes / t / 1e9
+    cpu = cpu_baseline(pools, args.cpu_seconds, "real", h) if args.cpu_seconds > 0 else None
+    nb = np.diff(pools.seg_offsets.astype(np.int64))
+    rec = {
+        "metric": METRIC,
+        "value": pools.num_requests / t,
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64 heuristics, u128 fixed-point sums",
+        "data": "synthetic",
+        "config": {
+            "workload": f"real-valued heuristics on {spec.name}: B={pools.num_segments} "
+                        f"snapshots, N_b={int(nb.min())}..{int(nb.max())} blocks, "
+                        f"{pools.num_requests} requests, h = cost / staleness U{{1..4096}} "
+                        f"(standard workload {args.config})",
+            "num_segments": pools.num_segments,
+            "num_blocks": pools.num_blocks,
+            "num_requests": pools.num_requests,
+            "seed": args.seed,
+            "input_sha256": pools.digest()[:16],
+            "resident_copies": copies,
+            "cache": "cold" if copies > 1 else "warm",
+        },
+        "blocks_scanned_per_s": block_queries / t,
+        "hbm_roofline_pct": 100.0 * achieved / PEAK_HBM_GBS,
+        "roofline": {
+            "kernel": "real_tile_kernel + real_offsets_kernel + real_search_kernel + "
+                      "real_reduce_kernel (one call)",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": achieved / PEAK_HBM_GBS,
+            "traffic": None,
+            "algorithmic_bytes_per_launch": alg_bytes,
+        },
+        "cpu_baseline": cpu,
+        "parity_vs_oracle": parity,
+        "status": status,
+        "wall_s_timed_region": wall,
+        "kernel_source": source_digest(REAL_SOURCE),
     }
     print(json.dumps(rec), flush=True)
 

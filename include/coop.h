@@ -53,7 +53,7 @@ typedef enum {
 } coop_status_t;
 
 /* Version of this ABI; bumped on any incompatible change. */
-#define COOP_ABI_VERSION 2
+#define COOP_ABI_VERSION 3
 int coop_abi_version(void);
 
 /* Human-readable text for a status code (static storage, never NULL). */
@@ -159,6 +159,50 @@ coop_status_t coop_first_fit(const uint64_t *size, const uint8_t *kind, uint64_t
                              const uint64_t *req_sizes, const uint64_t *req_offsets,
                              uint64_t num_requests, uint64_t *out,
                              void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * The search with real-valued heuristics (section 3.3 defines a tensor's
+ * heuristic as h = c / s, projected cost over staleness, a real number).
+ * Same batch layout and window rules as coop_window_search, with h[k]
+ * (binary64, device) in place of cost[k].  A window costs the exact real sum
+ * of its evictable blocks' h: each h is rounded once to a multiple of 2^-64
+ * (to nearest, ties to even; exact for every h >= 2^-12) and the sums are
+ * taken in 128-bit fixed point, so no summation order can change the answer.
+ * Ranking and tie-breaks as in coop_window_search.
+ *
+ * out (device) receives num_requests coop_window_real_t: start, end, the
+ * exact cost in units of 2^-64 (cost_lo, cost_hi) and that cost rounded to
+ * the nearest binary64 (ties to even).  S == 0 gives all zeros; an
+ * infeasible request start = end = cost_lo = cost_hi = ~0 and cost = +inf.
+ * status (device u32) is set to 0, then bit 0 if an evictable block's h is
+ * NaN, infinite, negative (other than -0) or at least 2^64; results for
+ * such a batch are unspecified.  The h of free and pinned blocks is
+ * ignored.  Precondition (unchecked): within every run each snapshot's byte
+ * total and h total stay below 2^64.
+ *
+ * workspace: coop_window_search_real_workspace_size() bytes (device,
+ * caller-owned, contents need not be initialised): about 26 bytes per block
+ * (tile-local prefix sums) plus partial results.  Five launches are
+ * enqueued on `stream`; nothing is allocated or synchronised.  Status codes
+ * as for coop_window_search.
+ */
+typedef struct {
+    uint64_t start;
+    uint64_t end;
+    uint64_t cost_lo; /* exact cost in units of 2^-64, low 64 bits */
+    uint64_t cost_hi; /* high 64 bits */
+    double cost;      /* the exact cost rounded to the nearest binary64 */
+} coop_window_real_t;
+
+coop_status_t coop_window_search_real_workspace_size(uint64_t num_blocks, uint64_t num_segments,
+                                                     uint64_t num_requests, size_t *bytes_out);
+
+coop_status_t coop_window_search_real(const uint64_t *size, const double *h, const uint8_t *kind,
+                                      uint64_t num_blocks, const uint64_t *seg_offsets,
+                                      uint64_t num_segments, const uint64_t *req_sizes,
+                                      const uint64_t *req_offsets, uint64_t num_requests,
+                                      coop_window_real_t *out, uint32_t *status,
+                                      void *workspace, size_t workspace_bytes, void *stream);
 
 /* Eviction policies of coop_replay. */
 typedef enum {

@@ -73,6 +73,11 @@ def load_library():
                                 ctypes.c_int32, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.coop_replay.restype = ctypes.c_int
     lib.coop_window_search.restype = ctypes.c_int
+    lib.coop_window_search_real_workspace_size.argtypes = [u64, u64, u64, ctypes.POINTER(sz)]
+    lib.coop_window_search_real_workspace_size.restype = ctypes.c_int
+    lib.coop_window_search_real.argtypes = [vp, vp, vp, u64, vp, u64, vp, vp, u64, vp, vp, vp,
+                                            sz, vp]
+    lib.coop_window_search_real.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -177,6 +182,69 @@ def window_search(size, cost, kind, seg_offsets, req_sizes, req_offsets, *,
     (start, end, cost).  Asynchronous on `stream` like any torch op."""
     ws = WindowSearch(size, cost, kind, seg_offsets, req_sizes, req_offsets, out, workspace)
     return ws(stream)
+
+
+def real_workspace_size(num_blocks: int, num_segments: int, num_requests: int) -> int:
+    """Device workspace bytes coop_window_search_real needs."""
+    out = ctypes.c_size_t(0)
+    _check(load_library().coop_window_search_real_workspace_size(
+        int(num_blocks), int(num_segments), int(num_requests), ctypes.byref(out)))
+    return out.value
+
+
+class WindowSearchReal:
+    """A prepared coop_window_search_real call: the search with real-valued
+    heuristics h (float64 device tensor in place of cost).  Results: `out`,
+    int64 (Q, 5) = (start, end, exact cost low word, high word, binary64 cost
+    bits) -- `cost` is its last column viewed as float64 -- and `status`
+    (int32, bit 0: an invalid h)."""
+
+    def __init__(self, size, h, kind, seg_offsets, req_sizes, req_offsets,
+                 workspace: Optional[torch.Tensor] = None):
+        device = size.device
+        if device.type != "cuda":
+            raise ValueError("coop window search runs on the GPU; tensors are on "
+                             f"{device} (there is no CPU fallback)")
+        lib = load_library()
+        self.size = _u64_tensor(size, "size", device)
+        if h.dtype != torch.float64 or h.device != device or not h.is_contiguous():
+            raise TypeError("h must be a contiguous float64 tensor on the same device")
+        self.h = h
+        if kind.dtype != torch.uint8 or kind.device != device or not kind.is_contiguous():
+            raise TypeError("kind must be a contiguous uint8 tensor on the same device")
+        self.kind = kind
+        self.seg_offsets = _u64_tensor(seg_offsets, "seg_offsets", device)
+        self.req_sizes = _u64_tensor(req_sizes, "req_sizes", device)
+        self.req_offsets = _u64_tensor(req_offsets, "req_offsets", device)
+        n, b1, q = size.numel(), seg_offsets.numel(), req_sizes.numel()
+        if h.numel() != n or kind.numel() != n:
+            raise ValueError("size, h and kind must have the same length")
+        if b1 < 1 or req_offsets.numel() != b1:
+            raise ValueError("seg_offsets and req_offsets need num_segments + 1 entries")
+        self.num_blocks, self.num_segments, self.num_requests = n, b1 - 1, q
+        self.out = torch.empty((q, 5), dtype=torch.int64, device=device)
+        self.cost = self.out[:, 4].view(torch.float64)
+        self.status = torch.zeros(1, dtype=torch.int32, device=device)
+        need = real_workspace_size(n, b1 - 1, q)
+        if workspace is None:
+            workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+        if workspace.numel() * workspace.element_size() < need:
+            raise ValueError(f"workspace holds {workspace.numel()} bytes, needs {need}")
+        self.workspace = workspace
+        self._fn = lib.coop_window_search_real
+        self._args = (_ptr(self.size), _ptr(self.h), _ptr(self.kind), n,
+                      _ptr(self.seg_offsets), b1 - 1, _ptr(self.req_sizes),
+                      _ptr(self.req_offsets), q, _ptr(self.out), _ptr(self.status),
+                      _ptr(self.workspace), workspace.numel() * workspace.element_size())
+
+    def launch(self, stream: Optional[int] = None) -> None:
+        if stream is None:
+            stream = torch.cuda.current_stream(self.size.device).cuda_stream
+        _check(self._fn(*self._args, stream))
+
+    def __call__(self, stream: Optional[int] = None) -> torch.Tensor:
+        self.launch(stream)
+        return self.out
 
 
 def first_fit_workspace_size(num_blocks: int) -> int:
@@ -349,5 +417,5 @@ def to_device(pools, device="cuda"):
 __all__ = ["COOP_EVICTABLE", "COOP_FREE", "COOP_PINNED", "CoopError", "FirstFit",
            "INFEASIBLE", "LIBRARY", "POLICY_GREEDY", "POLICY_WINDOW", "Replay", "WindowSearch",
            "first_fit", "first_fit_workspace_size", "load_library", "plan_info",
-           "replay_to_device", "replay_workspace_size", "to_device", "window_search",
-           "workspace_size"]
+           "real_workspace_size", "replay_to_device", "replay_workspace_size", "to_device",
+           "window_search", "WindowSearchReal", "workspace_size"]

@@ -7,7 +7,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 SOURCES = [os.path.join(PKG, "csrc", "coop_window_search.hip"),
            os.path.join(PKG, "csrc", "coop_first_fit.hip"),
-           os.path.join(PKG, "csrc", "coop_replay.hip")]
+           os.path.join(PKG, "csrc", "coop_replay.hip"),
+           os.path.join(PKG, "csrc", "coop_window_search_real.hip")]
 INCLUDE = os.path.join(ROOT, "include")
 LIBRARY = os.path.join(PKG, "libcoop.so")
 ARCH = "gfx950"

@@ -1,0 +1,549 @@
+// The sliding-window search with real-valued heuristics (Coop, section 3.3:
+// h(t) = c(t) / s(t), projected cost over staleness, a real number).
+//
+// Each evictable block carries h as a binary64 value, and a window costs the
+// exact real sum of its h values: every h is rounded once to a multiple of
+// 2^-64 (to nearest, ties to even; exact for h >= 2^-12) and the sums are
+// taken in 128-bit fixed point (64 fraction bits).  Integer sums are
+// associative, so the window that wins does not depend on how the GPU
+// splits the work.  Ranking as in the integer search: least cost, then
+// fewest bytes, then lowest start.
+//
+// Five launches (the first clears the status word):
+//   1. real_tile_kernel: tiles of 2048 blocks, each writes the tile-local
+//      exclusive prefix sums of bytes (u64), fixed-point cost (u128) and
+//      pinned count (u16) of every block, and the tile's totals; a block
+//      with an invalid h sets a status bit.  Prefix index num_blocks (the
+//      end of the batch) belongs to the last tile, so there are
+//      floor(num_blocks / 2048) + 1 tiles.
+//   2. real_offsets_kernel: one workgroup turns the tile totals into
+//      exclusive tile offsets.  The global prefix at index x is then
+//      offset[x >> 11] + local[x].  Prefixes run over the whole batch
+//      (snapshots are not reset): window sums are differences of two
+//      prefixes of one snapshot, so they come out the same.
+//   3. real_search_kernel: workgroup (group, part) takes up to 16
+//      consecutive requests and one of `parts` equal slices of each
+//      request's snapshot.  It walks its slice in chunks of 2048 starts;
+//      for each chunk it stages the byte and pinned-count prefixes of 4097
+//      indices (the chunk and the blocks after it) in LDS, then runs every
+//      request of the group that shares the snapshot: each thread takes 8
+//      consecutive starts, finds the first start's shortest end by
+//      bisection (in LDS, or in global memory when the window reaches past
+//      the staged indices) and the later ones by walking on, since ends
+//      never move left.  A window [i, k) is valid iff the pinned counts at
+//      i and k agree.  Its cost is C[k] - C[i].  The workgroup minimum is
+//      kept per request in LDS and written to the request's partial slot.
+//   4. real_reduce_kernel: one thread per request takes the least of its
+//      `parts` partial slots and writes the result, the exact cost both as
+//      two 64-bit words and rounded to the nearest binary64.
+
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+
+#include "coop.h"
+
+namespace {
+
+constexpr uint32_t kThreads = 256;
+constexpr uint32_t kWaves = kThreads / 64;
+constexpr uint32_t kItems = 8;
+constexpr uint32_t kTileLog2 = 11;
+constexpr uint32_t kTile = 1u << kTileLog2;  // blocks per prefix tile
+static_assert(kTile == kThreads * kItems, "tile = threads x items");
+constexpr uint32_t kChunk = kThreads * kItems;  // starts per staged chunk
+constexpr uint32_t kStage = 2 * kChunk;         // staged prefix indices beyond a chunk's start
+constexpr uint32_t kMaxGroup = 16;              // requests per search workgroup
+constexpr uint32_t kTargetGroups = 2048;        // search workgroups aimed for
+constexpr uint32_t kMaxParts = 1024;
+constexpr uint32_t kOffsetThreads = 256;
+constexpr uint64_t kNone = ~0ull;
+constexpr uint32_t kErrValue = 1;
+
+struct U128 {
+    uint64_t lo, hi;
+};
+
+__device__ __forceinline__ U128 add128(U128 a, U128 b) {
+    U128 r;
+    r.lo = a.lo + b.lo;
+    r.hi = a.hi + b.hi + (r.lo < a.lo ? 1u : 0u);
+    return r;
+}
+
+__device__ __forceinline__ U128 sub128(U128 a, U128 b) {
+    U128 r;
+    r.lo = a.lo - b.lo;
+    r.hi = a.hi - b.hi - (a.lo < b.lo ? 1u : 0u);
+    return r;
+}
+
+// h (binary64) in units of 2^-64, rounded to nearest, ties to even.  False
+// for NaN, infinities, negative values other than -0 and values >= 2^64.
+// h = m * 2^(e - 1075) for a normal number, so h * 2^64 = m * 2^(e - 1011).
+__device__ __forceinline__ bool to_fixed(double h, U128& q) {
+    const uint64_t bits = static_cast<uint64_t>(__double_as_longlong(h));
+    const uint32_t e = static_cast<uint32_t>(bits >> 52) & 0x7ffu;
+    const uint64_t frac = bits & ((1ull << 52) - 1);
+    q = U128{0, 0};
+    if (bits >> 63) return e == 0 && frac == 0;
+    if (e >= 1023 + 64) return false;  // also infinities and NaN (e == 2047)
+    if (e == 0) return true;           // subnormal: far below half a unit
+    const uint64_t m = frac | (1ull << 52);
+    const int s = static_cast<int>(e) - 1011;
+    if (s >= 64) {
+        q.hi = m << (s - 64);  // s <= 75: m << 11 < 2^64
+    } else if (s > 0) {
+        q.lo = m << s;
+        q.hi = m >> (64 - s);
+    } else if (s == 0) {
+        q.lo = m;
+    } else if (s > -64) {
+        const int r = -s;
+        uint64_t v = m >> r;
+        const uint64_t rem = m & ((1ull << r) - 1), half = 1ull << (r - 1);
+        if (rem > half || (rem == half && (v & 1))) ++v;
+        q.lo = v;
+    }  // else m < 2^53 <= half a unit times 2^-10: zero
+    return true;
+}
+
+__device__ __forceinline__ uint64_t bit128(U128 v, int j) {
+    return j >= 64 ? (v.hi >> (j - 64)) & 1 : (v.lo >> j) & 1;
+}
+
+// A fixed-point value to the nearest binary64, ties to even.
+__device__ __forceinline__ double to_real(U128 v) {
+    if (v.hi == 0 && v.lo < (1ull << 53)) return ldexp(static_cast<double>(v.lo), -64);
+    const int lz = v.hi ? __clzll(v.hi) : 64 + __clzll(v.lo);
+    int sh = (127 - lz) - 52;  // bits below the 53 kept, >= 1
+    uint64_t m = sh >= 64 ? v.hi >> (sh - 64) : (v.lo >> sh) | (v.hi << (64 - sh));
+    const bool round = bit128(v, sh - 1) != 0;
+    bool sticky;
+    if (sh - 1 >= 64)
+        sticky = v.lo != 0 || (v.hi & ((1ull << (sh - 1 - 64)) - 1)) != 0;
+    else
+        sticky = (v.lo & ((1ull << (sh - 1)) - 1)) != 0;
+    if (round && (sticky || (m & 1))) {
+        ++m;
+        if (m == (1ull << 53)) {
+            m >>= 1;
+            ++sh;
+        }
+    }
+    return ldexp(static_cast<double>(m), sh - 64);
+}
+
+__device__ __forceinline__ uint64_t shfl_up64(uint64_t v, int d) {
+    const uint32_t lo = __shfl_up(static_cast<uint32_t>(v), d, 64);
+    const uint32_t hi = __shfl_up(static_cast<uint32_t>(v >> 32), d, 64);
+    return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t shfl_xor64(uint64_t v, int m) {
+    const uint32_t lo = __shfl_xor(static_cast<uint32_t>(v), m, 64);
+    const uint32_t hi = __shfl_xor(static_cast<uint32_t>(v >> 32), m, 64);
+    return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+// Prefix triple: bytes, fixed-point cost, pinned count.
+struct Tri {
+    uint64_t p;
+    U128 c;
+    uint64_t r;
+};
+
+__device__ __forceinline__ Tri add_tri(const Tri& a, const Tri& b) {
+    return Tri{a.p + b.p, add128(a.c, b.c), a.r + b.r};
+}
+
+// Inclusive scan of a Tri over the wavefront.
+__device__ __forceinline__ Tri wave_scan(Tri v) {
+    const uint32_t lane = threadIdx.x & 63u;
+    for (int d = 1; d < 64; d <<= 1) {
+        const Tri x{shfl_up64(v.p, d), U128{shfl_up64(v.c.lo, d), shfl_up64(v.c.hi, d)},
+                    shfl_up64(v.r, d)};
+        if (lane >= static_cast<uint32_t>(d)) v = add_tri(v, x);
+    }
+    return v;
+}
+
+// Clears the status word (a kernel rather than a memset, so that the call
+// can be captured in a graph).
+__global__ void real_status_kernel(uint32_t* status) { *status = 0; }
+
+// Stage 1.  Tile t covers prefix indices [t * 2048, min((t + 1) * 2048, n + 1)).
+__global__ __launch_bounds__(kThreads) void real_tile_kernel(
+    const uint64_t* __restrict__ size, const double* __restrict__ h,
+    const uint8_t* __restrict__ kind, uint64_t n, uint64_t num_tiles, uint64_t* __restrict__ pl,
+    uint64_t* __restrict__ cl_lo, uint64_t* __restrict__ cl_hi, uint16_t* __restrict__ rl,
+    Tri* __restrict__ tot, uint32_t* __restrict__ status) {
+    __shared__ Tri wtot[kWaves];
+    const uint32_t tid = threadIdx.x, lane = tid & 63u, w = tid >> 6;
+    for (uint64_t t = blockIdx.x; t < num_tiles; t += gridDim.x) {
+        const uint64_t base = t * kTile + tid * kItems;
+        uint64_t sz[kItems];
+        U128 cq[kItems];
+        uint32_t pin = 0;  // bit u: item u pinned
+        bool bad = false;
+#pragma unroll
+        for (uint32_t u = 0; u < kItems; ++u) {
+            const uint64_t k = base + u;
+            sz[u] = 0;
+            cq[u] = U128{0, 0};
+            if (k < n) {
+                const uint8_t kd = kind[k];
+                sz[u] = size[k];
+                if (kd >= COOP_PINNED) pin |= 1u << u;
+                if (kd == COOP_EVICTABLE && !to_fixed(h[k], cq[u])) bad = true;
+            }
+        }
+        if (__ballot(bad) != 0 && lane == 0) atomicOr(status, kErrValue);
+        Tri mine{0, U128{0, 0}, 0};
+#pragma unroll
+        for (uint32_t u = 0; u < kItems; ++u) {
+            mine.p += sz[u];
+            mine.c = add128(mine.c, cq[u]);
+        }
+        mine.r = __popc(pin);
+        const Tri inc = wave_scan(mine);
+        if (lane == 63) wtot[w] = inc;
+        __syncthreads();
+        Tri run{0, U128{0, 0}, 0};
+        for (uint32_t v = 0; v < w; ++v) run = add_tri(run, wtot[v]);
+        Tri all = run;
+        for (uint32_t v = w; v < kWaves; ++v) all = add_tri(all, wtot[v]);
+        __syncthreads();
+        run = add_tri(run, Tri{inc.p - mine.p, sub128(inc.c, mine.c), inc.r - mine.r});
+#pragma unroll
+        for (uint32_t u = 0; u < kItems; ++u) {
+            const uint64_t k = base + u;
+            if (k <= n) {
+                pl[k] = run.p;
+                cl_lo[k] = run.c.lo;
+                cl_hi[k] = run.c.hi;
+                rl[k] = static_cast<uint16_t>(run.r);
+            }
+            run.p += sz[u];
+            run.c = add128(run.c, cq[u]);
+            run.r += (pin >> u) & 1u;
+        }
+        if (tid == 0) tot[t] = all;
+    }
+}
+
+// Stage 2: exclusive tile offsets, one workgroup.
+__global__ __launch_bounds__(kOffsetThreads) void real_offsets_kernel(const Tri* __restrict__ tot,
+                                                                      uint64_t num_tiles,
+                                                                      Tri* __restrict__ off) {
+    __shared__ Tri wtot[kOffsetThreads / 64];
+    const uint32_t tid = threadIdx.x, lane = tid & 63u, w = tid >> 6;
+    Tri carry{0, U128{0, 0}, 0};
+    for (uint64_t c0 = 0; c0 < num_tiles; c0 += kOffsetThreads) {
+        const uint64_t t = c0 + tid;
+        const Tri mine = t < num_tiles ? tot[t] : Tri{0, U128{0, 0}, 0};
+        const Tri inc = wave_scan(mine);
+        if (lane == 63) wtot[w] = inc;
+        __syncthreads();
+        Tri run = carry;
+        for (uint32_t v = 0; v < w; ++v) run = add_tri(run, wtot[v]);
+        Tri next = carry;
+        for (uint32_t v = 0; v < kOffsetThreads / 64; ++v) next = add_tri(next, wtot[v]);
+        __syncthreads();
+        if (t < num_tiles) off[t] = add_tri(run, Tri{inc.p - mine.p, sub128(inc.c, mine.c),
+                                                     inc.r - mine.r});
+        carry = next;
+    }
+}
+
+struct Prefix {
+    const uint64_t* pl;
+    const uint64_t* cl_lo;
+    const uint64_t* cl_hi;
+    const uint16_t* rl;
+    const Tri* off;
+
+    __device__ __forceinline__ uint64_t P(uint64_t x) const { return off[x >> kTileLog2].p + pl[x]; }
+    __device__ __forceinline__ uint64_t R(uint64_t x) const { return off[x >> kTileLog2].r + rl[x]; }
+    __device__ __forceinline__ U128 C(uint64_t x) const {
+        return add128(off[x >> kTileLog2].c, U128{cl_lo[x], cl_hi[x]});
+    }
+};
+
+// A partial result: exact cost, bytes, window [start, end) in batch indices.
+struct Best {
+    uint64_t c_lo, c_hi, bytes, start, end;
+};
+
+__device__ __forceinline__ Best best_none() { return Best{kNone, kNone, kNone, kNone, kNone}; }
+
+__device__ __forceinline__ bool best_less(const Best& a, const Best& b) {
+    if (a.c_hi != b.c_hi) return a.c_hi < b.c_hi;
+    if (a.c_lo != b.c_lo) return a.c_lo < b.c_lo;
+    if (a.bytes != b.bytes) return a.bytes < b.bytes;
+    return a.start < b.start;
+}
+
+// The workgroup's least Best (every thread calls it and gets it).
+__device__ __forceinline__ Best block_min(Best v, Best* wred) {
+    for (int o = 32; o >= 1; o >>= 1) {
+        const Best x{shfl_xor64(v.c_lo, o), shfl_xor64(v.c_hi, o), shfl_xor64(v.bytes, o),
+                     shfl_xor64(v.start, o), shfl_xor64(v.end, o)};
+        if (best_less(x, v)) v = x;
+    }
+    if ((threadIdx.x & 63u) == 0) wred[threadIdx.x >> 6] = v;
+    __syncthreads();
+    Best m = wred[0];
+    for (uint32_t w = 1; w < kWaves; ++w)
+        if (best_less(wred[w], m)) m = wred[w];
+    __syncthreads();
+    return m;
+}
+
+// The snapshot b with req_off[b] <= r < req_off[b + 1].
+__device__ __forceinline__ uint64_t owner(const uint64_t* req_off, uint64_t num_segments, uint64_t r) {
+    uint64_t lo = 0, hi = num_segments;  // answer in [lo, hi)
+    while (hi - lo > 1) {
+        const uint64_t mid = lo + (hi - lo) / 2;
+        if (req_off[mid] <= r) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+struct SearchArgs {
+    const uint64_t* seg;
+    uint64_t num_segments;
+    const uint64_t* req_sizes;
+    const uint64_t* req_off;
+    uint64_t num_requests;
+    uint64_t group;     // requests per workgroup
+    uint64_t parts;     // slices per snapshot
+    uint64_t units;     // number of (group, part) work units
+    Best* slots;        // num_requests * parts
+};
+
+// Stage 3.
+__global__ __launch_bounds__(kThreads) void real_search_kernel(Prefix pf, SearchArgs A) {
+    __shared__ uint64_t Ps[kStage + 1];
+    __shared__ uint32_t Rs[kStage + 1];
+    __shared__ Best best[kMaxGroup];
+    __shared__ Best wred[kWaves];
+    const uint32_t tid = threadIdx.x;
+    for (uint64_t L = blockIdx.x; L < A.units; L += gridDim.x) {
+        const uint64_t g = L % A.parts, qg = L / A.parts;
+        const uint64_t r0 = qg * A.group;
+        const uint64_t r1 = r0 + A.group < A.num_requests ? r0 + A.group : A.num_requests;
+        if (tid < kMaxGroup) best[tid] = best_none();
+        __syncthreads();
+        for (uint64_t r = r0; r < r1;) {
+            const uint64_t b = owner(A.req_off, A.num_segments, r);
+            const uint64_t rend = A.req_off[b + 1] < r1 ? A.req_off[b + 1] : r1;
+            const uint64_t s0 = A.seg[b], nend = A.seg[b + 1], nb = nend - s0;
+            // slice g of the snapshot's starts (nb * g fits: nb < 2^48 assumed by the host)
+            const uint64_t a = s0 + nb * g / A.parts, e = s0 + nb * (g + 1) / A.parts;
+            for (uint64_t c0 = a; c0 < e; c0 += kChunk) {
+                const uint64_t c1 = c0 + kChunk < e ? c0 + kChunk : e;
+                const uint64_t hi = c0 + kStage < nend ? c0 + kStage : nend;  // staged [c0, hi]
+                // pinned counts relative to the chunk's first index (< 2^13)
+                const uint64_t rbase = pf.R(c0);
+                for (uint64_t x = c0 + tid; x <= hi; x += kThreads) {
+                    Ps[x - c0] = pf.P(x);
+                    Rs[x - c0] = static_cast<uint32_t>(pf.R(x) - rbase);
+                }
+                const uint64_t i0 = c0 + static_cast<uint64_t>(tid) * kItems;  // this thread's starts
+                __syncthreads();
+                for (uint64_t rr = r; rr < rend; ++rr) {
+                    const uint64_t S = A.req_sizes[rr];
+                    if (S == 0) continue;
+                    Best mine = best_none();
+                    uint64_t k = kNone;
+#pragma unroll 1
+                    for (uint32_t u = 0; u < kItems; ++u) {
+                        const uint64_t i = i0 + u;
+                        if (i >= c1) break;
+                        const uint64_t pi = Ps[i - c0];
+                        const uint32_t ri = Rs[i - c0];
+                        // pred(x): x is past the run of i or [i, x) holds S bytes;
+                        // monotone in x, and the first x where it holds is the end
+                        // of the shortest window from i (or a pinned-crossing one)
+                        auto pred_lds = [&](uint64_t x) {
+                            return Rs[x - c0] != ri || Ps[x - c0] - pi >= S;
+                        };
+                        auto pred_glb = [&](uint64_t x) {
+                            return pf.R(x) - rbase != ri || pf.P(x) - pi >= S;
+                        };
+                        uint64_t x;
+                        if (k == kNone) {
+                            if (pred_lds(hi)) {
+                                uint64_t lo2 = i + 1, hi2 = hi;
+                                while (lo2 < hi2) {
+                                    const uint64_t mid = (lo2 + hi2) >> 1;
+                                    if (pred_lds(mid)) hi2 = mid; else lo2 = mid + 1;
+                                }
+                                x = lo2;
+                            } else if (hi < nend && pred_glb(nend)) {
+                                uint64_t lo2 = hi + 1, hi2 = nend;
+                                while (lo2 < hi2) {
+                                    const uint64_t mid = (lo2 + hi2) >> 1;
+                                    if (pred_glb(mid)) hi2 = mid; else lo2 = mid + 1;
+                                }
+                                x = lo2;
+                            } else {
+                                break;  // no window from i, nor from any later start
+                            }
+                        } else {
+                            x = k > i + 1 ? k : i + 1;
+                            while (x <= hi && !pred_lds(x)) ++x;
+                            if (x > hi) {
+                                while (x <= nend && !pred_glb(x)) ++x;
+                                if (x > nend) break;
+                            }
+                        }
+                        k = x;
+                        const bool in = x <= hi;
+                        const uint64_t rk = in ? Rs[x - c0] : pf.R(x) - rbase;
+                        if (rk == ri) {
+                            const uint64_t pk = in ? Ps[x - c0] : pf.P(x);
+                            const U128 cost = sub128(pf.C(x), pf.C(i));
+                            const Best cand{cost.lo, cost.hi, pk - pi, i, x};
+                            if (best_less(cand, mine)) mine = cand;
+                        }
+                    }
+                    const Best m = block_min(mine, wred);
+                    if (tid == 0 && best_less(m, best[rr - r0])) best[rr - r0] = m;
+                }
+                __syncthreads();
+            }
+            r = rend;
+        }
+        __syncthreads();
+        if (tid < r1 - r0) A.slots[(r0 + tid) * A.parts + g] = best[tid];
+        __syncthreads();
+    }
+}
+
+// Stage 4.
+__global__ __launch_bounds__(kThreads) void real_reduce_kernel(SearchArgs A,
+                                                               coop_window_real_t* __restrict__ out) {
+    const uint64_t r = static_cast<uint64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (r >= A.num_requests) return;
+    coop_window_real_t o;
+    if (A.req_sizes[r] == 0) {
+        o.start = o.end = o.cost_lo = o.cost_hi = 0;
+        o.cost = 0.0;
+        out[r] = o;
+        return;
+    }
+    Best m = best_none();
+    for (uint64_t g = 0; g < A.parts; ++g) {
+        const Best x = A.slots[r * A.parts + g];
+        if (best_less(x, m)) m = x;
+    }
+    if (m.start == kNone) {
+        o.start = o.end = o.cost_lo = o.cost_hi = kNone;
+        o.cost = __builtin_inf();
+    } else {
+        const uint64_t s0 = A.seg[owner(A.req_off, A.num_segments, r)];
+        o.start = m.start - s0;
+        o.end = m.end - s0;
+        o.cost_lo = m.c_lo;
+        o.cost_hi = m.c_hi;
+        o.cost = to_real(U128{m.c_lo, m.c_hi});
+    }
+    out[r] = o;
+}
+
+struct RealLayout {
+    uint64_t tiles, group, parts, units;
+    size_t pl, cl_lo, cl_hi, rl, tot, off, slots, bytes;
+};
+
+size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+bool real_layout(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests, RealLayout* l) {
+    if (num_segments == 0 || num_blocks >= (1ull << 40) || num_requests >= (1ull << 40))
+        return false;
+    l->tiles = (num_blocks >> kTileLog2) + 1;
+    uint64_t rps = num_requests / num_segments;
+    l->group = rps < 1 ? 1 : (rps > kMaxGroup ? kMaxGroup : rps);
+    const uint64_t groups = (num_requests + l->group - 1) / l->group;
+    const uint64_t avg = num_blocks / num_segments;
+    uint64_t parts = groups ? (kTargetGroups + groups - 1) / groups : 1;
+    const uint64_t cap = avg / kChunk > 1 ? avg / kChunk : 1;
+    if (parts > cap) parts = cap;
+    if (parts > kMaxParts) parts = kMaxParts;
+    if (parts < 1) parts = 1;
+    l->parts = parts;
+    l->units = groups * parts;
+    const uint64_t np = num_blocks + 1;
+    size_t at = 0;
+    l->pl = at; at = align256(at + np * 8);
+    l->cl_lo = at; at = align256(at + np * 8);
+    l->cl_hi = at; at = align256(at + np * 8);
+    l->rl = at; at = align256(at + np * 2);
+    l->tot = at; at = align256(at + l->tiles * sizeof(Tri));
+    l->off = at; at = align256(at + l->tiles * sizeof(Tri));
+    l->slots = at; at = align256(at + num_requests * parts * sizeof(Best));
+    l->bytes = at;
+    return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+coop_status_t coop_window_search_real_workspace_size(uint64_t num_blocks, uint64_t num_segments,
+                                                     uint64_t num_requests, size_t* bytes_out) {
+    if (!bytes_out) return COOP_ERR_INVALID;
+    if (num_requests == 0) {
+        *bytes_out = 0;
+        return COOP_OK;
+    }
+    RealLayout l;
+    if (!real_layout(num_blocks, num_segments, num_requests, &l)) return COOP_ERR_INVALID;
+    *bytes_out = l.bytes;
+    return COOP_OK;
+}
+
+coop_status_t coop_window_search_real(const uint64_t* size, const double* h, const uint8_t* kind,
+                                      uint64_t num_blocks, const uint64_t* seg_offsets,
+                                      uint64_t num_segments, const uint64_t* req_sizes,
+                                      const uint64_t* req_offsets, uint64_t num_requests,
+                                      coop_window_real_t* out, uint32_t* status, void* workspace,
+                                      size_t workspace_bytes, void* stream) {
+    if (num_requests == 0) return COOP_OK;
+    if (!seg_offsets || !req_sizes || !req_offsets || !out || !status) return COOP_ERR_INVALID;
+    if (num_blocks && (!size || !h || !kind)) return COOP_ERR_INVALID;
+    RealLayout l;
+    if (!real_layout(num_blocks, num_segments, num_requests, &l)) return COOP_ERR_INVALID;
+    if (!workspace || workspace_bytes < l.bytes) return COOP_ERR_WORKSPACE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char* w = static_cast<char*>(workspace);
+    uint64_t* pl = reinterpret_cast<uint64_t*>(w + l.pl);
+    uint64_t* cl_lo = reinterpret_cast<uint64_t*>(w + l.cl_lo);
+    uint64_t* cl_hi = reinterpret_cast<uint64_t*>(w + l.cl_hi);
+    uint16_t* rl = reinterpret_cast<uint16_t*>(w + l.rl);
+    Tri* tot = reinterpret_cast<Tri*>(w + l.tot);
+    Tri* off = reinterpret_cast<Tri*>(w + l.off);
+    Best* slots = reinterpret_cast<Best*>(w + l.slots);
+    hipLaunchKernelGGL(real_status_kernel, dim3(1), dim3(1), 0, s, status);
+    if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
+    const uint32_t tile_grid = static_cast<uint32_t>(l.tiles < (1u << 20) ? l.tiles : (1u << 20));
+    hipLaunchKernelGGL(real_tile_kernel, dim3(tile_grid), dim3(kThreads), 0, s, size, h, kind,
+                       num_blocks, l.tiles, pl, cl_lo, cl_hi, rl, tot, status);
+    if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
+    hipLaunchKernelGGL(real_offsets_kernel, dim3(1), dim3(kOffsetThreads), 0, s, tot, l.tiles, off);
+    if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
+    const Prefix pf{pl, cl_lo, cl_hi, rl, off};
+    const SearchArgs A{seg_offsets, num_segments, req_sizes, req_offsets, num_requests,
+                       l.group, l.parts, l.units, slots};
+    const uint32_t search_grid = static_cast<uint32_t>(l.units < (1u << 20) ? l.units : (1u << 20));
+    hipLaunchKernelGGL(real_search_kernel, dim3(search_grid), dim3(kThreads), 0, s, pf, A);
+    if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
+    const uint32_t reduce_grid = static_cast<uint32_t>((num_requests + kThreads - 1) / kThreads);
+    hipLaunchKernelGGL(real_reduce_kernel, dim3(reduce_grid), dim3(kThreads), 0, s, A, out);
+    if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
+    return COOP_OK;
+}
+
+}  // extern "C"

@@ -82,3 +82,34 @@ def parse_greedy_golden(path):
                 step["after"] = [(kinds[k], int(s) * mib, int(i)) for k, s, i in
                                  (p.split() for p in line[len("after"):].split("|"))]
     return cases
+
+
+def parse_real_golden(path):
+    """Parses tests/golden/real_examples.txt into a list of
+    {"name", "blocks": [(kind, bytes, h)], "reqs": [(S, (start, end, hi, lo)
+    or None)]}; h may be a decimal, a hex float or C/S (the binary64
+    quotient)."""
+    kinds, mib = {"F": 0, "E": 1, "P": 2}, 1 << 20
+
+    def real(tok):
+        if "/" in tok:
+            c, s = tok.split("/")
+            return int(c) / int(s)
+        return float.fromhex(tok) if tok.startswith("0x") else float(tok)
+
+    out, cur = [], None
+    with open(path) as f:
+        for raw in f:
+            line = raw.split("#", 1)[0].strip()
+            if not line:
+                continue
+            tok = line.split()
+            if tok[0] == "example":
+                cur = {"name": tok[1], "blocks": [], "reqs": []}
+                out.append(cur)
+            elif tok[0] == "block":
+                cur["blocks"].append((kinds[tok[1]], int(tok[2]) * mib, real(tok[3])))
+            elif tok[0] == "req":
+                want = None if tok[3] == "infeasible" else tuple(int(x) for x in tok[3:7])
+                cur["reqs"].append((int(tok[1]) * mib, want))
+    return out

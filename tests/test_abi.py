@@ -131,3 +131,23 @@ def test_replay_rejects_unknown_policy_and_null_buffers():
     assert call(coop.POLICY_GREEDY, ptr=None) == -1
     assert lib.coop_replay(*bufs, 1, 8, nz, nz, nz, nz, nz, 1, 1, nz, nz, nz, nz, nz, nz, 1,
                            None) == -2  # workspace too small
+
+
+def test_real_search_validates_host_arguments():
+    lib = coop.load_library()
+    nz = 16
+
+    def call(B=1, Q=1, ws=nz, wsb=1 << 30, **null):
+        a = dict(size=nz, h=nz, kind=nz, seg=nz, req=nz, roff=nz, out=nz, status=nz)
+        a.update(null)
+        return lib.coop_window_search_real(a["size"], a["h"], a["kind"], 8, a["seg"], B, a["req"],
+                                           a["roff"], Q, a["out"], a["status"], ws, wsb, None)
+
+    assert call(Q=0, seg=None) == 0
+    for name in ("size", "h", "kind", "seg", "req", "roff", "out", "status"):
+        assert call(**{name: None}) == -1, name
+    assert call(B=0) == -1
+    assert call(ws=None) == -2
+    assert call(wsb=1) == -2
+    assert coop.real_workspace_size(8, 1, 1) > 0
+    assert coop.real_workspace_size(8, 1, 0) == 0

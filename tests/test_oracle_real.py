@@ -20,39 +20,12 @@ import numpy as np
 import pytest
 
 import oracle
+from conftest import parse_real_golden
 
 MiB = 1 << 20
 U64MAX = (1 << 64) - 1
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
                       "real_examples.txt")
-KIND = {"F": 0, "E": 1, "P": 2}
-
-
-def _h(tok):
-    if "/" in tok:
-        c, s = tok.split("/")
-        return int(c) / int(s)
-    if tok.startswith("0x"):
-        return float.fromhex(tok)
-    return float(tok)
-
-
-def _examples():
-    out, cur = [], None
-    for raw in open(GOLDEN):
-        line = raw.split("#", 1)[0].strip()
-        if not line:
-            continue
-        tok = line.split()
-        if tok[0] == "example":
-            cur = {"name": tok[1], "blocks": [], "reqs": []}
-            out.append(cur)
-        elif tok[0] == "block":
-            cur["blocks"].append((KIND[tok[1]], int(tok[2]) * MiB, _h(tok[3])))
-        elif tok[0] == "req":
-            want = None if tok[3] == "infeasible" else tuple(int(x) for x in tok[3:7])
-            cur["reqs"].append((int(tok[1]) * MiB, want))
-    return out
 
 
 def _one(blocks, reqs):
@@ -63,7 +36,7 @@ def _one(blocks, reqs):
 
 
 def test_golden_real():
-    ex = _examples()
+    ex = parse_real_golden(GOLDEN)
     assert len(ex) >= 7
     for e in ex:
         res, cost = _one(e["blocks"], [s for s, _ in e["reqs"]])

@@ -277,3 +277,16 @@ def from_lists(snapshots, requests) -> Pools:
     return Pools(np.array(sizes, dtype=np.uint64), np.array(costs, dtype=np.uint64),
                  np.array(kinds, dtype=np.uint8), np.array(seg, dtype=np.uint64),
                  np.array(req, dtype=np.uint64), np.array(roff, dtype=np.uint64))
+
+
+def real_costs(pools: Pools, seed: int = 0, max_staleness: int = 4096) -> np.ndarray:
+    """Real-valued heuristics for a batch (float64, one per block): each
+    evictable block's integer cost divided by a staleness drawn uniform on
+    {1..max_staleness}, rounded to the nearest binary64; 0 for free and
+    pinned blocks.  Seeded by (seed, number of blocks), independent of the
+    draws that made the batch."""
+    rng = np.random.default_rng([0x5EA1, seed, pools.num_blocks])
+    s = rng.integers(1, max_staleness + 1, pools.num_blocks).astype(np.float64)
+    h = pools.cost.astype(np.float64) / s
+    h[pools.kind != EVICTABLE] = 0.0
+    return h
