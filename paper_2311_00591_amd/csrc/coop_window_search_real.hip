@@ -24,15 +24,13 @@
 //   3. real_search_kernel: workgroup (group, part) takes up to 16
 //      consecutive requests and one of `parts` equal slices of each
 //      request's snapshot.  It walks its slice in chunks of 2048 starts;
-//      for each chunk it stages the byte and pinned-count prefixes of 4097
-//      indices (the chunk and the blocks after it) in LDS, then runs every
-//      request of the group that shares the snapshot: each thread takes 8
-//      consecutive starts, finds the first start's shortest end by
-//      bisection (in LDS, or in global memory when the window reaches past
-//      the staged indices) and the later ones by walking on, since ends
-//      never move left.  A window [i, k) is valid iff the pinned counts at
-//      i and k agree.  Its cost is C[k] - C[i].  The workgroup minimum is
-//      kept per request in LDS and written to the request's partial slot.
+//      for each chunk it stages packed byte/pinned-count keys and cost
+//      prefixes of up to 3073 indices (the chunk and the blocks after it)
+//      in LDS, then runs every request of the group that shares the
+//      snapshot as a merge path (see the kernel).  A window [i, k) is valid
+//      iff it holds no pinned block; its cost is C[k] - C[i].  Each
+//      wavefront's minimum is kept per request in LDS; their least goes to
+//      the request's partial slot.
 //   4. real_reduce_kernel: one thread per request takes the least of its
 //      `parts` partial slots and writes the result, the exact cost both as
 //      two 64-bit words and rounded to the nearest binary64.
@@ -52,7 +50,16 @@ constexpr uint32_t kTileLog2 = 11;
 constexpr uint32_t kTile = 1u << kTileLog2;  // blocks per prefix tile
 static_assert(kTile == kThreads * kItems, "tile = threads x items");
 constexpr uint32_t kChunk = kThreads * kItems;  // starts per staged chunk
-constexpr uint32_t kStage = 2 * kChunk;         // staged prefix indices beyond a chunk's start
+constexpr uint32_t kStage = kChunk + kChunk / 2;  // staged prefix indices beyond a chunk's start
+// Packed staged keys: Y(x) = (pinned count since the chunk start) * 2^51 +
+// (bytes since the chunk start).  With fewer than 4096 staged indices and
+// staged bytes plus S below 2^51, Y(x) >= Y(i) + S holds exactly when x is
+// past the run of i or [i, x) holds S bytes, and Y(x) - Y(i) < 2^51 exactly
+// when [i, x) holds no pinned block (it is then the window's byte count).
+constexpr uint32_t kPackBits = 51;
+constexpr uint64_t kPackOne = 1ull << kPackBits;
+static_assert(kStage < (1u << (63 - kPackBits)), "packed keys stay below 2^63");
+constexpr uint64_t kEndKey = ~0ull;  // above every target: stops every merge
 constexpr uint32_t kMaxGroup = 16;              // requests per search workgroup
 constexpr uint32_t kTargetGroups = 2048;        // search workgroups aimed for
 constexpr uint32_t kMaxParts = 1024;
@@ -284,22 +291,6 @@ __device__ __forceinline__ bool best_less(const Best& a, const Best& b) {
     return a.start < b.start;
 }
 
-// The workgroup's least Best (every thread calls it and gets it).
-__device__ __forceinline__ Best block_min(Best v, Best* wred) {
-    for (int o = 32; o >= 1; o >>= 1) {
-        const Best x{shfl_xor64(v.c_lo, o), shfl_xor64(v.c_hi, o), shfl_xor64(v.bytes, o),
-                     shfl_xor64(v.start, o), shfl_xor64(v.end, o)};
-        if (best_less(x, v)) v = x;
-    }
-    if ((threadIdx.x & 63u) == 0) wred[threadIdx.x >> 6] = v;
-    __syncthreads();
-    Best m = wred[0];
-    for (uint32_t w = 1; w < kWaves; ++w)
-        if (best_less(wred[w], m)) m = wred[w];
-    __syncthreads();
-    return m;
-}
-
 // The snapshot b with req_off[b] <= r < req_off[b + 1].
 __device__ __forceinline__ uint64_t owner(const uint64_t* req_off, uint64_t num_segments, uint64_t r) {
     uint64_t lo = 0, hi = num_segments;  // answer in [lo, hi)
@@ -322,102 +313,187 @@ struct SearchArgs {
     Best* slots;        // num_requests * parts
 };
 
-// Stage 3.
+// The least Best of the wavefront (every lane gets it).
+__device__ __forceinline__ Best wave_min(Best v) {
+    for (int o = 32; o >= 1; o >>= 1) {
+        const Best x{shfl_xor64(v.c_lo, o), shfl_xor64(v.c_hi, o), shfl_xor64(v.bytes, o),
+                     shfl_xor64(v.start, o), shfl_xor64(v.end, o)};
+        if (best_less(x, v)) v = x;
+    }
+    return v;
+}
+
+// Starts [i, i_end) of one snapshot (ending at nend), walked by one thread
+// from the global prefixes alone: the first start's shortest end by
+// bisection, the later ones by walking on.  pred(x): x is past the run of
+// the start or [start, x) holds S bytes; it is monotone in x, and its first
+// x is the end of the shortest window (or of one that crosses a pinned
+// block, which is then invalid).
+__device__ void walk_global(const Prefix& pf, uint64_t i, uint64_t i_end, uint64_t nend,
+                            uint64_t S, Best& mine) {
+    uint64_t k = kNone;
+    for (; i < i_end; ++i) {
+        const uint64_t pi = pf.P(i), ri = pf.R(i);
+        auto pred = [&](uint64_t x) { return pf.R(x) != ri || pf.P(x) - pi >= S; };
+        uint64_t x;
+        if (k == kNone) {
+            if (!pred(nend)) return;  // no window from i, nor from any later start
+            uint64_t lo = i + 1, hi = nend;
+            while (lo < hi) {
+                const uint64_t mid = (lo + hi) >> 1;
+                if (pred(mid)) hi = mid; else lo = mid + 1;
+            }
+            x = lo;
+        } else {
+            x = k > i + 1 ? k : i + 1;
+            while (x <= nend && !pred(x)) ++x;
+            if (x > nend) return;
+        }
+        k = x;
+        if (pf.R(x) == ri) {
+            const U128 cost = sub128(pf.C(x), pf.C(i));
+            const Best cand{cost.lo, cost.hi, pf.P(x) - pi, i, x};
+            if (best_less(cand, mine)) mine = cand;
+        }
+    }
+}
+
+// Stage 3.  Per chunk the workgroup stages, for the indices [c0, hi] (the
+// chunk's starts and the blocks after them, at most 3073), the packed keys
+// Y and the fixed-point cost prefixes relative to c0 in LDS.  Each request
+// is then a merge of two sorted sequences, the targets Y(i) + S of the
+// starts and the end keys Y(x): a start meets, when it is merged, the first
+// end key at or above its target, which is the end of its shortest window.
+// Every lane bisects its diagonal of the merge once and walks a fixed
+// number of steps, scoring each start it takes on the spot.  Starts whose
+// target lies above every staged end key (windows reaching past hi) are
+// walked from the global prefixes, as are whole chunks whose bytes or
+// request break the packed-key bounds.  Each wavefront keeps its own least
+// window per request, so a request costs no barrier; the wavefronts' minima
+// meet once per unit.
 __global__ __launch_bounds__(kThreads) void real_search_kernel(Prefix pf, SearchArgs A) {
-    __shared__ uint64_t Ps[kStage + 1];
-    __shared__ uint32_t Rs[kStage + 1];
-    __shared__ Best best[kMaxGroup];
-    __shared__ Best wred[kWaves];
-    const uint32_t tid = threadIdx.x;
+    __shared__ uint64_t Y[kStage + 2];
+    __shared__ U128 Cr[kStage + 2];
+    __shared__ Best bestw[kWaves][kMaxGroup];
+    __shared__ int big_flag;
+    const uint32_t tid = threadIdx.x, lane = tid & 63u, w = tid >> 6;
     for (uint64_t L = blockIdx.x; L < A.units; L += gridDim.x) {
         const uint64_t g = L % A.parts, qg = L / A.parts;
         const uint64_t r0 = qg * A.group;
         const uint64_t r1 = r0 + A.group < A.num_requests ? r0 + A.group : A.num_requests;
-        if (tid < kMaxGroup) best[tid] = best_none();
-        __syncthreads();
+        if (lane < kMaxGroup) bestw[w][lane] = best_none();
         for (uint64_t r = r0; r < r1;) {
             const uint64_t b = owner(A.req_off, A.num_segments, r);
             const uint64_t rend = A.req_off[b + 1] < r1 ? A.req_off[b + 1] : r1;
             const uint64_t s0 = A.seg[b], nend = A.seg[b + 1], nb = nend - s0;
-            // slice g of the snapshot's starts (nb * g fits: nb < 2^48 assumed by the host)
+            // slice g of the snapshot's starts (nb * g fits: nb < 2^40, g < 2^10)
             const uint64_t a = s0 + nb * g / A.parts, e = s0 + nb * (g + 1) / A.parts;
             for (uint64_t c0 = a; c0 < e; c0 += kChunk) {
                 const uint64_t c1 = c0 + kChunk < e ? c0 + kChunk : e;
                 const uint64_t hi = c0 + kStage < nend ? c0 + kStage : nend;  // staged [c0, hi]
-                // pinned counts relative to the chunk's first index (< 2^13)
-                const uint64_t rbase = pf.R(c0);
+                const uint32_t nA = static_cast<uint32_t>(c1 - c0);
+                const uint32_t nB = static_cast<uint32_t>(hi - c0);
+                const uint64_t pbase = pf.P(c0), rbase = pf.R(c0);
+                const U128 cbase = pf.C(c0);
+                if (tid == 0) big_flag = 0;
+                __syncthreads();  // the previous chunk's readers are done; flag cleared
+                bool big = false;
                 for (uint64_t x = c0 + tid; x <= hi; x += kThreads) {
-                    Ps[x - c0] = pf.P(x);
-                    Rs[x - c0] = static_cast<uint32_t>(pf.R(x) - rbase);
+                    const uint64_t pr = pf.P(x) - pbase;
+                    big |= pr >= kPackOne;
+                    Y[x - c0] = ((pf.R(x) - rbase) << kPackBits) + pr;
+                    Cr[x - c0] = sub128(pf.C(x), cbase);
                 }
-                const uint64_t i0 = c0 + static_cast<uint64_t>(tid) * kItems;  // this thread's starts
+                if (tid == 0) {
+                    Y[nB + 1] = kEndKey;
+                    Cr[nB + 1] = U128{0, 0};
+                }
+                // a block of 2^51 bytes or more could wrap the staged byte count
+                for (uint64_t x = c0 + tid; x < hi; x += kThreads)
+                    big |= pf.P(x + 1) - pf.P(x) >= kPackOne;
+                if (big) big_flag = 1;
                 __syncthreads();
+                const bool packed_chunk = big_flag == 0;
+                const uint64_t span = packed_chunk ? Y[nB] & (kPackOne - 1) : 0;
                 for (uint64_t rr = r; rr < rend; ++rr) {
                     const uint64_t S = A.req_sizes[rr];
                     if (S == 0) continue;
                     Best mine = best_none();
-                    uint64_t k = kNone;
-#pragma unroll 1
-                    for (uint32_t u = 0; u < kItems; ++u) {
-                        const uint64_t i = i0 + u;
-                        if (i >= c1) break;
-                        const uint64_t pi = Ps[i - c0];
-                        const uint32_t ri = Rs[i - c0];
-                        // pred(x): x is past the run of i or [i, x) holds S bytes;
-                        // monotone in x, and the first x where it holds is the end
-                        // of the shortest window from i (or a pinned-crossing one)
-                        auto pred_lds = [&](uint64_t x) {
-                            return Rs[x - c0] != ri || Ps[x - c0] - pi >= S;
-                        };
-                        auto pred_glb = [&](uint64_t x) {
-                            return pf.R(x) - rbase != ri || pf.P(x) - pi >= S;
-                        };
-                        uint64_t x;
-                        if (k == kNone) {
-                            if (pred_lds(hi)) {
-                                uint64_t lo2 = i + 1, hi2 = hi;
-                                while (lo2 < hi2) {
-                                    const uint64_t mid = (lo2 + hi2) >> 1;
-                                    if (pred_lds(mid)) hi2 = mid; else lo2 = mid + 1;
-                                }
-                                x = lo2;
-                            } else if (hi < nend && pred_glb(nend)) {
-                                uint64_t lo2 = hi + 1, hi2 = nend;
-                                while (lo2 < hi2) {
-                                    const uint64_t mid = (lo2 + hi2) >> 1;
-                                    if (pred_glb(mid)) hi2 = mid; else lo2 = mid + 1;
-                                }
-                                x = lo2;
-                            } else {
-                                break;  // no window from i, nor from any later start
-                            }
-                        } else {
-                            x = k > i + 1 ? k : i + 1;
-                            while (x <= hi && !pred_lds(x)) ++x;
-                            if (x > hi) {
-                                while (x <= nend && !pred_glb(x)) ++x;
-                                if (x > nend) break;
-                            }
+                    if (!packed_chunk || S > kPackOne - span) {
+                        // the packed keys would not decide correctly: global walk
+                        const uint64_t per = (nA + kThreads - 1) / kThreads;
+                        const uint64_t i0 = c0 + tid * per;
+                        walk_global(pf, i0 < c1 ? i0 : c1, i0 + per < c1 ? i0 + per : c1, nend,
+                                    S, mine);
+                    } else {
+                        // merge path over targets Y[i] + S (i < nA) and end keys Y[1..nB]
+                        const uint32_t M = nA + nB;
+                        const uint32_t Ls = (M + kThreads - 1) / kThreads;
+                        const uint32_t d = tid * Ls < M ? tid * Ls : M;
+                        uint32_t lo = d > nB ? d - nB : 0, hi2 = d < nA ? d : nA;
+                        while (lo < hi2) {
+                            const uint32_t mid = (lo + hi2) >> 1;
+                            // start mid goes before end key Y[d - mid] iff its target is at
+                            // or below it
+                            if (Y[mid] + S <= Y[d - mid]) lo = mid + 1; else hi2 = mid;
                         }
-                        k = x;
-                        const bool in = x <= hi;
-                        const uint64_t rk = in ? Rs[x - c0] : pf.R(x) - rbase;
-                        if (rk == ri) {
-                            const uint64_t pk = in ? Ps[x - c0] : pf.P(x);
-                            const U128 cost = sub128(pf.C(x), pf.C(i));
-                            const Best cand{cost.lo, cost.hi, pk - pi, i, x};
-                            if (best_less(cand, mine)) mine = cand;
+                        uint32_t pa = lo, pb = d - lo + 1;  // next start, next end key index
+                        const uint32_t steps = d + Ls < M ? Ls : M - d;
+                        uint64_t bc_lo = kNone, bc_hi = kNone, bd = kNone;
+                        uint32_t bs = ~0u, be = 0;
+                        for (uint32_t t = 0; t < steps; ++t) {
+                            const uint64_t ya = Y[pa], yb = Y[pb];
+                            const bool takeA = (pa < nA) & (ya + S <= yb);
+                            const uint64_t D = yb - ya;
+                            const bool valid = takeA & (D < kPackOne);
+                            const U128 ca = Cr[pa], cb = Cr[pb];
+                            const U128 cost = sub128(cb, ca);
+                            const bool better =
+                                valid & ((cost.hi < bc_hi) |
+                                         ((cost.hi == bc_hi) &
+                                          ((cost.lo < bc_lo) | ((cost.lo == bc_lo) & (D < bd)))));
+                            bc_lo = better ? cost.lo : bc_lo;
+                            bc_hi = better ? cost.hi : bc_hi;
+                            bd = better ? D : bd;
+                            bs = better ? pa : bs;
+                            be = better ? pb : be;
+                            pa += takeA ? 1u : 0u;
+                            pb += takeA ? 0u : 1u;
+                        }
+                        // within a lane starts come in increasing order, so strict
+                        // comparison kept the lowest start among equal (cost, bytes)
+                        if (bs != ~0u) mine = Best{bc_lo, bc_hi, bd, c0 + bs, c0 + be};
+                        if (hi < nend) {
+                            // starts whose target is above every staged end key: their
+                            // windows end past hi (or nowhere); a suffix of the chunk
+                            uint32_t plo = 0, phi = nA;
+                            const uint64_t ylast = Y[nB];
+                            while (plo < phi) {
+                                const uint32_t mid = (plo + phi) >> 1;
+                                if (Y[mid] + S > ylast) phi = mid; else plo = mid + 1;
+                            }
+                            const uint64_t np = nA - plo;
+                            if (np) {
+                                const uint64_t per = (np + kThreads - 1) / kThreads;
+                                const uint64_t q0 = c0 + plo + tid * per;
+                                walk_global(pf, q0 < c1 ? q0 : c1, q0 + per < c1 ? q0 + per : c1,
+                                            nend, S, mine);
+                            }
                         }
                     }
-                    const Best m = block_min(mine, wred);
-                    if (tid == 0 && best_less(m, best[rr - r0])) best[rr - r0] = m;
+                    const Best m = wave_min(mine);
+                    if (lane == 0 && best_less(m, bestw[w][rr - r0])) bestw[w][rr - r0] = m;
                 }
-                __syncthreads();
             }
             r = rend;
         }
         __syncthreads();
-        if (tid < r1 - r0) A.slots[(r0 + tid) * A.parts + g] = best[tid];
+        if (tid < r1 - r0) {
+            Best m = bestw[0][tid];
+            for (uint32_t v = 1; v < kWaves; ++v)
+                if (best_less(bestw[v][tid], m)) m = bestw[v][tid];
+            A.slots[(r0 + tid) * A.parts + g] = m;
+        }
         __syncthreads();
     }
 }
