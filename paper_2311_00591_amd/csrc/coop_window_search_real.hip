@@ -25,7 +25,7 @@
 //      consecutive requests and one of `parts` equal slices of each
 //      request's snapshot.  It walks its slice in chunks of 2048 starts;
 //      for each chunk it stages packed byte/pinned-count keys and cost
-//      prefixes of up to 3073 indices (the chunk and the blocks after it)
+//      prefixes of up to 2561 indices (the chunk and the blocks after it)
 //      in LDS, then runs every request of the group that shares the
 //      snapshot as a merge path (see the kernel).  A window [i, k) is valid
 //      iff it holds no pinned block; its cost is C[k] - C[i].  Each
@@ -50,7 +50,7 @@ constexpr uint32_t kTileLog2 = 11;
 constexpr uint32_t kTile = 1u << kTileLog2;  // blocks per prefix tile
 static_assert(kTile == kThreads * kItems, "tile = threads x items");
 constexpr uint32_t kChunk = kThreads * kItems;  // starts per staged chunk
-constexpr uint32_t kStage = kChunk + kChunk / 2;  // staged prefix indices beyond a chunk's start
+constexpr uint32_t kStage = kChunk + kChunk / 4;  // staged prefix indices beyond a chunk's start
 // Packed staged keys: Y(x) = (pinned count since the chunk start) * 2^51 +
 // (bytes since the chunk start).  With fewer than 4096 staged indices and
 // staged bytes plus S below 2^51, Y(x) >= Y(i) + S holds exactly when x is
@@ -61,9 +61,9 @@ constexpr uint64_t kPackOne = 1ull << kPackBits;
 static_assert(kStage < (1u << (63 - kPackBits)), "packed keys stay below 2^63");
 constexpr uint64_t kEndKey = ~0ull;  // above every target: stops every merge
 constexpr uint32_t kMaxGroup = 16;              // requests per search workgroup
-constexpr uint32_t kTargetGroups = 2048;        // search workgroups aimed for
+constexpr uint32_t kTargetGroups = 4096;        // search workgroups aimed for
 constexpr uint32_t kMaxParts = 1024;
-constexpr uint32_t kOffsetThreads = 256;
+constexpr uint32_t kOffsetThreads = 1024;
 constexpr uint64_t kNone = ~0ull;
 constexpr uint32_t kErrValue = 1;
 
@@ -180,6 +180,10 @@ __device__ __forceinline__ Tri wave_scan(Tri v) {
 __global__ void real_status_kernel(uint32_t* status) { *status = 0; }
 
 // Stage 1.  Tile t covers prefix indices [t * 2048, min((t + 1) * 2048, n + 1)).
+// Each thread holds 8 consecutive blocks: 16-byte loads of sizes and h and
+// an 8-byte load of kinds when the block lies wholly inside the batch and
+// the inputs are aligned, single loads otherwise; the prefixes go out as
+// 16-byte stores the same way.
 __global__ __launch_bounds__(kThreads) void real_tile_kernel(
     const uint64_t* __restrict__ size, const double* __restrict__ h,
     const uint8_t* __restrict__ kind, uint64_t n, uint64_t num_tiles, uint64_t* __restrict__ pl,
@@ -187,23 +191,48 @@ __global__ __launch_bounds__(kThreads) void real_tile_kernel(
     Tri* __restrict__ tot, uint32_t* __restrict__ status) {
     __shared__ Tri wtot[kWaves];
     const uint32_t tid = threadIdx.x, lane = tid & 63u, w = tid >> 6;
+    const bool aligned = ((reinterpret_cast<uintptr_t>(size) | reinterpret_cast<uintptr_t>(h)) &
+                          15u) == 0 && (reinterpret_cast<uintptr_t>(kind) & 7u) == 0;
     for (uint64_t t = blockIdx.x; t < num_tiles; t += gridDim.x) {
         const uint64_t base = t * kTile + tid * kItems;
+        const bool full = base + kItems <= n;
         uint64_t sz[kItems];
+        double hv[kItems];
+        uint8_t kd[kItems];
+        if (full && aligned) {
+            const ulonglong2* s2 = reinterpret_cast<const ulonglong2*>(size + base);
+            const double2* h2 = reinterpret_cast<const double2*>(h + base);
+#pragma unroll
+            for (uint32_t v = 0; v < kItems / 2; ++v) {
+                const ulonglong2 a = s2[v];
+                const double2 c = h2[v];
+                sz[2 * v] = a.x; sz[2 * v + 1] = a.y;
+                hv[2 * v] = c.x; hv[2 * v + 1] = c.y;
+            }
+            const uint2 k8 = *reinterpret_cast<const uint2*>(kind + base);
+#pragma unroll
+            for (uint32_t u = 0; u < 4; ++u) {
+                kd[u] = static_cast<uint8_t>(k8.x >> (8 * u));
+                kd[u + 4] = static_cast<uint8_t>(k8.y >> (8 * u));
+            }
+        } else {
+#pragma unroll
+            for (uint32_t u = 0; u < kItems; ++u) {
+                const uint64_t k = base + u;
+                const bool in = k < n;
+                sz[u] = in ? size[k] : 0;
+                hv[u] = in ? h[k] : 0.0;
+                kd[u] = in ? kind[k] : static_cast<uint8_t>(COOP_FREE);
+            }
+        }
         U128 cq[kItems];
         uint32_t pin = 0;  // bit u: item u pinned
         bool bad = false;
 #pragma unroll
         for (uint32_t u = 0; u < kItems; ++u) {
-            const uint64_t k = base + u;
-            sz[u] = 0;
             cq[u] = U128{0, 0};
-            if (k < n) {
-                const uint8_t kd = kind[k];
-                sz[u] = size[k];
-                if (kd >= COOP_PINNED) pin |= 1u << u;
-                if (kd == COOP_EVICTABLE && !to_fixed(h[k], cq[u])) bad = true;
-            }
+            if (kd[u] >= COOP_PINNED) pin |= 1u << u;
+            if (kd[u] == COOP_EVICTABLE && !to_fixed(hv[u], cq[u])) bad = true;
         }
         if (__ballot(bad) != 0 && lane == 0) atomicOr(status, kErrValue);
         Tri mine{0, U128{0, 0}, 0};
@@ -222,44 +251,72 @@ __global__ __launch_bounds__(kThreads) void real_tile_kernel(
         for (uint32_t v = w; v < kWaves; ++v) all = add_tri(all, wtot[v]);
         __syncthreads();
         run = add_tri(run, Tri{inc.p - mine.p, sub128(inc.c, mine.c), inc.r - mine.r});
+        uint64_t op[kItems], oc_lo[kItems], oc_hi[kItems];
+        uint16_t orr[kItems];
 #pragma unroll
         for (uint32_t u = 0; u < kItems; ++u) {
-            const uint64_t k = base + u;
-            if (k <= n) {
-                pl[k] = run.p;
-                cl_lo[k] = run.c.lo;
-                cl_hi[k] = run.c.hi;
-                rl[k] = static_cast<uint16_t>(run.r);
-            }
+            op[u] = run.p;
+            oc_lo[u] = run.c.lo;
+            oc_hi[u] = run.c.hi;
+            orr[u] = static_cast<uint16_t>(run.r);
             run.p += sz[u];
             run.c = add128(run.c, cq[u]);
             run.r += (pin >> u) & 1u;
+        }
+        if (full) {  // the workspace arrays are 256-byte aligned
+#pragma unroll
+            for (uint32_t v = 0; v < kItems / 2; ++v) {
+                reinterpret_cast<ulonglong2*>(pl + base)[v] = ulonglong2{op[2 * v], op[2 * v + 1]};
+                reinterpret_cast<ulonglong2*>(cl_lo + base)[v] =
+                    ulonglong2{oc_lo[2 * v], oc_lo[2 * v + 1]};
+                reinterpret_cast<ulonglong2*>(cl_hi + base)[v] =
+                    ulonglong2{oc_hi[2 * v], oc_hi[2 * v + 1]};
+            }
+            uint4 r8;
+            r8.x = orr[0] | (static_cast<uint32_t>(orr[1]) << 16);
+            r8.y = orr[2] | (static_cast<uint32_t>(orr[3]) << 16);
+            r8.z = orr[4] | (static_cast<uint32_t>(orr[5]) << 16);
+            r8.w = orr[6] | (static_cast<uint32_t>(orr[7]) << 16);
+            *reinterpret_cast<uint4*>(rl + base) = r8;
+        } else {
+#pragma unroll
+            for (uint32_t u = 0; u < kItems; ++u) {
+                const uint64_t k = base + u;
+                if (k <= n) {
+                    pl[k] = op[u];
+                    cl_lo[k] = oc_lo[u];
+                    cl_hi[k] = oc_hi[u];
+                    rl[k] = orr[u];
+                }
+            }
         }
         if (tid == 0) tot[t] = all;
     }
 }
 
-// Stage 2: exclusive tile offsets, one workgroup.
+// Stage 2: exclusive tile offsets, one workgroup; each thread sums a run of
+// consecutive tiles, the runs are scanned, then each thread writes its
+// tiles' offsets.
 __global__ __launch_bounds__(kOffsetThreads) void real_offsets_kernel(const Tri* __restrict__ tot,
                                                                       uint64_t num_tiles,
                                                                       Tri* __restrict__ off) {
     __shared__ Tri wtot[kOffsetThreads / 64];
     const uint32_t tid = threadIdx.x, lane = tid & 63u, w = tid >> 6;
-    Tri carry{0, U128{0, 0}, 0};
-    for (uint64_t c0 = 0; c0 < num_tiles; c0 += kOffsetThreads) {
-        const uint64_t t = c0 + tid;
-        const Tri mine = t < num_tiles ? tot[t] : Tri{0, U128{0, 0}, 0};
-        const Tri inc = wave_scan(mine);
-        if (lane == 63) wtot[w] = inc;
-        __syncthreads();
-        Tri run = carry;
-        for (uint32_t v = 0; v < w; ++v) run = add_tri(run, wtot[v]);
-        Tri next = carry;
-        for (uint32_t v = 0; v < kOffsetThreads / 64; ++v) next = add_tri(next, wtot[v]);
-        __syncthreads();
-        if (t < num_tiles) off[t] = add_tri(run, Tri{inc.p - mine.p, sub128(inc.c, mine.c),
-                                                     inc.r - mine.r});
-        carry = next;
+    const uint64_t per = (num_tiles + kOffsetThreads - 1) / kOffsetThreads;
+    const uint64_t t0 = tid * per < num_tiles ? tid * per : num_tiles;
+    const uint64_t t1 = t0 + per < num_tiles ? t0 + per : num_tiles;
+    Tri mine{0, U128{0, 0}, 0};
+    for (uint64_t t = t0; t < t1; ++t) mine = add_tri(mine, tot[t]);
+    const Tri inc = wave_scan(mine);
+    if (lane == 63) wtot[w] = inc;
+    __syncthreads();
+    Tri run{0, U128{0, 0}, 0};
+    for (uint32_t v = 0; v < w; ++v) run = add_tri(run, wtot[v]);
+    run = add_tri(run, Tri{inc.p - mine.p, sub128(inc.c, mine.c), inc.r - mine.r});
+    for (uint64_t t = t0; t < t1; ++t) {
+        const Tri x = tot[t];
+        off[t] = run;
+        run = add_tri(run, x);
     }
 }
 
@@ -359,7 +416,7 @@ __device__ void walk_global(const Prefix& pf, uint64_t i, uint64_t i_end, uint64
 }
 
 // Stage 3.  Per chunk the workgroup stages, for the indices [c0, hi] (the
-// chunk's starts and the blocks after them, at most 3073), the packed keys
+// chunk's starts and the blocks after them, at most 2561), the packed keys
 // Y and the fixed-point cost prefixes relative to c0 in LDS.  Each request
 // is then a merge of two sorted sequences, the targets Y(i) + S of the
 // starts and the end keys Y(x): a start meets, when it is merged, the first

@@ -171,3 +171,32 @@ def test_invalid_values_set_the_status_bit(bad):
     # -0.0 is a valid zero, and the status word is cleared by every call
     _, _, status = gpu_real(pools, np.array([1.0, -0.0]))
     assert status == 0
+
+
+def test_unaligned_inputs():
+    """Inputs that start 8 bytes (sizes, h) and 1 byte (kinds) past an
+    aligned address take the single-load path of the prefix kernel."""
+    import paper_2311_00591_amd as coop
+    pools = workloads.make_config(1, 4, num_segments=8)
+    h = workloads.real_costs(pools, 4)
+    _announce("unaligned inputs")
+
+    def shifted(a, dt):
+        t = torch.zeros(len(a) + 1, dtype=dt, device="cuda")
+        t[1:] = torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
+        return t[1:]
+
+    size = shifted(pools.size.view(np.int64), torch.int64)
+    ht = shifted(h, torch.float64)
+    kind = shifted(pools.kind, torch.uint8)
+    assert size.data_ptr() % 16 == 8 and kind.data_ptr() % 8 == 1
+    _, _, _, seg, req, roff = coop.to_device(pools, "cuda")
+    r = coop.WindowSearchReal(size, ht, kind, seg, req, roff)
+    r.launch()
+    torch.cuda.synchronize()
+    want, want_cost = oracle.window_search_real(pools.size, h, pools.kind, pools.seg_offsets,
+                                                pools.req_sizes, pools.req_offsets, threads=4)
+    out = r.out.cpu().numpy()
+    assert int(r.status.item()) == 0
+    assert np.array_equal(out[:, :4].view(np.uint64), want)
+    assert np.array_equal(out[:, 4].copy().view(np.uint64), want_cost.view(np.uint64))
