@@ -123,10 +123,28 @@ def cpu_baseline(pools, target_s, op="window", h=None):
     for _ in range(reps):
         fn(*args, threads=threads)
     dt = time.perf_counter() - t0
+    # one thread, on the whole workload when that takes under a quarter of
+    # the budget, else not measured
+    single = None
+    if one * threads < target_s / 4:
+        t0 = time.perf_counter()
+        fn(*args, threads=1)
+        single = pools.num_requests / (time.perf_counter() - t0)
     return {"value": reps * pools.num_requests / dt, "unit": "queries/s", "cores": threads,
-            "kind": "oracle",
+            "kind": "oracle", "single_thread_value": single, "cpu_model": _cpu_model(),
             "sample": f"whole workload ({pools.num_requests} requests) x {reps} passes, "
                       f"{dt:.1f} s, {what}, {threads} threads"}
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def main():
