@@ -248,7 +248,7 @@ typedef enum {
  * status (device u32): set to 0, then bit 0 if a pool ran out of slots (that
  *   allocation is skipped), bit 1 for an invalid operation.
  * workspace: coop_replay_workspace_size() bytes (device, caller-owned).
- * Pools of up to about 4170 slots (39 bytes of LDS a slot, within 160 KiB)
+ * Pools of up to about 5250 slots (31 bytes of LDS a slot, within 160 KiB)
  * are replayed by two launches, a workgroup per pool holding the pool in
  * LDS; larger ones step by step, about five launches per operation (the
  * greedy policy skips the window search's).  Either way everything is enqueued on `stream`; nothing is

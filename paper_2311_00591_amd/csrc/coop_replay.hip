@@ -389,18 +389,19 @@ __global__ __launch_bounds__(kThreads) void replay_update_kernel(
 constexpr uint32_t kResThreads = 256;
 constexpr uint32_t kResWaves = kResThreads / 64;
 
-// LDS bytes for a pool of cap slots, 39 a slot: size, cost, prefix bytes and
-// cost (u64), tensor id (u32), pinned-count prefix (u16), kind (u8); plus one
-// prefix entry and padding to 8 bytes.
+// LDS bytes for a pool of cap slots, 31 a slot: size (which holds the byte
+// prefix sums during a window search), cost and cost prefix (u64), tensor id
+// (u32), pinned-count prefix (u16), kind (u8); plus one prefix entry and
+// padding to 8 bytes.  A pool of 2072 slots takes 64 KB, so two pools share
+// a CU.
 __host__ __device__ constexpr size_t resident_lds_bytes(uint64_t cap) {
-    return ((cap * 8 + 7) & ~7ull) * 2 + ((cap + 1) * 8) * 2 + ((cap * 4 + 7) & ~7ull) +
+    return ((cap + 1) * 8) * 2 + cap * 8 + ((cap * 4 + 7) & ~7ull) +
            (((cap + 1) * 2 + 7) & ~7ull) + ((cap + 7) & ~7ull);
 }
 
 struct Lds {
-    uint64_t* sz;
+    uint64_t* sz;  // sizes; byte prefix sums while res_window runs
     uint64_t* co;
-    uint64_t* P;
     uint64_t* C;
     uint32_t* id;
     uint16_t* R;
@@ -410,9 +411,8 @@ struct Lds {
 __device__ Lds lds_layout(char* base, uint64_t cap) {
     Lds l;
     size_t at = 0;
-    l.sz = reinterpret_cast<uint64_t*>(base + at); at += (cap * 8 + 7) & ~7ull;
-    l.co = reinterpret_cast<uint64_t*>(base + at); at += (cap * 8 + 7) & ~7ull;
-    l.P = reinterpret_cast<uint64_t*>(base + at); at += (cap + 1) * 8;
+    l.sz = reinterpret_cast<uint64_t*>(base + at); at += (cap + 1) * 8;
+    l.co = reinterpret_cast<uint64_t*>(base + at); at += cap * 8;
     l.C = reinterpret_cast<uint64_t*>(base + at); at += (cap + 1) * 8;
     l.id = reinterpret_cast<uint32_t*>(base + at); at += (cap * 4 + 7) & ~7ull;
     l.R = reinterpret_cast<uint16_t*>(base + at); at += ((cap + 1) * 2 + 7) & ~7ull;
@@ -501,7 +501,9 @@ __device__ void res_replace(const Lds& l, uint64_t n, uint64_t lo, uint64_t hi, 
     __syncthreads();
 }
 
-// The window search for S > 0 over a pool of n blocks held in LDS.
+// The window search for S > 0 over a pool of n blocks held in LDS.  The
+// byte prefix sums P overwrite the sizes for the search (P[k] in sz[k],
+// P[n] in sz[n]); the sizes are put back before it returns.
 __device__ WinKey res_window(const Lds& l, uint64_t n, uint64_t S, uint64_t* red, WinKey* wred) {
     const uint32_t tid = threadIdx.x, lane = tid & 63u, w = tid >> 6;
     // each thread owns blocks [a, a1): local sums, then a workgroup scan
@@ -533,38 +535,40 @@ __device__ WinKey res_window(const Lds& l, uint64_t n, uint64_t S, uint64_t* red
     }
     __syncthreads();
     uint64_t xs = bs + is - ps, xc = bc + ic - pc, xr = br + ir - pr;
-    for (uint64_t k = a; k < a1; ++k) {
-        l.P[k] = xs; l.C[k] = xc; l.R[k] = static_cast<uint16_t>(xr);
-        xs += l.sz[k];
+    for (uint64_t k = a; k < a1; ++k) {  // each thread rewrites only its own blocks
+        const uint64_t szk = l.sz[k];
+        l.sz[k] = xs; l.C[k] = xc; l.R[k] = static_cast<uint16_t>(xr);
+        xs += szk;
         xc += l.kd[k] == COOP_EVICTABLE ? l.co[k] : 0;
         xr += l.kd[k] >= COOP_PINNED ? 1 : 0;
     }
     if (a1 == n && a < a1) {
-        l.P[n] = xs; l.C[n] = xc; l.R[n] = static_cast<uint16_t>(xr);
+        l.sz[n] = xs; l.C[n] = xc; l.R[n] = static_cast<uint16_t>(xr);
     }
     if (n == 0 && tid == 0) {
-        l.P[0] = 0; l.C[0] = 0; l.R[0] = 0;
+        l.sz[0] = 0; l.C[0] = 0; l.R[0] = 0;
     }
     __syncthreads();
+    const uint64_t* const P = l.sz;
     // starts [a, a1): the first end by bisection, later ends by walking on
     WinKey best{kNone, kNone, kNone, kNone};
     uint64_t k = 0;
     for (uint64_t i = a; i < a1; ++i) {
-        const uint64_t pi = l.P[i];
+        const uint64_t pi = P[i];
         if (i == a) {
             uint64_t lo = i + 1, hi = n + 1;  // first k in [i + 1, n] with P[k] - P[i] >= S, or n + 1
             while (lo < hi) {
                 const uint64_t mid = (lo + hi) >> 1;
-                if (l.P[mid] - pi >= S) hi = mid; else lo = mid + 1;
+                if (P[mid] - pi >= S) hi = mid; else lo = mid + 1;
             }
             k = lo;
         } else {
             if (k < i + 1) k = i + 1;
-            while (k <= n && l.P[k] - pi < S) ++k;
+            while (k <= n && P[k] - pi < S) ++k;
         }
         if (k > n) break;  // no later start of this thread reaches S either
         if (l.R[k] == l.R[i]) {
-            const WinKey c{l.C[k] - l.C[i], l.P[k] - pi, i, k};
+            const WinKey c{l.C[k] - l.C[i], P[k] - pi, i, k};
             if (win_less(c, best)) best = c;
         }
     }
@@ -575,10 +579,20 @@ __device__ WinKey res_window(const Lds& l, uint64_t n, uint64_t S, uint64_t* red
         if (win_less(x, best)) best = x;
     }
     if (lane == 0) wred[w] = best;
-    __syncthreads();
+    __syncthreads();  // also: every read of P is done
     WinKey m = wred[0];
     for (uint32_t v = 1; v < kResWaves; ++v)
         if (win_less(wred[v], m)) m = wred[v];
+    // sizes back from the prefixes: sz[k] = P[k + 1] - P[k], each thread over
+    // its own blocks, last to first, after reading the prefix just past them
+    uint64_t nxt = a < a1 ? P[a1] : 0;
+    __syncthreads();
+    for (uint64_t k = a1; k > a;) {
+        --k;
+        const uint64_t pk = l.sz[k];
+        l.sz[k] = nxt - pk;
+        nxt = pk;
+    }
     __syncthreads();
     return m;
 }

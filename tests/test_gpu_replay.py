@@ -174,9 +174,20 @@ def test_pools_too_large_for_lds_take_the_stepwise_path(policy):
     """Capacity beyond what one workgroup's LDS holds: the replay runs one
     step per operation with the batched first-fit and window kernels."""
     _announce(f"stepwise path, policy {policy}")
-    import paper_2311_00591_amd as coop
+    state, trace = traces.make_replay(1, 7, layers=2700, num_pools=6, iterations=1,
+                                      budget_frac=0.9)
+    # 31 bytes of LDS per slot (sizes or byte prefixes, costs, cost
+    # prefixes, ids, pinned counts, kinds): above 160 KiB
+    assert state["capacity"] * 31 > 160 * 1024
+    assert_same(state, trace, f"stepwise policy {policy}", policy)
+
+
+@pytest.mark.parametrize("policy", [WINDOW, GREEDY])
+def test_large_pools_held_in_lds(policy):
+    """A capacity that still fits one workgroup's LDS but needs more than
+    64 KiB of it (one pool per CU)."""
+    _announce(f"large resident pools, policy {policy}")
     state, trace = traces.make_replay(1, 7, layers=2200, num_pools=6, iterations=1,
                                       budget_frac=0.9)
-    # 39 bytes of LDS per slot (pool, prefix sums, ids, run counts): above 160 KiB
-    assert state["capacity"] * 39 > 160 * 1024
-    assert_same(state, trace, f"stepwise policy {policy}", policy)
+    assert 64 * 1024 < state["capacity"] * 31 < 150 * 1024
+    assert_same(state, trace, f"large resident policy {policy}", policy)
