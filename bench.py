@@ -150,8 +150,8 @@ def _cpu_model():
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for {args.gpus}); "
-              "multi-GPU sharding is a design note, not implemented", file=sys.stderr)
+        print(f"bench.py: the search runs on one GPU only (asked for {args.gpus}); "
+              "sharding across GPUs is not implemented", file=sys.stderr)
         sys.exit(2)
 
     import torch
