@@ -60,6 +60,11 @@ constexpr uint32_t kPackBits = 51;
 constexpr uint64_t kPackOne = 1ull << kPackBits;
 static_assert(kStage < (1u << (63 - kPackBits)), "packed keys stay below 2^63");
 constexpr uint64_t kEndKey = ~0ull;  // above every target: stops every merge
+// Every lane walks the same number of merge steps, at most this many; a lane
+// whose slice ends earlier goes on into its neighbour's (the same windows
+// again) or past the end keys, into this many more sentinel keys.
+constexpr uint32_t kPadSteps = 32;
+static_assert(kPadSteps >= (kChunk + kStage + kThreads - 1) / kThreads, "padding covers a slice");
 constexpr uint32_t kMaxGroup = 16;              // requests per search workgroup
 constexpr uint32_t kTargetGroups = 4096;        // search workgroups aimed for
 constexpr uint32_t kMaxParts = 1024;
@@ -429,8 +434,8 @@ __device__ void walk_global(const Prefix& pf, uint64_t i, uint64_t i_end, uint64
 // window per request, so a request costs no barrier; the wavefronts' minima
 // meet once per unit.
 __global__ __launch_bounds__(kThreads) void real_search_kernel(Prefix pf, SearchArgs A) {
-    __shared__ uint64_t Y[kStage + 2];
-    __shared__ U128 Cr[kStage + 2];
+    __shared__ uint64_t Y[kStage + 1 + kPadSteps + 1];
+    __shared__ U128 Cr[kStage + 1 + kPadSteps + 1];
     __shared__ Best bestw[kWaves][kMaxGroup];
     __shared__ int big_flag;
     const uint32_t tid = threadIdx.x, lane = tid & 63u, w = tid >> 6;
@@ -461,9 +466,9 @@ __global__ __launch_bounds__(kThreads) void real_search_kernel(Prefix pf, Search
                     Y[x - c0] = ((pf.R(x) - rbase) << kPackBits) + pr;
                     Cr[x - c0] = sub128(pf.C(x), cbase);
                 }
-                if (tid == 0) {
-                    Y[nB + 1] = kEndKey;
-                    Cr[nB + 1] = U128{0, 0};
+                if (tid <= kPadSteps) {
+                    Y[nB + 1 + tid] = kEndKey;
+                    Cr[nB + 1 + tid] = U128{0, 0};
                 }
                 // a block of 2^51 bytes or more could wrap the staged byte count
                 for (uint64_t x = c0 + tid; x < hi; x += kThreads)
@@ -495,20 +500,22 @@ __global__ __launch_bounds__(kThreads) void real_search_kernel(Prefix pf, Search
                             if (Y[mid] + S <= Y[d - mid]) lo = mid + 1; else hi2 = mid;
                         }
                         uint32_t pa = lo, pb = d - lo + 1;  // next start, next end key index
-                        const uint32_t steps = d + Ls < M ? Ls : M - d;
                         uint64_t bc_lo = kNone, bc_hi = kNone, bd = kNone;
                         uint32_t bs = ~0u, be = 0;
-                        for (uint32_t t = 0; t < steps; ++t) {
+#pragma unroll 2
+                        for (uint32_t t = 0; t < Ls; ++t) {  // the same count in every lane
                             const uint64_t ya = Y[pa], yb = Y[pb];
+                            const U128 ca = Cr[pa], cb = Cr[pb];
                             const bool takeA = (pa < nA) & (ya + S <= yb);
                             const uint64_t D = yb - ya;
                             const bool valid = takeA & (D < kPackOne);
-                            const U128 ca = Cr[pa], cb = Cr[pb];
                             const U128 cost = sub128(cb, ca);
-                            const bool better =
-                                valid & ((cost.hi < bc_hi) |
-                                         ((cost.hi == bc_hi) &
-                                          ((cost.lo < bc_lo) | ((cost.lo == bc_lo) & (D < bd)))));
+                            // (cost, D) < (bc, bd) as a 192-bit subtraction's final borrow
+                            unsigned long long b0, b1, b2;
+                            (void)__builtin_subcll(D, bd, 0ull, &b0);
+                            (void)__builtin_subcll(cost.lo, bc_lo, b0, &b1);
+                            (void)__builtin_subcll(cost.hi, bc_hi, b1, &b2);
+                            const bool better = valid & (b2 != 0);
                             bc_lo = better ? cost.lo : bc_lo;
                             bc_hi = better ? cost.hi : bc_hi;
                             bd = better ? D : bd;
