@@ -420,6 +420,78 @@ __device__ void walk_global(const Prefix& pf, uint64_t i, uint64_t i_end, uint64
     }
 }
 
+// The merge path of NR requests over one staged chunk, interleaved so that
+// their chains of LDS reads overlap: targets Y[i] + S (starts i < nA) against
+// end keys Y[1..nB].  Each lane bisects its diagonal (a fixed 12 rounds: the
+// range is at most nA + 1 <= 2049) and walks the same number of steps; a
+// start meets, when it is merged, the first end key at or above its target,
+// the end of its shortest window, and is scored on the spot (valid iff the
+// keys differ by less than 2^51: no pinned block between).  mine[r] receives
+// the lane's least window (batch indices).
+template <int NR>
+__device__ __forceinline__ void merge_requests(const uint64_t* Y, const U128* Cr, uint32_t nA,
+                                               uint32_t nB, const uint64_t (&S)[NR], uint64_t c0,
+                                               Best (&mine)[NR]) {
+    const uint32_t tid = threadIdx.x;
+    const uint32_t M = nA + nB;
+    const uint32_t Ls = (M + kThreads - 1) / kThreads;
+    const uint32_t d = tid * Ls < M ? tid * Ls : M;
+    uint32_t lo[NR], hi[NR];
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+        lo[r] = d > nB ? d - nB : 0;
+        hi[r] = d < nA ? d : nA;
+    }
+#pragma unroll
+    for (int it = 0; it < 12; ++it) {
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
+            if (lo[r] < hi[r]) {
+                const uint32_t mid = (lo[r] + hi[r]) >> 1;
+                // start mid goes before end key Y[d - mid] iff its target is at or below it
+                if (Y[mid] + S[r] <= Y[d - mid]) lo[r] = mid + 1; else hi[r] = mid;
+            }
+        }
+    }
+    uint32_t pa[NR], pb[NR], bs[NR], be[NR];
+    uint64_t bc_lo[NR], bc_hi[NR], bd[NR];
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+        pa[r] = lo[r];
+        pb[r] = d - lo[r] + 1;  // next start, next end key index
+        bc_lo[r] = bc_hi[r] = bd[r] = kNone;
+        bs[r] = ~0u;
+        be[r] = 0;
+    }
+    for (uint32_t t = 0; t < Ls; ++t) {  // the same count in every lane
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
+            const uint64_t ya = Y[pa[r]], yb = Y[pb[r]];
+            const U128 ca = Cr[pa[r]], cb = Cr[pb[r]];
+            const bool takeA = (pa[r] < nA) & (ya + S[r] <= yb);
+            const uint64_t D = yb - ya;
+            const bool valid = takeA & (D < kPackOne);
+            const U128 cost = sub128(cb, ca);
+            const bool better =
+                valid & ((cost.hi < bc_hi[r]) |
+                         ((cost.hi == bc_hi[r]) &
+                          ((cost.lo < bc_lo[r]) | ((cost.lo == bc_lo[r]) & (D < bd[r])))));
+            bc_lo[r] = better ? cost.lo : bc_lo[r];
+            bc_hi[r] = better ? cost.hi : bc_hi[r];
+            bd[r] = better ? D : bd[r];
+            bs[r] = better ? pa[r] : bs[r];
+            be[r] = better ? pb[r] : be[r];
+            pa[r] += takeA ? 1u : 0u;
+            pb[r] += takeA ? 0u : 1u;
+        }
+    }
+    // within a lane starts come in increasing order, so strict comparison kept
+    // the lowest start among equal (cost, bytes)
+#pragma unroll
+    for (int r = 0; r < NR; ++r)
+        if (bs[r] != ~0u) mine[r] = Best{bc_lo[r], bc_hi[r], bd[r], c0 + bs[r], c0 + be[r]};
+}
+
 // Stage 3.  Per chunk the workgroup stages, for the indices [c0, hi] (the
 // chunk's starts and the blocks after them, at most 2561), the packed keys
 // Y and the fixed-point cost prefixes relative to c0 in LDS.  Each request
@@ -477,76 +549,65 @@ __global__ __launch_bounds__(kThreads) void real_search_kernel(Prefix pf, Search
                 __syncthreads();
                 const bool packed_chunk = big_flag == 0;
                 const uint64_t span = packed_chunk ? Y[nB] & (kPackOne - 1) : 0;
-                for (uint64_t rr = r; rr < rend; ++rr) {
-                    const uint64_t S = A.req_sizes[rr];
-                    if (S == 0) continue;
-                    Best mine = best_none();
-                    if (!packed_chunk || S > kPackOne - span) {
-                        // the packed keys would not decide correctly: global walk
-                        const uint64_t per = (nA + kThreads - 1) / kThreads;
-                        const uint64_t i0 = c0 + tid * per;
-                        walk_global(pf, i0 < c1 ? i0 : c1, i0 + per < c1 ? i0 + per : c1, nend,
-                                    S, mine);
-                    } else {
-                        // merge path over targets Y[i] + S (i < nA) and end keys Y[1..nB]
-                        const uint32_t M = nA + nB;
-                        const uint32_t Ls = (M + kThreads - 1) / kThreads;
-                        const uint32_t d = tid * Ls < M ? tid * Ls : M;
-                        uint32_t lo = d > nB ? d - nB : 0, hi2 = d < nA ? d : nA;
-                        while (lo < hi2) {
-                            const uint32_t mid = (lo + hi2) >> 1;
-                            // start mid goes before end key Y[d - mid] iff its target is at
-                            // or below it
-                            if (Y[mid] + S <= Y[d - mid]) lo = mid + 1; else hi2 = mid;
-                        }
-                        uint32_t pa = lo, pb = d - lo + 1;  // next start, next end key index
-                        uint64_t bc_lo = kNone, bc_hi = kNone, bd = kNone;
-                        uint32_t bs = ~0u, be = 0;
-#pragma unroll 2
-                        for (uint32_t t = 0; t < Ls; ++t) {  // the same count in every lane
-                            const uint64_t ya = Y[pa], yb = Y[pb];
-                            const U128 ca = Cr[pa], cb = Cr[pb];
-                            const bool takeA = (pa < nA) & (ya + S <= yb);
-                            const uint64_t D = yb - ya;
-                            const bool valid = takeA & (D < kPackOne);
-                            const U128 cost = sub128(cb, ca);
-                            // (cost, D) < (bc, bd) as a 192-bit subtraction's final borrow
-                            unsigned long long b0, b1, b2;
-                            (void)__builtin_subcll(D, bd, 0ull, &b0);
-                            (void)__builtin_subcll(cost.lo, bc_lo, b0, &b1);
-                            (void)__builtin_subcll(cost.hi, bc_hi, b1, &b2);
-                            const bool better = valid & (b2 != 0);
-                            bc_lo = better ? cost.lo : bc_lo;
-                            bc_hi = better ? cost.hi : bc_hi;
-                            bd = better ? D : bd;
-                            bs = better ? pa : bs;
-                            be = better ? pb : be;
-                            pa += takeA ? 1u : 0u;
-                            pb += takeA ? 0u : 1u;
-                        }
-                        // within a lane starts come in increasing order, so strict
-                        // comparison kept the lowest start among equal (cost, bytes)
-                        if (bs != ~0u) mine = Best{bc_lo, bc_hi, bd, c0 + bs, c0 + be};
-                        if (hi < nend) {
-                            // starts whose target is above every staged end key: their
-                            // windows end past hi (or nowhere); a suffix of the chunk
-                            uint32_t plo = 0, phi = nA;
-                            const uint64_t ylast = Y[nB];
-                            while (plo < phi) {
-                                const uint32_t mid = (plo + phi) >> 1;
-                                if (Y[mid] + S > ylast) phi = mid; else plo = mid + 1;
-                            }
-                            const uint64_t np = nA - plo;
-                            if (np) {
-                                const uint64_t per = (np + kThreads - 1) / kThreads;
-                                const uint64_t q0 = c0 + plo + tid * per;
-                                walk_global(pf, q0 < c1 ? q0 : c1, q0 + per < c1 ? q0 + per : c1,
-                                            nend, S, mine);
-                            }
-                        }
+                // starts whose target is above every staged end key: their windows
+                // end past hi (or nowhere); a suffix of the chunk, walked globally
+                auto pending = [&](uint64_t S, Best& mine) {
+                    if (hi >= nend) return;
+                    uint32_t plo = 0, phi = nA;
+                    const uint64_t ylast = Y[nB];
+                    while (plo < phi) {
+                        const uint32_t mid = (plo + phi) >> 1;
+                        if (Y[mid] + S > ylast) phi = mid; else plo = mid + 1;
                     }
-                    const Best m = wave_min(mine);
-                    if (lane == 0 && best_less(m, bestw[w][rr - r0])) bestw[w][rr - r0] = m;
+                    const uint64_t np = nA - plo;
+                    if (np) {
+                        const uint64_t per = (np + kThreads - 1) / kThreads;
+                        const uint64_t q0 = c0 + plo + tid * per;
+                        walk_global(pf, q0 < c1 ? q0 : c1, q0 + per < c1 ? q0 + per : c1, nend, S,
+                                    mine);
+                    }
+                };
+                auto fast = [&](uint64_t S) {
+                    return S != 0 && packed_chunk && S <= kPackOne - span;
+                };
+                for (uint64_t rr = r; rr < rend;) {
+                    const uint64_t S0 = A.req_sizes[rr];
+                    const bool pair = rr + 1 < rend;
+                    const uint64_t S1 = pair ? A.req_sizes[rr + 1] : 0;
+                    if (pair && fast(S0) && fast(S1)) {
+                        // two requests' merges interleaved: independent chains of LDS reads
+                        const uint64_t SS[2] = {S0, S1};
+                        Best m2[2] = {best_none(), best_none()};
+                        merge_requests<2>(Y, Cr, nA, nB, SS, c0, m2);
+#pragma unroll
+                        for (uint32_t j = 0; j < 2; ++j) {
+                            pending(SS[j], m2[j]);
+                            const Best m = wave_min(m2[j]);
+                            if (lane == 0 && best_less(m, bestw[w][rr + j - r0]))
+                                bestw[w][rr + j - r0] = m;
+                        }
+                        rr += 2;
+                        continue;
+                    }
+                    if (S0 != 0) {
+                        Best mine = best_none();
+                        if (fast(S0)) {
+                            const uint64_t SS[1] = {S0};
+                            Best m1[1] = {best_none()};
+                            merge_requests<1>(Y, Cr, nA, nB, SS, c0, m1);
+                            mine = m1[0];
+                            pending(S0, mine);
+                        } else {
+                            // the packed keys would not decide correctly: global walk
+                            const uint64_t per = (nA + kThreads - 1) / kThreads;
+                            const uint64_t i0 = c0 + tid * per;
+                            walk_global(pf, i0 < c1 ? i0 : c1, i0 + per < c1 ? i0 + per : c1,
+                                        nend, S0, mine);
+                        }
+                        const Best m = wave_min(mine);
+                        if (lane == 0 && best_less(m, bestw[w][rr - r0])) bestw[w][rr - r0] = m;
+                    }
+                    rr += 1;
                 }
             }
             r = rend;
