@@ -546,9 +546,15 @@ def bench_replay(args, dev):
         for _ in range(reps):
             oracle.replay(state, trace, threads=threads, policy=policy)
         dt = time.perf_counter() - t0
+        single = None
+        if one * threads < args.cpu_seconds / 4:
+            t0 = time.perf_counter()
+            oracle.replay(state, trace, threads=1, policy=policy)
+            single = P * T / (time.perf_counter() - t0)
         cpu = {"value": reps * P * T / dt, "unit": "operations/s", "cores": threads,
-               "kind": "oracle", "sample": f"whole replay ({P} pools x {T} operations) x {reps}, "
-                                           f"{dt:.1f} s, {threads} threads"}
+               "kind": "oracle", "single_thread_value": single, "cpu_model": _cpu_model(),
+               "sample": f"whole replay ({P} pools x {T} operations) x {reps}, "
+                         f"{dt:.1f} s, {threads} threads"}
     rec = {
         "metric": REPLAY_METRIC,
         "value": P * T / t,
