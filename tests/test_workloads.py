@@ -70,3 +70,18 @@ def test_from_lists():
     p = workloads.from_lists([([512, 1024], [0, 5], [0, 1]), ([], [], [])], [[1, 2], [3]])
     assert p.seg_offsets.tolist() == [0, 2, 2]
     assert p.req_offsets.tolist() == [0, 2, 3]
+
+
+def test_real_costs():
+    """h = cost / staleness with staleness on 1..4096: deterministic, zero off
+    evictable blocks, within [cost / 4096, cost], and not mostly integers."""
+    p = workloads.make_config(1, 0, num_segments=16)
+    h = workloads.real_costs(p, 3)
+    assert h.dtype == np.float64 and len(h) == p.num_blocks
+    assert np.array_equal(h, workloads.real_costs(p, 3))
+    assert not np.array_equal(h, workloads.real_costs(p, 4))
+    ev = p.kind == EVICTABLE
+    assert (h[~ev] == 0).all()
+    c = p.cost[ev].astype(np.float64)
+    assert (h[ev] <= c).all() and (h[ev] >= c / 4096 * (1 - 1e-15)).all()
+    assert np.mean(h[ev] != np.floor(h[ev])) > 0.9
