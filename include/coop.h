@@ -16,6 +16,11 @@
  * nothing, never synchronises the stream, and may be called from several
  * host threads (with distinct workspaces).  It needs no HIP header: streams
  * are passed as void* (a hipStream_t; NULL is the default stream).
+ *
+ * Every entry point may be called on a stream that is capturing a HIP graph,
+ * and the graph replayed any number of times: each replay recomputes the
+ * outputs from whatever the input buffers hold at that point.  No entry point
+ * records a memset node.
  */
 #ifndef COOP_H
 #define COOP_H
@@ -112,7 +117,12 @@ coop_status_t coop_window_search_plan(uint64_t num_blocks, uint64_t num_segments
  * workspace (device): at least coop_window_search_workspace_size() bytes,
  *   256-byte aligned, owned by the caller; its contents need not be
  *   initialised and are meaningless afterwards.  Two calls in flight at the
- *   same time must not share a workspace.
+ *   same time must not share a workspace.  The kernels tell one call's
+ *   cross-workgroup counters from an earlier call's by a tag: an eager call
+ *   takes it from the per-process call counter; a call made while the stream
+ *   is capturing a graph records one single-thread kernel ahead of the search
+ *   that advances a tag word kept in the workspace, and the search reads its
+ *   tag from there, so every replay gets a fresh one.
  * stream: hipStream_t the work is enqueued on; out is valid once the
  *   stream has reached this point.
  *

@@ -108,7 +108,14 @@ constexpr uint32_t kNone32 = ~0u;
 constexpr uint32_t kMaxWpr = 8;                  // wavefronts that may share one request
 constexpr uint64_t kPartialBudget = 1ull << 23;  // partial keys (32 B each) before chunks grow
 constexpr uint32_t kEpochShift = 24;             // counter = epoch << 24 | tickets
-constexpr uint64_t kEpochMask = (1ull << 40) - 1;
+// Call tags (40 bits).  An eager call takes the next value of a host counter
+// (bit 39 clear); a call captured into a graph takes bit 39 and 39 bits that
+// an odd multiplier maps one-to-one from a word in the workspace, which a
+// one-thread kernel advances ahead of every replay.  The two kinds never
+// meet, and no two replays on one workspace share a tag before 2^39 calls.
+constexpr uint64_t kTagMask = (1ull << 39) - 1;
+constexpr uint64_t kGraphTag = 1ull << 39;
+constexpr uint64_t kTagOdd = 0x9e3779b97f4a7c15ull;
 // Queue word: call tag << 32 | chunks claimed.  A reserve chunk slot holds a
 // chunk index, kQEmpty (nothing claimed yet) or kQDone (the queue ran dry).
 constexpr uint64_t kQEmpty = ~0ull, kQDone = ~0ull - 1;
@@ -263,7 +270,8 @@ struct Params {
     uint64_t qtag;         // this call's queue tag (32 bits)
     uint32_t queue_on;     // units past u1 go through the queue
     uint64_t pc;           // partial slots per request
-    uint64_t epoch;
+    uint64_t epoch;        // this call's tag on the arrival tickets
+    const uint64_t* tag_word;  // captured calls: the workspace word the tags come from
     uint32_t slices_log2;  // request slices (a power of two): slice y takes y, y + slices, ...
     double inv_slope;      // guess of b per tile id, for the first snapshot lookup
 };
@@ -1215,6 +1223,14 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
     const uint32_t tid = threadIdx.x;
     const uint32_t w = uniform(tid >> 6);
     Params P = Pin;
+    if (P.tag_word) {
+        // A call replayed from a graph: the tag word was advanced by the
+        // kernel before this one on the stream, so every workgroup reads the
+        // same value; P.epoch holds a per-process salt.
+        const uint64_t t = __hip_atomic_load(P.tag_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        P.epoch = kGraphTag | ((t * kTagOdd + P.epoch) & kTagMask);
+        P.qtag = P.epoch & 0xffffffffull;
+    }
     // The queue, when there is one: workgroup 0 stamps this call's tag; claims
     // that reach the word before the stamp see an old tag and try again.
     // Queued chunks are sized from the snapshots' tile counts, the same in
@@ -1387,7 +1403,8 @@ bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests
     pl->nchunks = nchunks;
     pl->pc = pc;
     pl->part_bytes = (num_requests * pc * sizeof(Key) + 255) & ~static_cast<size_t>(255);
-    pl->bytes = pl->part_bytes + (slices * num_segments + 1) * sizeof(uint64_t);
+    // then the arrival counters, the queue word and the tag word
+    pl->bytes = pl->part_bytes + (slices * num_segments + 2) * sizeof(uint64_t);
     return true;
 }
 
@@ -1396,6 +1413,15 @@ uint64_t magic(uint64_t d) { return d == 1 ? 0 : ~0ull / d + 1; }
 
 std::atomic<uint64_t> g_calls{
     static_cast<uint64_t>(std::chrono::steady_clock::now().time_since_epoch().count())};
+const uint64_t g_salt =
+    static_cast<uint64_t>(std::chrono::steady_clock::now().time_since_epoch().count()) * kTagOdd;
+
+// Advances a workspace's tag word (one thread); recorded ahead of every
+// search captured into a graph.
+__global__ void window_tag_kernel(uint64_t* word) {
+    const uint64_t t = __hip_atomic_load(word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(word, t + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 }  // namespace
 
@@ -1477,16 +1503,33 @@ coop_status_t coop_window_search(const uint64_t* size, const uint64_t* cost, con
     P.c2_magic = magic(pl.c2);
     P.nv_magic = magic(pl.num_virtual);
     P.pc = pl.pc;
-    const uint64_t call = g_calls.fetch_add(1, std::memory_order_relaxed);
-    P.epoch = call & kEpochMask;
-    P.qtag = call & 0xffffffffull;
     P.queue_on = pl.nchunks > pl.grid ? 1u : 0u;
     P.slices_log2 = pl.slices_log2;
     P.inv_slope = static_cast<double>(num_segments) /
                   (static_cast<double>(num_blocks) / kTile + static_cast<double>(num_segments));
 
+    // A captured launch replays with the arguments it was recorded with, so
+    // its tag cannot come from the host: it comes from the workspace's tag
+    // word, advanced by a kernel recorded just before.
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipStreamCaptureStatus capture = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &capture) != hipSuccess) return COOP_ERR_HIP;
+    if (capture == hipStreamCaptureStatusNone) {
+        const uint64_t call = g_calls.fetch_add(1, std::memory_order_relaxed);
+        P.epoch = call & kTagMask;
+        P.qtag = call & 0xffffffffull;
+        P.tag_word = nullptr;
+    } else {
+        uint64_t* word = P.queue + 1;
+        hipLaunchKernelGGL(window_tag_kernel, dim3(1), dim3(1), 0, s, word);
+        if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
+        P.epoch = g_salt;
+        P.qtag = 0;
+        P.tag_word = word;
+    }
+
     hipLaunchKernelGGL(coop_window_search_kernel, dim3(static_cast<uint32_t>(pl.grid)),
-                       dim3(kThreads), 0, static_cast<hipStream_t>(stream), P);
+                       dim3(kThreads), 0, s, P);
     if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
     return COOP_OK;
 }
