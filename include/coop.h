@@ -21,6 +21,16 @@
  * and the graph replayed any number of times: each replay recomputes the
  * outputs from whatever the input buffers hold at that point.  No entry point
  * records a memset node.
+ *
+ * Debug checks: with COOP_DEBUG=1 in the environment (read on every call),
+ * coop_window_search, coop_first_fit and coop_window_search_real first copy
+ * the batch's offset arrays (and, where the entry point sums, its blocks)
+ * back on the call's stream, synchronise the stream, and reject a batch that
+ * breaks a device-resident rule: COOP_ERR_INVALID for an offset rule,
+ * COOP_ERR_OVERFLOW for a run whose byte total, or the cost total of its
+ * evictable blocks, exceeds 2^64 - 1.  Nothing is launched then.  Calls made
+ * while the stream is capturing a graph skip the checks (a capture cannot
+ * synchronise).  The checks cost a copy of the arrays per call.
  */
 #ifndef COOP_H
 #define COOP_H
@@ -54,7 +64,8 @@ typedef enum {
     COOP_OK = 0,
     COOP_ERR_INVALID = -1,   /* null pointer with a nonzero count, bad sizes */
     COOP_ERR_WORKSPACE = -2, /* workspace missing or smaller than required */
-    COOP_ERR_HIP = -3        /* a HIP launch failed; the HIP error is cleared */
+    COOP_ERR_HIP = -3,       /* a HIP launch failed; the HIP error is cleared */
+    COOP_ERR_OVERFLOW = -4   /* debug checks only: a run's total exceeds 2^64 - 1 */
 } coop_status_t;
 
 /* Version of this ABI; bumped on any incompatible change. */
@@ -126,17 +137,19 @@ coop_status_t coop_window_search_plan(uint64_t num_blocks, uint64_t num_segments
  * stream: hipStream_t the work is enqueued on; out is valid once the
  *   stream has reached this point.
  *
- * Preconditions that live in device memory are not checked: the offset
- * rules above, and that within every run (a maximal stretch of unpinned
- * blocks) the byte total and the total cost of evictable blocks fit in
- * 64 bits.  When they fail the results are unspecified (but every memory
- * access stays inside the arrays described by the counts).
+ * Preconditions that live in device memory are not checked by the kernels
+ * (only by the debug checks above): the offset rules above, and that within
+ * every run (a maximal stretch of unpinned blocks) the byte total and the
+ * total cost of evictable blocks fit in 64 bits.  When they fail the results
+ * are unspecified (but every memory access stays inside the arrays described
+ * by the counts).
  *
  * Returns COOP_OK once the work is enqueued (and immediately, enqueuing
  * nothing, when num_requests == 0); COOP_ERR_INVALID for a NULL pointer
  * whose array is non-empty, requests without snapshots, or a batch too large
  * to launch; COOP_ERR_WORKSPACE for a missing or too small workspace;
- * COOP_ERR_HIP when the launch fails.
+ * COOP_ERR_HIP when the launch fails; under the debug checks also
+ * COOP_ERR_INVALID for a broken offset rule and COOP_ERR_OVERFLOW.
  */
 coop_status_t coop_window_search(const uint64_t *size, const uint64_t *cost,
                                  const uint8_t *kind, uint64_t num_blocks,
@@ -187,8 +200,9 @@ coop_status_t coop_first_fit(const uint64_t *size, const uint8_t *kind, uint64_t
  * status (device u32) is set to 0, then bit 0 if an evictable block's h is
  * NaN, infinite, negative (other than -0) or at least 2^64; results for
  * such a batch are unspecified.  The h of free and pinned blocks is
- * ignored.  Precondition (unchecked): within every run each snapshot's byte
- * total and h total stay below 2^64.
+ * ignored.  Precondition: within every run each snapshot's byte total and
+ * h total stay below 2^64 (the debug checks cover the offsets and the byte
+ * totals, not the h totals).
  *
  * workspace: coop_window_search_real_workspace_size() bytes (device,
  * caller-owned, contents need not be initialised): about 26 bytes per block

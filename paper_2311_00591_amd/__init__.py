@@ -26,7 +26,7 @@ INFEASIBLE = -1  # int64 view of the all-ones sentinel
 POLICY_WINDOW, POLICY_GREEDY = 0, 1  # coop_replay's eviction policies
 
 _STATUS = {0: "ok", -1: "invalid argument", -2: "workspace missing or too small",
-           -3: "HIP launch failed"}
+           -3: "HIP launch failed", -4: "a run's byte or cost total exceeds 2^64 - 1"}
 
 _lib = None
 

@@ -28,6 +28,7 @@
 #include <stdint.h>
 
 #include "coop.h"
+#include "coop_host.h"
 
 namespace {
 
@@ -229,6 +230,19 @@ coop_status_t coop_first_fit(const uint64_t* size, const uint8_t* kind, uint64_t
                              const uint64_t* req_sizes, const uint64_t* req_offsets,
                              uint64_t num_requests, uint64_t* out, void* workspace,
                              size_t workspace_bytes, void* stream) {
+    return coop_first_fit_enqueue(size, kind, num_blocks, seg_offsets, num_segments, req_sizes,
+                                  req_offsets, num_requests, out, workspace, workspace_bytes,
+                                  stream, coop_host::checks_requested());
+}
+
+}  // extern "C"
+
+coop_status_t coop_first_fit_enqueue(const uint64_t* size, const uint8_t* kind,
+                                     uint64_t num_blocks, const uint64_t* seg_offsets,
+                                     uint64_t num_segments, const uint64_t* req_sizes,
+                                     const uint64_t* req_offsets, uint64_t num_requests,
+                                     uint64_t* out, void* workspace, size_t workspace_bytes,
+                                     void* stream, bool check) {
     if (num_requests == 0) return COOP_OK;
     if (num_segments == 0 || num_blocks > (1ull << 60)) return COOP_ERR_INVALID;
     if (num_blocks && (!size || !kind)) return COOP_ERR_INVALID;
@@ -238,6 +252,13 @@ coop_status_t coop_first_fit(const uint64_t* size, const uint8_t* kind, uint64_t
     uint64_t* g1 = static_cast<uint64_t*>(workspace);
     uint64_t* g2 = reinterpret_cast<uint64_t*>(static_cast<char*>(workspace) + l.g2_offset);
     hipStream_t s = static_cast<hipStream_t>(stream);
+    if (check) {
+        // first fit sums nothing: only the offset rules
+        const coop_host::Batch b{size, nullptr, kind, num_blocks, seg_offsets, num_segments,
+                                 req_offsets, num_requests, false};
+        const coop_status_t rc = coop_host::check_batch(b, s);
+        if (rc != COOP_OK) return rc;
+    }
     if (l.tiles) {
         const uint64_t grid = l.tiles < kMaxSummaryWGs ? l.tiles : kMaxSummaryWGs;
         hipLaunchKernelGGL(first_fit_summary_kernel, dim3(static_cast<uint32_t>(grid)), dim3(kThreads),
@@ -252,5 +273,3 @@ coop_status_t coop_first_fit(const uint64_t* size, const uint8_t* kind, uint64_t
     if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
     return COOP_OK;
 }
-
-}  // extern "C"

@@ -36,6 +36,7 @@
 #include <stdint.h>
 
 #include "coop.h"
+#include "coop_host.h"
 
 namespace {
 
@@ -853,15 +854,17 @@ coop_status_t coop_replay(uint64_t* size, uint64_t* cost, uint8_t* kind, uint32_
                        req_off, req_ff, op, op_size, num_ops, status);
     if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
     for (uint64_t t = 0; t < num_ops; ++t) {
-        coop_status_t rc = coop_first_fit(size, kind, nb, seg, num_pools, req_ff, req_off, num_pools,
-                                          ff, w + l.ff_ws, l.ff_ws_bytes, stream);
+        coop_status_t rc = coop_first_fit_enqueue(size, kind, nb, seg, num_pools, req_ff, req_off,
+                                                  num_pools, ff, w + l.ff_ws, l.ff_ws_bytes,
+                                                  stream, false);
         if (rc != COOP_OK) return rc;
         if (policy == COOP_POLICY_WINDOW) {
             hipLaunchKernelGGL(replay_gate_kernel, dim3(small), dim3(256), 0, s, num_pools, req_ff,
                                ff, req_win);
             if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
-            rc = coop_window_search(size, cost, kind, nb, seg, num_pools, req_win, req_off,
-                                    num_pools, win, w + l.win_ws, l.win_ws_bytes, stream);
+            rc = coop_window_search_enqueue(size, cost, kind, nb, seg, num_pools, req_win,
+                                            req_off, num_pools, win, w + l.win_ws,
+                                            l.win_ws_bytes, stream, false);
             if (rc != COOP_OK) return rc;
         }
         hipLaunchKernelGGL(replay_update_kernel, dim3(static_cast<uint32_t>(num_pools)),

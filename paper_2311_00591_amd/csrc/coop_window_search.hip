@@ -71,6 +71,7 @@
 #include <stdint.h>
 
 #include "coop.h"
+#include "coop_host.h"
 
 namespace {
 
@@ -1435,6 +1436,7 @@ const char* coop_status_string(int status) {
         case COOP_ERR_INVALID: return "invalid argument";
         case COOP_ERR_WORKSPACE: return "workspace missing or too small";
         case COOP_ERR_HIP: return "HIP launch failed";
+        case COOP_ERR_OVERFLOW: return "a run's byte or cost total exceeds 2^64 - 1";
         default: return "unknown status";
     }
 }
@@ -1470,6 +1472,20 @@ coop_status_t coop_window_search(const uint64_t* size, const uint64_t* cost, con
                                  const uint64_t* req_offsets, uint64_t num_requests,
                                  coop_window_t* out, void* workspace, size_t workspace_bytes,
                                  void* stream) {
+    return coop_window_search_enqueue(size, cost, kind, num_blocks, seg_offsets, num_segments,
+                                      req_sizes, req_offsets, num_requests, out, workspace,
+                                      workspace_bytes, stream, coop_host::checks_requested());
+}
+
+}  // extern "C"
+
+coop_status_t coop_window_search_enqueue(const uint64_t* size, const uint64_t* cost,
+                                         const uint8_t* kind, uint64_t num_blocks,
+                                         const uint64_t* seg_offsets, uint64_t num_segments,
+                                         const uint64_t* req_sizes, const uint64_t* req_offsets,
+                                         uint64_t num_requests, coop_window_t* out,
+                                         void* workspace, size_t workspace_bytes, void* stream,
+                                         bool check) {
     if (num_requests == 0) return COOP_OK;
     if (num_segments == 0) return COOP_ERR_INVALID;
     if (num_blocks && (!size || !cost || !kind)) return COOP_ERR_INVALID;
@@ -1477,6 +1493,13 @@ coop_status_t coop_window_search(const uint64_t* size, const uint64_t* cost, con
     Plan pl;
     if (!make_plan(num_blocks, num_segments, num_requests, &pl)) return COOP_ERR_INVALID;
     if (!workspace || workspace_bytes < pl.bytes) return COOP_ERR_WORKSPACE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (check) {
+        const coop_host::Batch b{size, cost, kind, num_blocks, seg_offsets, num_segments,
+                                 req_offsets, num_requests, true};
+        const coop_status_t rc = coop_host::check_batch(b, s);
+        if (rc != COOP_OK) return rc;
+    }
 
     Params P;
     P.size = size;
@@ -1511,7 +1534,6 @@ coop_status_t coop_window_search(const uint64_t* size, const uint64_t* cost, con
     // A captured launch replays with the arguments it was recorded with, so
     // its tag cannot come from the host: it comes from the workspace's tag
     // word, advanced by a kernel recorded just before.
-    hipStream_t s = static_cast<hipStream_t>(stream);
     hipStreamCaptureStatus capture = hipStreamCaptureStatusNone;
     if (hipStreamIsCapturing(s, &capture) != hipSuccess) return COOP_ERR_HIP;
     if (capture == hipStreamCaptureStatusNone) {
@@ -1533,5 +1555,3 @@ coop_status_t coop_window_search(const uint64_t* size, const uint64_t* cost, con
     if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
     return COOP_OK;
 }
-
-}  // extern "C"

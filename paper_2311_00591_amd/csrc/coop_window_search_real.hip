@@ -40,6 +40,7 @@
 #include <stdint.h>
 
 #include "coop.h"
+#include "coop_host.h"
 
 namespace {
 
@@ -719,6 +720,13 @@ coop_status_t coop_window_search_real(const uint64_t* size, const double* h, con
     if (!real_layout(num_blocks, num_segments, num_requests, &l)) return COOP_ERR_INVALID;
     if (!workspace || workspace_bytes < l.bytes) return COOP_ERR_WORKSPACE;
     hipStream_t s = static_cast<hipStream_t>(stream);
+    if (coop_host::checks_requested()) {
+        // offsets and run byte totals; the exact h totals are not checked
+        const coop_host::Batch b{size, nullptr, kind, num_blocks, seg_offsets, num_segments,
+                                 req_offsets, num_requests, true};
+        const coop_status_t rc = coop_host::check_batch(b, s);
+        if (rc != COOP_OK) return rc;
+    }
     char* w = static_cast<char*>(workspace);
     uint64_t* pl = reinterpret_cast<uint64_t*>(w + l.pl);
     uint64_t* cl_lo = reinterpret_cast<uint64_t*>(w + l.cl_lo);

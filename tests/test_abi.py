@@ -34,8 +34,23 @@ def test_abi_version_matches_header():
 
 def test_status_strings():
     lib = coop.load_library()
-    for s in (0, -1, -2, -3, 7):
+    for s in (0, -1, -2, -3, -4, 7):
         assert lib.coop_status_string(s)
+    # the binding's table agrees with the library for every named status
+    for s, text in coop._STATUS.items():
+        assert lib.coop_status_string(s).decode() == text
+    assert b"unknown" in lib.coop_status_string(7)
+
+
+def test_only_the_declared_functions_are_exported():
+    """The unchecked enqueue functions and the debug-check helpers are
+    internal: the dynamic symbol table holds the header's functions only."""
+    import subprocess
+    nm = subprocess.run(["nm", "-D", "--defined-only", coop.LIBRARY], capture_output=True,
+                        text=True, check=True).stdout
+    exported = {line.split()[-1] for line in nm.splitlines() if " T " in line or " W " in line}
+    ours = {n for n in exported if "coop" in n}
+    assert ours == set(_declared_functions()), sorted(ours ^ set(_declared_functions()))
 
 
 def test_workspace_size_depends_on_counts_only():
