@@ -79,6 +79,29 @@ def fit_bytes(pools):
     return 9 * pools.num_blocks + 16 * pools.num_requests
 
 
+def copy_ceiling(dev, nbytes=1 << 30, reps=10):
+    """Measured HBM ceiling: GB/s (bytes read + bytes written) of a plain
+    device-to-device copy of `nbytes`, timed with events over `reps` copies
+    after one warm-up; the buffers are 4x the Infinity Cache, so every copy
+    streams from HBM."""
+    import torch
+    a = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    b = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    a.fill_(1)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(reps):
+        b.copy_(a)
+    stop.record()
+    torch.cuda.synchronize()
+    gbs = 2 * nbytes * reps / (start.elapsed_time(stop) / 1e3) / 1e9
+    del a, b
+    torch.cuda.empty_cache()
+    return gbs
+
+
 def source_digest(source=None):
     """First 16 hex digits of the sha256 of a kernel's source file."""
     with open(source or KERNEL_SOURCE, "rb") as f:
@@ -215,6 +238,7 @@ def main():
 
     achieved = alg_bytes / t / 1e9
     traffic = measured_traffic(spec.name)
+    ceiling = copy_ceiling(dev)
     cpu = cpu_baseline(pools, args.cpu_seconds) if args.cpu_seconds > 0 else None
     nb = np.diff(pools.seg_offsets.astype(np.int64))
     rec = {
@@ -254,6 +278,8 @@ def main():
             "frac": achieved / PEAK_HBM_GBS,
             "traffic": traffic,
             "algorithmic_bytes_per_launch": alg_bytes,
+            "copy_ceiling": ceiling,
+            "frac_of_copy_ceiling": achieved / ceiling,
         },
         "cpu_baseline": cpu,
         "parity_vs_oracle": parity,

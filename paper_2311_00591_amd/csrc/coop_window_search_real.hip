@@ -68,6 +68,7 @@ constexpr uint32_t kPadSteps = 32;
 static_assert(kPadSteps >= (kChunk + kStage + kThreads - 1) / kThreads, "padding covers a slice");
 constexpr uint32_t kMaxGroup = 16;              // requests per search workgroup
 constexpr uint32_t kTargetGroups = 4096;        // search workgroups aimed for
+constexpr uint64_t kResidentUnits = 512;        // search workgroups the chip holds at once
 constexpr uint32_t kMaxParts = 1024;
 constexpr uint32_t kOffsetThreads = 1024;
 constexpr uint64_t kNone = ~0ull;
@@ -668,13 +669,23 @@ bool real_layout(uint64_t num_blocks, uint64_t num_segments, uint64_t num_reques
     l->tiles = (num_blocks >> kTileLog2) + 1;
     uint64_t rps = num_requests / num_segments;
     l->group = rps < 1 ? 1 : (rps > kMaxGroup ? kMaxGroup : rps);
-    const uint64_t groups = (num_requests + l->group - 1) / l->group;
+    uint64_t groups = (num_requests + l->group - 1) / l->group;
     const uint64_t avg = num_blocks / num_segments;
     uint64_t parts = groups ? (kTargetGroups + groups - 1) / groups : 1;
     const uint64_t cap = avg / kChunk > 1 ? avg / kChunk : 1;
     if (parts > cap) parts = cap;
     if (parts > kMaxParts) parts = kMaxParts;
     if (parts < 1) parts = 1;
+    // Few small snapshots with many requests (parts stuck at 1): smaller
+    // request groups, so that the batch still fills the chip; each
+    // workgroup then stages its chunk for fewer requests.
+    if (groups * parts < kResidentUnits && l->group > 1) {
+        const uint64_t want = (num_requests * parts + kResidentUnits - 1) / kResidentUnits;
+        if (want < l->group) {
+            l->group = want < 1 ? 1 : want;
+            groups = (num_requests + l->group - 1) / l->group;
+        }
+    }
     l->parts = parts;
     l->units = groups * parts;
     const uint64_t np = num_blocks + 1;
