@@ -258,19 +258,22 @@ struct Params {
     uint64_t num_blocks;
     uint64_t num_segments;
     uint64_t num_requests;
-    uint64_t num_virtual;  // tile ids per slice: floor(num_blocks / kTile) + num_segments
-    uint64_t units;        // work units: slices * num_virtual (below 2^32)
-    uint64_t grid;         // workgroups; chunk w < grid is workgroup w's first
-    uint64_t c1, c2;       // units per chunk: first chunks [0, u1), queued chunks after
+    // Counts of units and chunks are below 2^32 (units < 2^32 by the plan)
+    // and held in 32 bits, which keeps the kernel's uniform state within the
+    // scalar registers; products of them are formed in 64 bits.
+    uint32_t num_virtual;  // tile ids per slice: floor(num_blocks / kTile) + num_segments
+    uint32_t units;        // work units: slices * num_virtual (below 2^32)
+    uint32_t grid;         // workgroups; chunk w < grid is workgroup w's first
+    uint32_t c1, c2;       // units per chunk: first chunks [0, u1), queued chunks after
                            // (c2 is a lower bound from the host, set by the kernel)
-    uint64_t u1;           // units in the first chunks
+    uint32_t u1;           // units in the first chunks
     uint64_t nchunks;      // chunks in all (set by the kernel when there is a queue)
     uint64_t c1_magic;     // ceil(2^64 / c1), for division by c1
     uint64_t c2_magic;     // ceil(2^64 / c2) (set by the kernel)
     uint64_t nv_magic;     // ceil(2^64 / num_virtual)
-    uint64_t qtag;         // this call's queue tag (32 bits)
+    uint32_t qtag;         // this call's queue tag
     uint32_t queue_on;     // units past u1 go through the queue
-    uint64_t pc;           // partial slots per request
+    uint32_t pc;           // partial slots per request (at most 2^23)
     uint64_t epoch;        // this call's tag on the arrival tickets
     const uint64_t* tag_word;  // captured calls: the workspace word the tags come from
     uint32_t slices_log2;  // request slices (a power of two): slice y takes y, y + slices, ...
@@ -302,7 +305,7 @@ __device__ __forceinline__ void chunk_range(const Params& P, uint64_t c, uint64_
         b = c * P.c1;
         e = b + P.c1 < P.u1 ? b + P.c1 : P.u1;
     } else {
-        b = P.u1 + (c - P.grid) * P.c2;
+        b = P.u1 + (c - P.grid) * static_cast<uint64_t>(P.c2);
         e = b + P.c2 < P.units ? b + P.c2 : P.units;
     }
     if (b > e) b = e;
@@ -327,7 +330,7 @@ __device__ __forceinline__ uint64_t first_id(uint64_t b, uint64_t seg_b) {
 // after it.  The third pair is loaded ahead, so that stepping to the next
 // snapshot needs no wait.
 struct Cursor {
-    uint64_t y, b;
+    uint32_t y, b;  // b < num_segments <= 2^32
     uint64_t sb, sb1, sb2;  // seg[b], seg[b + 1], seg[min(b + 2, B)]
     uint64_t rb, rb1, rb2;  // req_off likewise
 };
@@ -368,13 +371,13 @@ __device__ void cursor_locate(const Params& P, uint64_t v, Cursor& c) {
 // the cursor's first id).
 __device__ __forceinline__ void cursor_advance(const Params& P, uint64_t v, Cursor& c) {
     const uint64_t B = P.num_segments;
-    while (c.b + 1 < B && v >= first_id(c.b + 1, c.sb1)) {
+    while (c.b + 1ull < B && v >= first_id(c.b + 1ull, c.sb1)) {
         ++c.b;
         c.sb = c.sb1;
         c.sb1 = c.sb2;
         c.rb = c.rb1;
         c.rb1 = c.rb2;
-        const uint64_t b2 = c.b + 2 < B ? c.b + 2 : B;
+        const uint64_t b2 = c.b + 2ull < B ? c.b + 2ull : B;
         c.sb2 = ld_const(P.seg, b2);
         c.rb2 = ld_const(P.req_off, b2);
     }
@@ -387,15 +390,17 @@ __device__ __forceinline__ void cursor_advance(const Params& P, uint64_t v, Curs
 // lengths: malformed offsets give wrong answers, never an out-of-bounds
 // access.
 struct Job {
-    uint64_t u, y, b, s0, s1, q0, R, K, tiles, p, g, G;
+    uint32_t u, y, b;  // unit, slice, snapshot (b < num_segments <= 2^32)
+    uint64_t s0, s1, q0, R, K, tiles, p;
+    uint32_t g, G;     // at most pc
     bool first, last, direct;
 };
 
 // The first unit in [u, u_end) holding a tile to search (a tile of a
 // snapshot with requests in the unit's slice); false if there is none.
 // (y, v) is unit u as (slice, tile id) and moves along with it.
-__device__ bool next_job(const Params& P, Cursor& c, bool& have_cursor, uint64_t u, uint64_t& y,
-                         uint64_t& v, uint64_t u_begin, uint64_t u_end, uint64_t chunk, Job& job) {
+__device__ bool next_job(const Params& P, Cursor& c, bool& have_cursor, uint64_t u, uint32_t& y,
+                         uint32_t& v, uint64_t u_begin, uint64_t u_end, uint64_t chunk, Job& job) {
     for (; u < u_end; ++u, ++v) {
         if (v == P.num_virtual) {
             v = 0;
@@ -418,7 +423,7 @@ __device__ bool next_job(const Params& P, Cursor& c, bool& have_cursor, uint64_t
         const uint64_t f = first_id(c.b, c.sb);
         const uint64_t p = v - f;  // wraps (and is skipped) if the offsets are malformed
         if (p >= tiles || y >= R) continue;  // (the loop moves v with u)
-        const uint64_t ub = y * P.num_virtual + f;  // unit of tile 0 of (b, y)
+        const uint64_t ub = static_cast<uint64_t>(y) * P.num_virtual + f;  // unit of tile 0 of (b, y)
         const uint64_t lo = ub > u_begin ? ub : u_begin;
         const uint64_t hi = ub + tiles < u_end ? ub + tiles : u_end;
         job.u = u;
@@ -433,10 +438,10 @@ __device__ bool next_job(const Params& P, Cursor& c, bool& have_cursor, uint64_t
         job.p = p;
         const uint64_t ue = ub + tiles - 1 < P.units ? ub + tiles - 1 : P.units - 1;
         const uint64_t i_lo = chunk_of(P, ub), i_hi = chunk_of(P, ue);
-        job.G = i_hi - i_lo + 1;
-        if (job.G > P.pc) job.G = P.pc;  // only with malformed offsets
-        job.g = chunk - i_lo;
-        if (job.g >= job.G) job.g = job.G - 1;  // only with malformed offsets
+        const uint64_t G = i_hi - i_lo + 1;
+        job.G = static_cast<uint32_t>(G > P.pc ? P.pc : G);  // P.pc only with malformed offsets
+        const uint64_t g = chunk - i_lo;
+        job.g = g >= job.G ? job.G - 1 : static_cast<uint32_t>(g);  // likewise
         job.first = u == lo;
         job.last = u + 1 == hi;
         job.direct = job.G == 1;
@@ -1099,7 +1104,7 @@ __device__ void combine_partials(const Params& P, const Job& job, uint32_t tid, 
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
     __syncthreads();
     if (tid == 0) {
-        uint64_t* ctr = P.counters + job.y * P.num_segments + job.b;
+        uint64_t* ctr = P.counters + static_cast<uint64_t>(job.y) * P.num_segments + job.b;
         uint64_t old = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         uint64_t want;
         do {
@@ -1186,13 +1191,17 @@ __device__ uint64_t claim_chunk(const Params& P, Smem& sm, uint32_t tid) {
 // Position of the walk over the units: the current chunk and its units, and
 // unit u as (slice y, tile id v).
 struct Walk {
-    uint64_t chunk, u_begin, u_end, y, v;
+    uint64_t chunk;
+    uint32_t u_begin, u_end, y, v;  // units, slice and tile id: below 2^32
 };
 
 __device__ __forceinline__ void walk_chunk(const Params& P, uint64_t c, Walk& wk) {
     wk.chunk = c;
-    chunk_range(P, c, wk.u_begin, wk.u_end);
-    wk.y = div_magic(wk.u_begin, P.nv_magic);
+    uint64_t b, e;
+    chunk_range(P, c, b, e);
+    wk.u_begin = static_cast<uint32_t>(b);
+    wk.u_end = static_cast<uint32_t>(e);
+    wk.y = static_cast<uint32_t>(div_magic(wk.u_begin, P.nv_magic));
     wk.v = wk.u_begin - wk.y * P.num_virtual;
 }
 
@@ -1230,7 +1239,7 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
         // same value; P.epoch holds a per-process salt.
         const uint64_t t = __hip_atomic_load(P.tag_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         P.epoch = kGraphTag | ((t * kTagOdd + P.epoch) & kTagMask);
-        P.qtag = P.epoch & 0xffffffffull;
+        P.qtag = static_cast<uint32_t>(P.epoch);
     }
     // The queue, when there is one: workgroup 0 stamps this call's tag; claims
     // that reach the word before the stamp see an old tag and try again.
@@ -1239,12 +1248,13 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
     uint64_t reserve = kQDone;
     if (P.queue_on) {
         if (blockIdx.x == 0 && tid == 0)
-            __hip_atomic_store(P.queue, P.qtag << 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(P.queue, static_cast<uint64_t>(P.qtag) << 32, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
         const uint64_t tmax = max_tiles(P, sm, tid);
         const uint64_t need = (tmax + P.pc - 3) / (P.pc - 2);
-        P.c2 = need > P.c2 ? need : P.c2;
+        P.c2 = static_cast<uint32_t>(need > P.c2 ? need : P.c2);
         P.c2_magic = P.c2 == 1 ? 0 : ~0ull / P.c2 + 1;
-        P.nchunks = P.grid + (P.units - P.u1 + P.c2 - 1) / P.c2;
+        P.nchunks = P.grid + (static_cast<uint64_t>(P.units) - P.u1 + P.c2 - 1) / P.c2;
         reserve = kQEmpty;
     }
     Walk wk;
@@ -1515,17 +1525,17 @@ coop_status_t coop_window_search_enqueue(const uint64_t* size, const uint64_t* c
     P.num_blocks = num_blocks;
     P.num_segments = num_segments;
     P.num_requests = num_requests;
-    P.num_virtual = pl.num_virtual;
-    P.units = pl.units;
-    P.grid = pl.grid;
-    P.c1 = pl.c1;
-    P.c2 = pl.c2;
-    P.u1 = pl.u1;
+    P.num_virtual = static_cast<uint32_t>(pl.num_virtual);
+    P.units = static_cast<uint32_t>(pl.units);
+    P.grid = static_cast<uint32_t>(pl.grid);
+    P.c1 = static_cast<uint32_t>(pl.c1);
+    P.c2 = static_cast<uint32_t>(pl.c2);
+    P.u1 = static_cast<uint32_t>(pl.u1);
     P.nchunks = pl.nchunks;
     P.c1_magic = magic(pl.c1);
     P.c2_magic = magic(pl.c2);
     P.nv_magic = magic(pl.num_virtual);
-    P.pc = pl.pc;
+    P.pc = static_cast<uint32_t>(pl.pc);
     P.queue_on = pl.nchunks > pl.grid ? 1u : 0u;
     P.slices_log2 = pl.slices_log2;
     P.inv_slope = static_cast<double>(num_segments) /
@@ -1539,7 +1549,7 @@ coop_status_t coop_window_search_enqueue(const uint64_t* size, const uint64_t* c
     if (capture == hipStreamCaptureStatusNone) {
         const uint64_t call = g_calls.fetch_add(1, std::memory_order_relaxed);
         P.epoch = call & kTagMask;
-        P.qtag = call & 0xffffffffull;
+        P.qtag = static_cast<uint32_t>(call);
         P.tag_word = nullptr;
     } else {
         uint64_t* word = P.queue + 1;
