@@ -816,9 +816,9 @@ __device__ __forceinline__ TileState stage_tile(Smem& sm, const TileGeom& tg, ui
     Sums t{0, 0, 0};
     uint32_t hi_or = 0;
     uint32_t kinds[kItems];
-#pragma unroll
-    for (uint32_t j = 0; j < kItems; ++j) {
-        const bool in = (nt == kTile || i0 + j < nt) && i0 + j >= lead;
+    // one block: its kind k_j (masked blocks as described above) and size
+    // s_j; r.sz / r.ct then hold the sums before it
+    auto item = [&](uint32_t j, bool in) {
         const uint64_t s_j = in ? r.sz[j] : 0;
         const uint32_t raw = (r.kd[j >> 2] >> (8 * (j & 3))) & 0xffu;
         const uint32_t k_j = in ? raw
@@ -833,6 +833,15 @@ __device__ __forceinline__ TileState stage_tile(Smem& sm, const TileGeom& tg, ui
         t.c += c_j;
         t.r += p_j;
         hi_or |= static_cast<uint32_t>(s_j >> 32);
+    };
+    if (nt == kTile && lead == 0) {
+        // a whole tile from the snapshot's blocks (uniform): nothing masked
+#pragma unroll
+        for (uint32_t j = 0; j < kItems; ++j) item(j, true);
+    } else {
+#pragma unroll
+        for (uint32_t j = 0; j < kItems; ++j)
+            item(j, (nt == kTile || i0 + j < nt) && i0 + j >= lead);
     }
     Sums wi = t;
     wave_inclusive_sum(wi);
