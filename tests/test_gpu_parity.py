@@ -186,6 +186,28 @@ def test_many_requests_cap_workgroups_per_snapshot():
     assert_parity(pools, gpu_search(pools), "strided tiles")
 
 
+def test_millions_of_tiny_snapshots():
+    """2^22 snapshots of 0..3 blocks (a quarter empty), one request each:
+    snapshot indices and tile ids in the millions, most tile ids naming an
+    empty remainder, and the cursor stepping over many snapshots per tile."""
+    _announce("2^22 tiny snapshots")
+    rng = np.random.default_rng(21)
+    B = 1 << 22
+    nb = rng.integers(0, 4, size=B)
+    seg = np.zeros(B + 1, np.uint64)
+    seg[1:] = np.cumsum(nb)
+    n = int(seg[-1])
+    size = (rng.integers(1, 1 << 12, size=n) * 512).astype(np.uint64)
+    kind = rng.choice(np.array([0, 1, 1, 1, 2], np.uint8), size=n)
+    cost = rng.integers(0, 1 << 40, size=n).astype(np.uint64)
+    req = rng.integers(0, 1 << 22, size=B).astype(np.uint64)
+    roff = np.arange(B + 1, dtype=np.uint64)
+    pools = workloads.Pools(size, cost, kind, seg, req, roff)
+    got = gpu_search(pools)
+    assert_parity(pools, got, "2^22 tiny snapshots")
+    check_results(pools, got, sample=range(0, B, 4099))
+
+
 def test_workspace_contents_do_not_matter_and_calls_repeat():
     _announce("workspace garbage / repeat")
     pools = workloads.make_config(2, 3, num_segments=6, blocks=(30000, 30000),
