@@ -1089,17 +1089,26 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
             if (!job.first) k = min_key(load_key_device(P.part + q * P.pc + job.g), k);
             if (lane == 0) store_answer(P, job, q, k, S);
         }
-    } else {
-        __syncthreads();
-        if (tid < job.K) {
-            Key k = sm.slot[tid << wl2];
-            for (uint32_t u = 1; u < wpr; ++u) k = min_key(k, sm.slot[(tid << wl2) + u]);
-            acc = job.first ? k : min_key(acc, k);
-            if (job.last)
-                store_answer(P, job, job.q0 + job.y + (static_cast<uint64_t>(tid) << P.slices_log2),
-                             acc, sm.slot_s[tid << wl2]);
-        }
     }
+    // (shared requests: the wavefronts' keys stay in sm.slot for
+    // reduce_shared, after the barrier that ends the tile)
+}
+
+// Shared requests (wpr > 1): thread j reduces the wpr keys of request j that
+// the wavefronts left in sm.slot, into its running key, and writes the
+// result after the snapshot's last tile.  Called after the barrier that
+// ends the tile, so every key is in place; the next tile's keys are written
+// only after the next staging barriers, which wavefront 0 reaches after this.
+__device__ __forceinline__ void reduce_shared(const Params& P, const Smem& sm, const Job& job,
+                                              uint32_t wpr, uint32_t tid, Key& acc) {
+    if (tid >= job.K) return;
+    const uint32_t wl2 = static_cast<uint32_t>(__builtin_ctz(wpr));
+    Key k = sm.slot[tid << wl2];
+    for (uint32_t u = 1; u < wpr; ++u) k = min_key(k, sm.slot[(tid << wl2) + u]);
+    acc = job.first ? k : min_key(acc, k);
+    if (job.last)
+        store_answer(P, job, job.q0 + job.y + (static_cast<uint64_t>(tid) << P.slices_log2), acc,
+                     sm.slot_s[tid << wl2]);
 }
 
 // After the last tile of (b, y) in the current chunk, when other chunks
@@ -1321,6 +1330,7 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
         // ---- 2./3. the requests
         tile_requests(P, sm, job, tg, ts, wpr, t, acc, s_lane);
         __syncthreads();  // LDS is restaged next
+        if (wpr > 1) reduce_shared(P, sm, job, wpr, t, acc);
         if (job.last && !job.direct) combine_partials(P, job, t, last_flag);
         if (!has_next) break;
         job = next;
