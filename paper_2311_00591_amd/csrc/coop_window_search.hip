@@ -43,7 +43,8 @@
 //     equal slices of merge steps (merge path, one bisection per lane), and
 //     every step that takes a start meets that start's shortest window and
 //     scores it at once.  A lexicographic argmin over the lanes (DPP) gives
-//     the wavefront's answer; wavefronts sharing a request combine in LDS.
+//     the wavefront's answer; wavefronts sharing a request combine in LDS
+//     after the barrier that ends the tile.
 //  3. Starts whose windows end past the staged region (the region's last run
 //     goes on) are a suffix of the tile, found by one search; the request's
 //     wavefront finishes them by walking the rest of the run 64 blocks at a
@@ -58,7 +59,9 @@
 // chunk writes one partial key per request into the workspace and takes a
 // ticket on a per-snapshot counter; the chunk holding the last ticket reduces
 // the partials and writes the results.  Counters and the queue carry a
-// per-call tag, so the workspace never needs clearing.
+// per-call tag, so the workspace never needs clearing: eager calls take it
+// from a host counter; calls captured into a graph derive it from a tag word
+// in the workspace, advanced by a one-thread kernel ahead of each replay.
 //
 // All arithmetic is unsigned 64-bit integer.  Prefix sums wrap modulo 2^64;
 // differences over a window are exact whenever each run's byte and cost
