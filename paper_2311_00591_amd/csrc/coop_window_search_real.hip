@@ -66,6 +66,7 @@ constexpr uint64_t kEndKey = ~0ull;  // above every target: stops every merge
 // again) or past the end keys, into this many more sentinel keys.
 constexpr uint32_t kPadSteps = 32;
 static_assert(kPadSteps >= (kChunk + kStage + kThreads - 1) / kThreads, "padding covers a slice");
+constexpr uint32_t kStageBatch = 4;             // staged indices per thread whose loads go together
 constexpr uint32_t kMaxGroup = 16;              // requests per search workgroup
 constexpr uint32_t kTargetGroups = 4096;        // search workgroups aimed for
 constexpr uint64_t kResidentUnits = 512;        // search workgroups the chip holds at once
@@ -533,20 +534,40 @@ __global__ __launch_bounds__(kThreads) void real_search_kernel(Prefix pf, Search
                 const U128 cbase = pf.C(c0);
                 if (tid == 0) big_flag = 0;
                 __syncthreads();  // the previous chunk's readers are done; flag cleared
+                // kStageBatch indices per thread at a time, their loads issued
+                // together (indices clamped to hi, so every load is in bounds;
+                // only indices up to hi are staged).  A block of 2^51 bytes or
+                // more could wrap the staged byte count: P(x + 1) - P(x) is
+                // checked in the same pass.
                 bool big = false;
-                for (uint64_t x = c0 + tid; x <= hi; x += kThreads) {
-                    const uint64_t pr = pf.P(x) - pbase;
-                    big |= pr >= kPackOne;
-                    Y[x - c0] = ((pf.R(x) - rbase) << kPackBits) + pr;
-                    Cr[x - c0] = sub128(pf.C(x), cbase);
+                for (uint64_t xb = c0 + tid; xb <= hi; xb += kStageBatch * kThreads) {
+                    uint64_t pv[kStageBatch], pn[kStageBatch], rv[kStageBatch];
+                    U128 cv[kStageBatch];
+#pragma unroll
+                    for (uint32_t j = 0; j < kStageBatch; ++j) {
+                        const uint64_t xj = xb + j * kThreads;
+                        const uint64_t x = xj < hi ? xj : hi;
+                        const uint64_t xn = x < hi ? x + 1 : x;
+                        pv[j] = pf.P(x);
+                        pn[j] = pf.P(xn);
+                        rv[j] = pf.R(x);
+                        cv[j] = pf.C(x);
+                    }
+#pragma unroll
+                    for (uint32_t j = 0; j < kStageBatch; ++j) {
+                        const uint64_t x = xb + j * kThreads;
+                        if (x <= hi) {
+                            const uint64_t pr = pv[j] - pbase;
+                            big |= (pr >= kPackOne) | (pn[j] - pv[j] >= kPackOne);
+                            Y[x - c0] = ((rv[j] - rbase) << kPackBits) + pr;
+                            Cr[x - c0] = sub128(cv[j], cbase);
+                        }
+                    }
                 }
                 if (tid <= kPadSteps) {
                     Y[nB + 1 + tid] = kEndKey;
                     Cr[nB + 1 + tid] = U128{0, 0};
                 }
-                // a block of 2^51 bytes or more could wrap the staged byte count
-                for (uint64_t x = c0 + tid; x < hi; x += kThreads)
-                    big |= pf.P(x + 1) - pf.P(x) >= kPackOne;
                 if (big) big_flag = 1;
                 __syncthreads();
                 const bool packed_chunk = big_flag == 0;
