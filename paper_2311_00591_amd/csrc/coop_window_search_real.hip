@@ -66,7 +66,7 @@ constexpr uint64_t kEndKey = ~0ull;  // above every target: stops every merge
 // again) or past the end keys, into this many more sentinel keys.
 constexpr uint32_t kPadSteps = 32;
 static_assert(kPadSteps >= (kChunk + kStage + kThreads - 1) / kThreads, "padding covers a slice");
-constexpr uint32_t kStageBatch = 4;             // staged indices per thread whose loads go together
+constexpr uint32_t kStageBatch = 11;            // staged indices per thread whose loads go together
 constexpr uint32_t kMaxGroup = 16;              // requests per search workgroup
 constexpr uint32_t kTargetGroups = 4096;        // search workgroups aimed for
 constexpr uint64_t kResidentUnits = 512;        // search workgroups the chip holds at once
