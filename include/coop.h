@@ -206,7 +206,7 @@ coop_status_t coop_first_fit(const uint64_t *size, const uint8_t *kind, uint64_t
  *
  * workspace: coop_window_search_real_workspace_size() bytes (device,
  * caller-owned, contents need not be initialised): about 26 bytes per block
- * (tile-local prefix sums) plus partial results.  Five launches are
+ * (tile-local prefix sums) plus partial results.  Four launches are
  * enqueued on `stream`; nothing is allocated or synchronised.  Status codes
  * as for coop_window_search.
  */

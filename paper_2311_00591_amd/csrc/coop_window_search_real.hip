@@ -9,15 +9,17 @@
 // splits the work.  Ranking as in the integer search: least cost, then
 // fewest bytes, then lowest start.
 //
-// Five launches (the first clears the status word):
+// Four launches:
 //   1. real_tile_kernel: tiles of 2048 blocks, each writes the tile-local
 //      exclusive prefix sums of bytes (u64), fixed-point cost (u128) and
-//      pinned count (u16) of every block, and the tile's totals; a block
-//      with an invalid h sets a status bit.  Prefix index num_blocks (the
-//      end of the batch) belongs to the last tile, so there are
+//      pinned count (u16) of every block, and the tile's totals; a tile
+//      holding a block with an invalid h flags its total (bit 63 of the
+//      pinned count, which never exceeds 2048).  Prefix index num_blocks
+//      (the end of the batch) belongs to the last tile, so there are
 //      floor(num_blocks / 2048) + 1 tiles.
 //   2. real_offsets_kernel: one workgroup turns the tile totals into
-//      exclusive tile offsets.  The global prefix at index x is then
+//      exclusive tile offsets and writes the status word (bit 0 when any
+//      tile was flagged).  The global prefix at index x is then
 //      offset[x >> 11] + local[x].  Prefixes run over the whole batch
 //      (snapshots are not reset): window sums are differences of two
 //      prefixes of one snapshot, so they come out the same.
@@ -183,9 +185,7 @@ __device__ __forceinline__ Tri wave_scan(Tri v) {
     return v;
 }
 
-// Clears the status word (a kernel rather than a memset, so that the call
-// can be captured in a graph).
-__global__ void real_status_kernel(uint32_t* status) { *status = 0; }
+constexpr uint64_t kBadTile = 1ull << 63;  // in a tile total's pinned count
 
 // Stage 1.  Tile t covers prefix indices [t * 2048, min((t + 1) * 2048, n + 1)).
 // Each thread holds 8 consecutive blocks: 16-byte loads of sizes and h and
@@ -196,8 +196,9 @@ __global__ __launch_bounds__(kThreads) void real_tile_kernel(
     const uint64_t* __restrict__ size, const double* __restrict__ h,
     const uint8_t* __restrict__ kind, uint64_t n, uint64_t num_tiles, uint64_t* __restrict__ pl,
     uint64_t* __restrict__ cl_lo, uint64_t* __restrict__ cl_hi, uint16_t* __restrict__ rl,
-    Tri* __restrict__ tot, uint32_t* __restrict__ status) {
+    Tri* __restrict__ tot) {
     __shared__ Tri wtot[kWaves];
+    __shared__ uint32_t wbad[kWaves];
     const uint32_t tid = threadIdx.x, lane = tid & 63u, w = tid >> 6;
     const bool aligned = ((reinterpret_cast<uintptr_t>(size) | reinterpret_cast<uintptr_t>(h)) &
                           15u) == 0 && (reinterpret_cast<uintptr_t>(kind) & 7u) == 0;
@@ -242,7 +243,7 @@ __global__ __launch_bounds__(kThreads) void real_tile_kernel(
             if (kd[u] >= COOP_PINNED) pin |= 1u << u;
             if (kd[u] == COOP_EVICTABLE && !to_fixed(hv[u], cq[u])) bad = true;
         }
-        if (__ballot(bad) != 0 && lane == 0) atomicOr(status, kErrValue);
+        const bool wave_bad = __ballot(bad) != 0;
         Tri mine{0, U128{0, 0}, 0};
 #pragma unroll
         for (uint32_t u = 0; u < kItems; ++u) {
@@ -251,12 +252,18 @@ __global__ __launch_bounds__(kThreads) void real_tile_kernel(
         }
         mine.r = __popc(pin);
         const Tri inc = wave_scan(mine);
-        if (lane == 63) wtot[w] = inc;
+        if (lane == 63) {
+            wtot[w] = inc;
+            wbad[w] = wave_bad ? 1u : 0u;
+        }
         __syncthreads();
         Tri run{0, U128{0, 0}, 0};
         for (uint32_t v = 0; v < w; ++v) run = add_tri(run, wtot[v]);
         Tri all = run;
+        uint32_t tile_bad = 0;
         for (uint32_t v = w; v < kWaves; ++v) all = add_tri(all, wtot[v]);
+        for (uint32_t v = 0; v < kWaves; ++v) tile_bad |= wbad[v];
+        if (tile_bad) all.r |= kBadTile;
         __syncthreads();
         run = add_tri(run, Tri{inc.p - mine.p, sub128(inc.c, mine.c), inc.r - mine.r});
         uint64_t op[kItems], oc_lo[kItems], oc_hi[kItems];
@@ -307,14 +314,24 @@ __global__ __launch_bounds__(kThreads) void real_tile_kernel(
 // tiles' offsets.
 __global__ __launch_bounds__(kOffsetThreads) void real_offsets_kernel(const Tri* __restrict__ tot,
                                                                       uint64_t num_tiles,
-                                                                      Tri* __restrict__ off) {
+                                                                      Tri* __restrict__ off,
+                                                                      uint32_t* __restrict__ status) {
     __shared__ Tri wtot[kOffsetThreads / 64];
     const uint32_t tid = threadIdx.x, lane = tid & 63u, w = tid >> 6;
     const uint64_t per = (num_tiles + kOffsetThreads - 1) / kOffsetThreads;
     const uint64_t t0 = tid * per < num_tiles ? tid * per : num_tiles;
     const uint64_t t1 = t0 + per < num_tiles ? t0 + per : num_tiles;
     Tri mine{0, U128{0, 0}, 0};
-    for (uint64_t t = t0; t < t1; ++t) mine = add_tri(mine, tot[t]);
+    uint64_t flags = 0;
+    for (uint64_t t = t0; t < t1; ++t) {
+        Tri x = tot[t];
+        flags |= x.r;
+        x.r &= ~kBadTile;
+        mine = add_tri(mine, x);
+    }
+    // the status word: bit 0 when any tile held an invalid h
+    const int any_bad = __syncthreads_or((flags & kBadTile) != 0);
+    if (tid == 0) *status = any_bad ? kErrValue : 0u;
     const Tri inc = wave_scan(mine);
     if (lane == 63) wtot[w] = inc;
     __syncthreads();
@@ -322,7 +339,8 @@ __global__ __launch_bounds__(kOffsetThreads) void real_offsets_kernel(const Tri*
     for (uint32_t v = 0; v < w; ++v) run = add_tri(run, wtot[v]);
     run = add_tri(run, Tri{inc.p - mine.p, sub128(inc.c, mine.c), inc.r - mine.r});
     for (uint64_t t = t0; t < t1; ++t) {
-        const Tri x = tot[t];
+        Tri x = tot[t];
+        x.r &= ~kBadTile;
         off[t] = run;
         run = add_tri(run, x);
     }
@@ -767,13 +785,12 @@ coop_status_t coop_window_search_real(const uint64_t* size, const double* h, con
     Tri* tot = reinterpret_cast<Tri*>(w + l.tot);
     Tri* off = reinterpret_cast<Tri*>(w + l.off);
     Best* slots = reinterpret_cast<Best*>(w + l.slots);
-    hipLaunchKernelGGL(real_status_kernel, dim3(1), dim3(1), 0, s, status);
-    if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
     const uint32_t tile_grid = static_cast<uint32_t>(l.tiles < (1u << 20) ? l.tiles : (1u << 20));
     hipLaunchKernelGGL(real_tile_kernel, dim3(tile_grid), dim3(kThreads), 0, s, size, h, kind,
-                       num_blocks, l.tiles, pl, cl_lo, cl_hi, rl, tot, status);
+                       num_blocks, l.tiles, pl, cl_lo, cl_hi, rl, tot);
     if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
-    hipLaunchKernelGGL(real_offsets_kernel, dim3(1), dim3(kOffsetThreads), 0, s, tot, l.tiles, off);
+    hipLaunchKernelGGL(real_offsets_kernel, dim3(1), dim3(kOffsetThreads), 0, s, tot, l.tiles, off,
+                       status);
     if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
     const Prefix pf{pl, cl_lo, cl_hi, rl, off};
     const SearchArgs A{seg_offsets, num_segments, req_sizes, req_offsets, num_requests,
