@@ -384,6 +384,27 @@ __device__ __forceinline__ uint64_t owner(const uint64_t* req_off, uint64_t num_
     return lo;
 }
 
+// The same snapshot, found by a whole wavefront (every lane active, same
+// arguments): the first i in [1, B) with req_off[i] > r, by 64 probes a
+// round, so a thousand snapshots take two rounds of loads instead of ten
+// dependent ones.  Probes stay below B (malformed offsets give some b in
+// [0, B), never an access outside req_off).
+__device__ __forceinline__ uint64_t wave_owner(const uint64_t* req_off, uint64_t num_segments,
+                                               uint64_t r, uint32_t lane) {
+    uint64_t lo = 1, hi = num_segments;  // the first such i lies in [lo, hi] (hi: none)
+    while (hi - lo > 64) {
+        const uint64_t step = (hi - lo + 63) >> 6;
+        const uint64_t i = lo + lane * step;
+        const uint64_t m = __ballot(i >= hi || req_off[i] > r);
+        const uint32_t f = m ? static_cast<uint32_t>(__builtin_ctzll(m)) : 64u;
+        const uint64_t nhi = f < 64 ? lo + f * step : hi;
+        lo = f ? lo + (f - 1) * step + 1 : lo;
+        hi = nhi < hi ? nhi : hi;
+    }
+    const uint64_t m = __ballot(lo + lane >= hi || req_off[lo + lane] > r);
+    return (m ? lo + static_cast<uint64_t>(__builtin_ctzll(m)) : hi) - 1;
+}
+
 struct SearchArgs {
     const uint64_t* seg;
     uint64_t num_segments;
@@ -538,7 +559,7 @@ __global__ __launch_bounds__(kThreads) void real_search_kernel(Prefix pf, Search
         const uint64_t r1 = r0 + A.group < A.num_requests ? r0 + A.group : A.num_requests;
         if (lane < kMaxGroup) bestw[w][lane] = best_none();
         for (uint64_t r = r0; r < r1;) {
-            const uint64_t b = owner(A.req_off, A.num_segments, r);
+            const uint64_t b = wave_owner(A.req_off, A.num_segments, r, lane);
             const uint64_t rend = A.req_off[b + 1] < r1 ? A.req_off[b + 1] : r1;
             const uint64_t s0 = A.seg[b], nend = A.seg[b + 1], nb = nend - s0;
             // slice g of the snapshot's starts (nb * g fits: nb < 2^40, g < 2^10)
