@@ -360,10 +360,20 @@ struct Prefix {
     }
 };
 
-// A partial result: exact cost, bytes, window [start, end) in batch indices.
+// A partial result: exact cost, bytes, window [start, end) in batch indices
+// (in snapshot-local indices once to_local has run; the order of candidates
+// of one request is the same either way).
 struct Best {
     uint64_t c_lo, c_hi, bytes, start, end;
 };
+
+__device__ __forceinline__ Best to_local(Best m, uint64_t s0) {
+    if (m.start != ~0ull) {
+        m.start -= s0;
+        m.end -= s0;
+    }
+    return m;
+}
 
 __device__ __forceinline__ Best best_none() { return Best{kNone, kNone, kNone, kNone, kNone}; }
 
@@ -374,19 +384,9 @@ __device__ __forceinline__ bool best_less(const Best& a, const Best& b) {
     return a.start < b.start;
 }
 
-// The snapshot b with req_off[b] <= r < req_off[b + 1].
-__device__ __forceinline__ uint64_t owner(const uint64_t* req_off, uint64_t num_segments, uint64_t r) {
-    uint64_t lo = 0, hi = num_segments;  // answer in [lo, hi)
-    while (hi - lo > 1) {
-        const uint64_t mid = lo + (hi - lo) / 2;
-        if (req_off[mid] <= r) lo = mid; else hi = mid;
-    }
-    return lo;
-}
-
-// The same snapshot, found by a whole wavefront (every lane active, same
-// arguments): the first i in [1, B) with req_off[i] > r, by 64 probes a
-// round, so a thousand snapshots take two rounds of loads instead of ten
+// The snapshot b with req_off[b] <= r < req_off[b + 1], found by a whole
+// wavefront (every lane active, same arguments): the first i in [1, B) with
+// req_off[i] > r, minus one, by 64 probes a round, so a thousand snapshots take two rounds of loads instead of ten
 // dependent ones.  Probes stay below B (malformed offsets give some b in
 // [0, B), never an access outside req_off).
 __device__ __forceinline__ uint64_t wave_owner(const uint64_t* req_off, uint64_t num_segments,
@@ -644,7 +644,7 @@ __global__ __launch_bounds__(kThreads) void real_search_kernel(Prefix pf, Search
 #pragma unroll
                         for (uint32_t j = 0; j < 2; ++j) {
                             pending(SS[j], m2[j]);
-                            const Best m = wave_min(m2[j]);
+                            const Best m = to_local(wave_min(m2[j]), s0);
                             if (lane == 0 && best_less(m, bestw[w][rr + j - r0]))
                                 bestw[w][rr + j - r0] = m;
                         }
@@ -666,7 +666,7 @@ __global__ __launch_bounds__(kThreads) void real_search_kernel(Prefix pf, Search
                             walk_global(pf, i0 < c1 ? i0 : c1, i0 + per < c1 ? i0 + per : c1,
                                         nend, S0, mine);
                         }
-                        const Best m = wave_min(mine);
+                        const Best m = to_local(wave_min(mine), s0);
                         if (lane == 0 && best_less(m, bestw[w][rr - r0])) bestw[w][rr - r0] = m;
                     }
                     rr += 1;
@@ -706,9 +706,8 @@ __global__ __launch_bounds__(kThreads) void real_reduce_kernel(SearchArgs A,
         o.start = o.end = o.cost_lo = o.cost_hi = kNone;
         o.cost = __builtin_inf();
     } else {
-        const uint64_t s0 = A.seg[owner(A.req_off, A.num_segments, r)];
-        o.start = m.start - s0;
-        o.end = m.end - s0;
+        o.start = m.start;
+        o.end = m.end;
         o.cost_lo = m.c_lo;
         o.cost_hi = m.c_hi;
         o.cost = to_real(U128{m.c_lo, m.c_hi});
