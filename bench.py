@@ -48,6 +48,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=5.0,
                     help="target duration of the CPU-oracle baseline (0 disables it)")
     ap.add_argument("--no-parity", action="store_true")
+    ap.add_argument("--medians", action="store_true",
+                    help="window search: after the timed region, also time single launches "
+                         "(medians, cold and warm cache)")
     ap.add_argument("--policy", choices=["window", "greedy"], default="window",
                     help="replay eviction policy timed by --op replay: Coop's sliding window "
                          "or the DTR-style greedy baseline")
@@ -77,6 +80,20 @@ def fit_bytes(pools):
     of every block once, whatever the number of requests, plus S (8 B) and
     the 8-byte result per request."""
     return 9 * pools.num_blocks + 16 * pools.num_requests
+
+
+def per_launch_ms(launch, count, stream):
+    """Milliseconds of each of `count` launches, timed one by one with events
+    on `stream` (outside the timed region; for medians)."""
+    import torch
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(count)]
+    for i, (a, b) in enumerate(evs):
+        a.record(stream)
+        launch(i)
+        b.record(stream)
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) for a, b in evs]
 
 
 def copy_ceiling(dev, nbytes=1 << 30, reps=10):
@@ -238,6 +255,15 @@ def main():
 
     achieved = alg_bytes / t / 1e9
     traffic = measured_traffic(spec.name)
+    # medians of single launches: cold (copies in turn, as timed above) and
+    # warm (the same copy every time, inputs left in the Infinity Cache)
+    single = None
+    if args.medians:
+        n_each = max(20, args.steps)
+        cold_each = per_launch_ms(lambda i: calls[i % copies].launch(sh), n_each, stream)
+        warm_each = per_launch_ms(lambda i: calls[0].launch(sh), n_each, stream)
+        single = {"count": n_each, "median_cold": float(np.median(cold_each)),
+                  "median_warm": float(np.median(warm_each)), "min_cold": float(np.min(cold_each))}
     ceiling = copy_ceiling(dev)
     cpu = cpu_baseline(pools, args.cpu_seconds) if args.cpu_seconds > 0 else None
     nb = np.diff(pools.seg_offsets.astype(np.int64))
@@ -284,6 +310,7 @@ def main():
         "cpu_baseline": cpu,
         "parity_vs_oracle": parity,
         "wall_s_timed_region": wall,
+        "single_launch_ms": single,
         "kernel_source": source_digest(),
     }
     print(json.dumps(rec), flush=True)
