@@ -192,7 +192,7 @@ constexpr uint64_t kBadTile = 1ull << 63;  // in a tile total's pinned count
 // an 8-byte load of kinds when the block lies wholly inside the batch and
 // the inputs are aligned, single loads otherwise; the prefixes go out as
 // 16-byte stores the same way.
-__global__ __launch_bounds__(kThreads) void real_tile_kernel(
+__global__ __launch_bounds__(kThreads, 4) void real_tile_kernel(
     const uint64_t* __restrict__ size, const double* __restrict__ h,
     const uint8_t* __restrict__ kind, uint64_t n, uint64_t num_tiles, uint64_t* __restrict__ pl,
     uint64_t* __restrict__ cl_lo, uint64_t* __restrict__ cl_hi, uint16_t* __restrict__ rl,
