@@ -233,6 +233,36 @@ __device__ __forceinline__ Cand wave_argmin(Cand k) {
     return Cand{readlane64(k.cost, 63), readlane64(k.excess, 63), readlane32(k.start, 63)};
 }
 
+// The same minimum for windows inside a packed staged region, whose excess
+// is below 2^50 and whose start is a staged index below 2^13: (excess,
+// start) then orders as the one word excess << 13 | start, and each step
+// moves and compares two words instead of three.
+constexpr uint32_t kStartBits = 13;
+static_assert(kTile <= (1u << kStartBits), "in-region starts fit the start field");
+static_assert(kValBits + kStartBits < 64, "a packed key stays below the empty value");
+template <int Ctrl, int RowMask>
+__device__ __forceinline__ void argmin2_step(uint64_t& cost, uint64_t& key) {
+    const uint64_t oc = dpp64<Ctrl, RowMask>(cost, kNone), ok = dpp64<Ctrl, RowMask>(key, kNone);
+    const bool less = oc < cost || (oc == cost && ok < key);
+    cost = less ? oc : cost;
+    key = less ? ok : key;
+}
+
+__device__ __forceinline__ Cand wave_argmin_packed(const Cand& k) {
+    uint64_t cost = k.cost;
+    uint64_t key = k.start == kNone32 ? kNone : (k.excess << kStartBits) | k.start;
+    argmin2_step<kQuadXor1, 0xf>(cost, key);
+    argmin2_step<kQuadXor2, 0xf>(cost, key);
+    argmin2_step<kRowHalfMirror, 0xf>(cost, key);
+    argmin2_step<kRowMirror, 0xf>(cost, key);
+    argmin2_step<kRowBcast15, 0xa>(cost, key);
+    argmin2_step<kRowBcast31, 0xc>(cost, key);
+    cost = readlane64(cost, 63);
+    key = readlane64(key, 63);
+    if (key == kNone) return cand_none();
+    return Cand{cost, key >> kStartBits, static_cast<uint32_t>(key & ((1u << kStartBits) - 1))};
+}
+
 // Candidate window: ordered by (cost, bytes, start); `end` rides along.
 // Start and end are snapshot-local.
 struct Key {
@@ -965,9 +995,10 @@ __device__ __forceinline__ void store_answer(const Params& P, const Job& job, ui
 
 // This wavefront's answer from per-lane bests: the lexicographic minimum,
 // with its end taken from a lane that holds it.
+template <bool kPacked = false>
 __device__ __forceinline__ Key wave_answer(const Cand& best, uint64_t best_end, uint64_t tl,
                                            uint64_t S) {
-    const Cand m = wave_argmin(best);
+    const Cand m = kPacked ? wave_argmin_packed(best) : wave_argmin(best);
     if (m.start == kNone32) return key_none();
     const uint64_t won = __ballot(best.start == m.start);
     const uint64_t e = readlane64(best_end, static_cast<uint32_t>(__builtin_ctzll(won)));
@@ -1030,7 +1061,9 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
                 if (lane == n) pend = cur;
             }
         }
-        Key k = wave_answer(best, best_end, tl, S);
+        // in-region windows of a packed region: excess below 2^50
+        Key k = ts.packed ? wave_answer<true>(best, best_end, tl, S)
+                          : wave_answer(best, best_end, tl, S);
         if (wpr == 1) {
             k = min_key(readlane_key(acc, n), k);
             if (lane == n) acc = k;
