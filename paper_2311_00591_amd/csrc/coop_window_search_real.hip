@@ -427,6 +427,37 @@ __device__ __forceinline__ Best wave_min(Best v) {
     return v;
 }
 
+// The same minimum over windows that the merge path found in the chunk
+// starting at c0: their bytes are below 2^51 and their starts lie in
+// [c0, c0 + 2^12), so (bytes, start) orders as the one word
+// bytes << 12 | (start - c0), and the end need not travel: it is read from a
+// lane that holds the winning start (lanes holding the same start hold the
+// same window).
+constexpr uint32_t kChunkBits = 12;
+static_assert(kChunk <= (1u << kChunkBits), "chunk offsets fit the start field");
+static_assert(kPackBits + kChunkBits < 64, "a packed key stays below the empty value");
+
+__device__ __forceinline__ Best wave_min_chunk(const Best& v, uint64_t c0) {
+    uint64_t c_lo = v.c_lo, c_hi = v.c_hi;
+    uint64_t key = v.start == kNone ? kNone : (v.bytes << kChunkBits) | (v.start - c0);
+    for (int o = 32; o >= 1; o >>= 1) {
+        const uint64_t xl = shfl_xor64(c_lo, o), xh = shfl_xor64(c_hi, o), xk = shfl_xor64(key, o);
+        const bool less = xh < c_hi || (xh == c_hi && (xl < c_lo || (xl == c_lo && xk < key)));
+        c_lo = less ? xl : c_lo;
+        c_hi = less ? xh : c_hi;
+        key = less ? xk : key;
+    }
+    if (key == kNone) return best_none();
+    const uint64_t start = c0 + (key & ((1ull << kChunkBits) - 1));
+    const uint64_t won = __ballot(v.start == start);
+    const uint32_t wl = static_cast<uint32_t>(__builtin_ctzll(won));
+    const uint64_t end =
+        (static_cast<uint64_t>(static_cast<uint32_t>(__builtin_amdgcn_readlane(
+             static_cast<int>(v.end >> 32), static_cast<int>(wl)))) << 32) |
+        static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v.end), static_cast<int>(wl)));
+    return Best{c_lo, c_hi, key >> kChunkBits, start, end};
+}
+
 // Starts [i, i_end) of one snapshot (ending at nend), walked by one thread
 // from the global prefixes alone: the first start's shortest end by
 // bisection, the later ones by walking on.  pred(x): x is past the run of
@@ -613,8 +644,9 @@ __global__ __launch_bounds__(kThreads) void real_search_kernel(Prefix pf, Search
                 const uint64_t span = packed_chunk ? Y[nB] & (kPackOne - 1) : 0;
                 // starts whose target is above every staged end key: their windows
                 // end past hi (or nowhere); a suffix of the chunk, walked globally
-                auto pending = [&](uint64_t S, Best& mine) {
-                    if (hi >= nend) return;
+                // (true when some start of the chunk was walked globally)
+                auto pending = [&](uint64_t S, Best& mine) -> bool {
+                    if (hi >= nend) return false;
                     uint32_t plo = 0, phi = nA;
                     const uint64_t ylast = Y[nB];
                     while (plo < phi) {
@@ -628,6 +660,7 @@ __global__ __launch_bounds__(kThreads) void real_search_kernel(Prefix pf, Search
                         walk_global(pf, q0 < c1 ? q0 : c1, q0 + per < c1 ? q0 + per : c1, nend, S,
                                     mine);
                     }
+                    return np != 0;
                 };
                 auto fast = [&](uint64_t S) {
                     return S != 0 && packed_chunk && S <= kPackOne - span;
@@ -643,8 +676,9 @@ __global__ __launch_bounds__(kThreads) void real_search_kernel(Prefix pf, Search
                         merge_requests<2>(Y, Cr, nA, nB, SS, c0, m2);
 #pragma unroll
                         for (uint32_t j = 0; j < 2; ++j) {
-                            pending(SS[j], m2[j]);
-                            const Best m = to_local(wave_min(m2[j]), s0);
+                            const bool walked = pending(SS[j], m2[j]);
+                            const Best m = to_local(
+                                walked ? wave_min(m2[j]) : wave_min_chunk(m2[j], c0), s0);
                             if (lane == 0 && best_less(m, bestw[w][rr + j - r0]))
                                 bestw[w][rr + j - r0] = m;
                         }
