@@ -2,18 +2,22 @@
 
 A step is one coop_window_search call: every request of one batch of
 synthetic pool snapshots, inputs already resident in HBM (--op first_fit:
-one coop_first_fit call on the same batch instead).  The default
-workload is the batched mid-pool batch (1024 snapshots x 4096 blocks, one
-request each).  To measure HBM rather than the 256 MB Infinity Cache, the
+one coop_first_fit call on the same batch instead).  The headline workload
+is the ragged heavy-tailed batch (4096 snapshots of 64..32768 blocks, four
+requests each, about 66 M blocks), the largest batch; the batched mid pools,
+the large pools with 16 requests each and the single huge pool are timed in
+the same run and reported under per_config.  To measure HBM rather than the
+256 MB Infinity Cache, the
 batch is replicated into enough distinct device buffers that consecutive
 steps never find their inputs cached (each copy is revisited only after
 more than twice the cache size has been streamed); --copies 1 gives the
 warm-cache number.
 
 Prints one JSON line (rank 0): queries/s as `value`, blocks scanned/s, the
-HBM roofline of the search kernel (algorithmic bytes per launch / average
-launch time, timed with HIP events on the launch stream), and the CPU oracle
-timed on this host as a reported baseline.
+HBM roofline of the search kernel (algorithmic bytes per launch, counted per
+request, / average launch time, timed with HIP events on the launch stream),
+the fraction of compulsory bytes (every block once), an integer-arithmetic
+roofline, and the CPU oracle timed on this host as a reported baseline.
 """
 import argparse
 import hashlib
@@ -33,6 +37,7 @@ REPLAY_METRIC = "Algorithm 1 replay: allocator operations/sec over independent p
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E, published
 INFINITY_CACHE_BYTES = 256 << 20
 KERNEL = "coop_window_search_kernel"
+HEADLINE_CONFIG = 3   # the ragged heavy-tailed batch: the largest batch
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2311_00591_amd", "csrc", "coop_window_search.hip")
 
 
@@ -41,12 +46,18 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=1, help="standard workload index 0..4")
+    ap.add_argument("--config", type=int, default=None,
+                    help="standard workload index 0..4 (default: the ragged batch, 3, as the "
+                         "headline, with --extra-configs timed in the same run)")
+    ap.add_argument("--extra-configs", default="1,2,4",
+                    help="window search without --config: further workloads timed after the "
+                         "headline and reported under per_config")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--copies", type=int, default=0,
                     help="distinct device copies of the batch (0: enough to defeat the cache)")
-    ap.add_argument("--cpu-seconds", type=float, default=5.0,
-                    help="target duration of the CPU-oracle baseline (0 disables it)")
+    ap.add_argument("--cpu-seconds", type=float, default=8.0,
+                    help="CPU-oracle budget for the headline workload, half of it for each "
+                         "further one (0: no CPU baseline)")
     ap.add_argument("--no-parity", action="store_true")
     ap.add_argument("--medians", action="store_true",
                     help="window search: after the timed region, also time single launches "
@@ -187,32 +198,106 @@ def _cpu_model():
     return None
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py: the search runs on one GPU only (asked for {args.gpus}); "
-              "sharding across GPUs is not implemented", file=sys.stderr)
-        sys.exit(2)
+def sub_requests(pools, idx):
+    """The batch with only requests idx (sorted indices into req_sizes): same
+    blocks and snapshots, req_offsets recounted."""
+    import workloads
+    idx = np.asarray(idx, dtype=np.int64)
+    roff = np.searchsorted(idx, pools.req_offsets.astype(np.int64), side="left").astype(np.uint64)
+    return workloads.Pools(pools.size, pools.cost, pools.kind, pools.seg_offsets,
+                           pools.req_sizes[idx], roff)
 
+
+def _threads():
+    try:
+        threads = len(os.sched_getaffinity(0))
+    except AttributeError:
+        threads = os.cpu_count() or 1
+    return max(1, min(threads, 64))
+
+
+def _even_sample(n, m):
+    """m evenly spaced indices of range(n) (all of them when m >= n)."""
+    if m >= n:
+        return np.arange(n, dtype=np.int64)
+    return np.unique((np.arange(m, dtype=np.float64) * n / m).astype(np.int64))
+
+
+def oracle_window_timed(pools, budget_s, threads):
+    """The oracle's answers and its rate on this host: whole passes over the
+    batch when one pass fits the budget, else an evenly spaced sample of
+    requests sized to it.  Returns (request indices answered, their oracle
+    results, CPU-baseline record)."""
+    import oracle
+    Q = pools.num_requests
+    # two probes separate the per-call cost (a pass over the blocks) from
+    # the per-request cost
+    times = []
+    for m0 in (max(1, min(Q, 8 * threads)), max(1, min(Q, 32 * threads))):
+        probe = _even_sample(Q, m0)
+        t0 = time.perf_counter()
+        oracle.window_search(*sub_requests(pools, probe).arrays(), threads=threads)
+        times.append((len(probe), time.perf_counter() - t0))
+    (m1_, t1_), (m2_, t2_) = times
+    per_req = max((t2_ - t1_) / (m2_ - m1_) if m2_ > m1_ else t2_ / m2_, t2_ / m2_ / 8, 1e-9)
+    fixed = max(0.0, t2_ - per_req * m2_)
+    m = Q if fixed + per_req * Q <= budget_s else max(m2_, int((budget_s - fixed) / per_req))
+    idx = _even_sample(Q, m)
+    batch = pools if len(idx) == Q else sub_requests(pools, idx)
+    t0 = time.perf_counter()
+    want = oracle.window_search(*batch.arrays(), threads=threads)
+    dt = time.perf_counter() - t0
+    passes = 1
+    if len(idx) == Q and dt < budget_s / 2:
+        passes += max(0, min(1000, int((budget_s - dt) / max(dt, 1e-6))))
+        t0 = time.perf_counter()
+        for _ in range(passes - 1):
+            oracle.window_search(*batch.arrays(), threads=threads)
+        dt += time.perf_counter() - t0
+    # one thread, on an evenly spaced sample taking about a quarter of the budget
+    m1 = max(1, min(Q, int(budget_s / 4 / max(per_req * threads, 1e-9))))
+    s1 = sub_requests(pools, _even_sample(Q, m1))
+    t0 = time.perf_counter()
+    oracle.window_search(*s1.arrays(), threads=1)
+    d1 = time.perf_counter() - t0
+    what = (f"whole workload ({Q} requests) x {passes} passes" if len(idx) == Q else
+            f"{len(idx)} of {Q} requests, evenly spaced")
+    cpu = {"value": passes * len(idx) / dt, "unit": "queries/s", "cores": threads,
+           "kind": "oracle", "single_thread_value": s1.num_requests / d1,
+           "cpu_model": _cpu_model(),
+           "sample": f"{what}, {dt:.1f} s, two-pointer sweep, {threads} threads; one thread: "
+                     f"{s1.num_requests} requests evenly spaced, {d1:.1f} s"}
+    return idx, want, cpu
+
+
+# Peak of the u64 lane operations the search needs (see alu_ops): 256 CUs x
+# 4 SIMDs x 16 lanes x 2.4 GHz, one 32-bit or single-instruction 64-bit
+# lane operation per lane and cycle (no packed forms).
+PEAK_ALU_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
+ALU_OPS_PER_BLOCK_QUERY = 8
+
+
+def alu_ops(block_queries):
+    """Algorithmic integer operations of one pass: per block and request the
+    start's target (an add) and its end search (two compares: every start
+    and every end key is met once by a two-pointer sweep), the window's cost
+    and bytes (two subtractions), and its place in the ranking (two compares
+    on cost and bytes, one on the run): 8 u64 operations.  The prefix sums
+    (two adds per block) are shared by the snapshot's requests and left out."""
+    return ALU_OPS_PER_BLOCK_QUERY * block_queries
+
+
+def bench_window_config(k, args, dev, cpu_budget, steps, warmup):
+    """One workload: parity with the oracle, warm-up, `steps` timed calls,
+    rooflines and the oracle's rate.  Returns the record (without the
+    top-level contract keys)."""
     import torch
 
     import paper_2311_00591_amd as coop
     import workloads
 
-    if not torch.cuda.is_available():
-        print("bench.py needs a GPU", file=sys.stderr)
-        sys.exit(1)
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-
-    if args.op == "replay":
-        return bench_replay(args, dev)
-    spec = workloads.CONFIGS[args.config]
-    pools = workloads.make_config(args.config, args.seed)
-    if args.op == "first_fit":
-        return bench_first_fit(args, pools, spec, dev)
-    if args.op == "real":
-        return bench_real(args, pools, spec, dev)
+    spec = workloads.CONFIGS[k]
+    pools = workloads.make_config(k, args.seed)
     block_queries, alg_bytes, unique_bytes = workload_bytes(pools)
     batch_dev_bytes = 17 * pools.num_blocks + 16 * pools.num_segments + 8 * pools.num_requests
     copies = args.copies or max(1, -(-2 * INFINITY_CACHE_BYTES // batch_dev_bytes) + 1)
@@ -229,94 +314,171 @@ def main():
 
     stream = torch.cuda.current_stream(dev)
     sh = stream.cuda_stream
-    parity = None
-    if not args.no_parity:
-        import oracle
+    parity = parity_sample = cpu = None
+    threads = _threads()
+    if not args.no_parity or cpu_budget > 0:
         calls[0].launch(sh)
         torch.cuda.synchronize()
         got = out.cpu().numpy().view(np.uint64)
-        want = oracle.window_search(*pools.arrays(), threads=16)
-        parity = bool(np.array_equal(got, want))
+        idx, want, cpu = oracle_window_timed(pools, max(cpu_budget, 1.0), threads)
+        parity = bool(np.array_equal(got[idx], want))
+        parity_sample = ("every request" if len(idx) == pools.num_requests else
+                         f"{len(idx)} of {pools.num_requests} requests, evenly spaced")
+        if cpu_budget <= 0:
+            cpu = None
+        if args.no_parity:
+            parity = parity_sample = None
 
-    for i in range(args.warmup):
+    for i in range(warmup):
         calls[i % copies].launch(sh)
     torch.cuda.synchronize()
 
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     w0 = time.perf_counter()
     start.record(stream)
-    for i in range(args.steps):
+    for i in range(steps):
         calls[i % copies].launch(sh)
     stop.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
-    ms = start.elapsed_time(stop) / args.steps
+    ms = start.elapsed_time(stop) / steps
     t = ms / 1e3
 
     achieved = alg_bytes / t / 1e9
-    traffic = measured_traffic(spec.name)
-    # medians of single launches: cold (copies in turn, as timed above) and
-    # warm (the same copy every time, inputs left in the Infinity Cache)
+    ops = alu_ops(block_queries)
+    alu = {"bound": "alu", "achieved": ops / t / 1e12, "peak": PEAK_ALU_TOPS, "unit": "TOP/s",
+           "frac": ops / t / 1e12 / PEAK_ALU_TOPS, "ops_per_launch": ops,
+           "ops_per_block_query": ALU_OPS_PER_BLOCK_QUERY}
+    hbm = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+           "frac": achieved / PEAK_HBM_GBS, "traffic": measured_traffic(spec.name),
+           "algorithmic_bytes_per_launch": alg_bytes,
+           "bytes_counted": "per request: 17 B per block of its snapshot + 32 B",
+           "compulsory_frac": unique_bytes / t / 1e9 / PEAK_HBM_GBS,
+           "compulsory_bytes_per_launch": unique_bytes}
+    # Where the staged tiles serve so many requests that the per-request
+    # count passes the HBM peak, the bound is the integer arithmetic.
+    if achieved > PEAK_HBM_GBS:
+        roofline = dict(alu, per_request_hbm=hbm)
+    else:
+        roofline = dict(hbm, alu=alu)
+    roofline["kernel"] = KERNEL
     single = None
     if args.medians:
-        n_each = max(20, args.steps)
+        n_each = max(20, steps)
         cold_each = per_launch_ms(lambda i: calls[i % copies].launch(sh), n_each, stream)
         warm_each = per_launch_ms(lambda i: calls[0].launch(sh), n_each, stream)
         single = {"count": n_each, "median_cold": float(np.median(cold_each)),
                   "median_warm": float(np.median(warm_each)), "min_cold": float(np.min(cold_each))}
-    ceiling = copy_ceiling(dev)
-    cpu = cpu_baseline(pools, args.cpu_seconds) if args.cpu_seconds > 0 else None
     nb = np.diff(pools.seg_offsets.astype(np.int64))
     rec = {
-        "metric": METRIC,
+        "workload": f"{spec.name}: B={pools.num_segments} snapshots, "
+                    f"N_b={int(nb.min())}..{int(nb.max())} blocks, "
+                    f"{pools.num_requests} requests (standard workload {k})",
+        "config_index": k,
         "value": pools.num_requests / t,
+        "unit": "queries/s",
+        "ms_per_step": ms,
+        "steps": steps,
+        "warmup": warmup,
+        "num_segments": pools.num_segments,
+        "num_blocks": pools.num_blocks,
+        "num_requests": pools.num_requests,
+        "seed": args.seed,
+        "input_sha256": pools.digest()[:16],
+        "resident_copies": copies,
+        "cache": "cold" if copies > 1 else "warm",
+        "blocks_scanned_per_s": block_queries / t,
+        "hbm_roofline_pct": 100.0 * achieved / PEAK_HBM_GBS,
+        "compulsory_hbm_pct": 100.0 * unique_bytes / t / 1e9 / PEAK_HBM_GBS,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "parity_vs_oracle": parity,
+        "parity_sample": parity_sample,
+        "wall_s_timed_region": wall,
+        "single_launch_ms": single,
+    }
+    del calls, base, out, workspace
+    torch.cuda.empty_cache()
+    return rec
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: the search runs on one GPU only (asked for {args.gpus}); "
+              "sharding across GPUs is not implemented", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    if args.op == "replay":
+        return bench_replay(args, dev)
+    import workloads
+    if args.op in ("first_fit", "real"):
+        k = HEADLINE_CONFIG if args.config is None else args.config
+        pools = workloads.make_config(k, args.seed)
+        spec = workloads.CONFIGS[k]
+        if args.op == "first_fit":
+            return bench_first_fit(args, pools, spec, dev, k)
+        return bench_real(args, pools, spec, dev, k)
+
+    # The window search: the headline workload, then (by default) the other
+    # batched workloads in the same run, each timed the same way.
+    head_k = HEADLINE_CONFIG if args.config is None else args.config
+    extra = [] if args.config is not None else [int(x) for x in args.extra_configs.split(",") if x]
+    head = bench_window_config(head_k, args, dev, args.cpu_seconds, args.steps, args.warmup)
+    per_config = {}
+    for k in extra:
+        if k == head_k:
+            continue
+        steps = args.steps if k != 4 else max(1, min(args.steps, 10))
+        warmup = args.warmup if k != 4 else max(1, min(args.warmup, 2))
+        per_config[f"config{k}"] = bench_window_config(k, args, dev, args.cpu_seconds / 2,
+                                                       steps, warmup)
+    ceiling = copy_ceiling(dev)
+    for r in [head, *per_config.values()]:
+        rf = r["roofline"]
+        hb = rf if rf["bound"] == "hbm" else rf["per_request_hbm"]
+        hb["copy_ceiling"] = ceiling
+        hb["frac_of_copy_ceiling"] = hb["achieved"] / ceiling
+    rec = {
+        "metric": METRIC,
+        "value": head["value"],
         "unit": "queries/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms,
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "u64",
         "data": "synthetic",
-        "config": {
-            "workload": f"{spec.name}: B={pools.num_segments} snapshots, "
-                        f"N_b={int(nb.min())}..{int(nb.max())} blocks, "
-                        f"{pools.num_requests} requests (standard workload {args.config})",
-            "num_segments": pools.num_segments,
-            "num_blocks": pools.num_blocks,
-            "num_requests": pools.num_requests,
-            "seed": args.seed,
-            "input_sha256": pools.digest()[:16],
-            "resident_copies": copies,
-            "cache": "cold" if copies > 1 else "warm",
-        },
-        "blocks_scanned_per_s": block_queries / t,
-        "hbm_roofline_pct": 100.0 * achieved / PEAK_HBM_GBS,
-        "compulsory_hbm_pct": 100.0 * unique_bytes / t / 1e9 / PEAK_HBM_GBS,
-        "roofline": {
-            "kernel": KERNEL,
-            "bound": "hbm",
-            "achieved": achieved,
-            "peak": PEAK_HBM_GBS,
-            "unit": "GB/s",
-            "frac": achieved / PEAK_HBM_GBS,
-            "traffic": traffic,
-            "algorithmic_bytes_per_launch": alg_bytes,
-            "copy_ceiling": ceiling,
-            "frac_of_copy_ceiling": achieved / ceiling,
-        },
-        "cpu_baseline": cpu,
-        "parity_vs_oracle": parity,
-        "wall_s_timed_region": wall,
-        "single_launch_ms": single,
+        "config": {k2: head[k2] for k2 in ("workload", "num_segments", "num_blocks",
+                                             "num_requests", "seed", "input_sha256",
+                                             "resident_copies", "cache")},
+        "blocks_scanned_per_s": head["blocks_scanned_per_s"],
+        "hbm_roofline_pct": head["hbm_roofline_pct"],
+        "compulsory_hbm_pct": head["compulsory_hbm_pct"],
+        "roofline": head["roofline"],
+        "cpu_baseline": head["cpu_baseline"],
+        "parity_vs_oracle": head["parity_vs_oracle"],
+        "parity_sample": head["parity_sample"],
+        "wall_s_timed_region": head["wall_s_timed_region"],
+        "single_launch_ms": head["single_launch_ms"],
+        "per_config": per_config,
         "kernel_source": source_digest(),
     }
     print(json.dumps(rec), flush=True)
 
 
-def bench_first_fit(args, pools, spec, dev):
+def bench_first_fit(args, pools, spec, dev, k):
     import torch
 
     import paper_2311_00591_amd as coop
@@ -376,7 +538,7 @@ def bench_first_fit(args, pools, spec, dev):
         "config": {
             "workload": f"first fit on {spec.name}: B={pools.num_segments} snapshots, "
                         f"N_b={int(nb.min())}..{int(nb.max())} blocks, "
-                        f"{pools.num_requests} requests (standard workload {args.config})",
+                        f"{pools.num_requests} requests (standard workload {k})",
             "num_segments": pools.num_segments,
             "num_blocks": pools.num_blocks,
             "num_requests": pools.num_requests,
@@ -407,7 +569,7 @@ def bench_first_fit(args, pools, spec, dev):
 REAL_SOURCE = os.path.join(ROOT, "paper_2311_00591_amd", "csrc", "coop_window_search_real.hip")
 
 
-def bench_real(args, pools, spec, dev):
+def bench_real(args, pools, spec, dev, k):
     """The search with real-valued heuristics h = cost / staleness on a
     standard workload: same metric and byte accounting as the integer
     search (17 B per block and request: size, h, kind), timed per call."""
@@ -480,7 +642,7 @@ def bench_real(args, pools, spec, dev):
             "workload": f"real-valued heuristics on {spec.name}: B={pools.num_segments} "
                         f"snapshots, N_b={int(nb.min())}..{int(nb.max())} blocks, "
                         f"{pools.num_requests} requests, h = cost / staleness U{{1..4096}} "
-                        f"(standard workload {args.config})",
+                        f"(standard workload {k})",
             "num_segments": pools.num_segments,
             "num_blocks": pools.num_blocks,
             "num_requests": pools.num_requests,
@@ -517,7 +679,8 @@ def bench_replay(args, dev):
     import paper_2311_00591_amd as coop
     from workloads import traces
 
-    k = args.config if args.config < len(traces.REPLAY_CONFIGS) else len(traces.REPLAY_CONFIGS) - 1
+    kc = 1 if args.config is None else args.config
+    k = kc if kc < len(traces.REPLAY_CONFIGS) else len(traces.REPLAY_CONFIGS) - 1
     spec = traces.REPLAY_CONFIGS[k]
     state, trace = traces.make_replay(k, args.seed)
     P, cap, T = len(state["len"]), state["capacity"], trace["num_ops"]

@@ -159,7 +159,7 @@ coop_status_t coop_window_search(const uint64_t *size, const uint64_t *cost,
                                  void *workspace, size_t workspace_bytes, void *stream);
 
 /*
- * First fit (section 2.4; Algorithm 1's find_free_block_not_less_than, the
+ * First fit (section 2.1; Algorithm 1's find_free_block_not_less_than, the
  * step before any eviction): for every request of S bytes, the leftmost free
  * chunk (kind == COOP_FREE) of its snapshot holding at least S bytes, where
  * a first-fit allocator places the tensor.  Evictable and pinned blocks are
@@ -267,7 +267,7 @@ typedef enum {
  *   skipped release), out_window[2] (the evicted window, indices before the
  *   eviction, or ~0; greedy: {number of tensors evicted, ~0}), out_cost (the
  *   evicted cost, modulo 2^64), out_free (free bytes just before an
- *   eviction, else ~0: the fragmentation-rate sample of section 4.1, free
+ *   eviction, else ~0: the fragmentation-rate sample of section 4.2, free
  *   memory over the memory the allocator holds).
  * status (device u32): set to 0, then bit 0 if a pool ran out of slots (that
  *   allocation is skipped), bit 1 for an invalid operation.

@@ -137,7 +137,7 @@ def search_single(size, cost, kind, requests, threads=1):
 
 
 def first_fit(size, kind, seg_offsets, req_sizes, req_offsets, threads=1):
-    """Leftmost free chunk of at least S bytes (section 2.4, Algorithm 1's
+    """Leftmost free chunk of at least S bytes (section 2.1, Algorithm 1's
     find_free_block_not_less_than); returns uint64 (Q,) snapshot-local block
     indices, 2**64-1 where the snapshot has no such chunk."""
     size, seg_offsets = _u64(size), _u64(seg_offsets)

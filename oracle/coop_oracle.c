@@ -480,7 +480,7 @@ int coop_oracle_brute_eq1(const uint64_t *size, const uint64_t *cost,
 }
 
 /* ---------------------------------------------------------------------------
- * First fit (section 2.4, and find_free_block_not_less_than in Algorithm 1):
+ * First fit (section 2.1, and find_free_block_not_less_than in Algorithm 1):
  * the allocator places a tensor of S bytes at the left end of a free chunk
  * of at least S bytes, the leftmost such chunk.  The answer is that chunk's
  * index in its snapshot, found by walking the list from the left.
@@ -559,7 +559,7 @@ int coop_oracle_first_fit(const uint64_t *size, const uint8_t *kind, uint64_t nu
 /* ---------------------------------------------------------------------------
  * Replay of Algorithm 1 on independent pools.  A pool is its address-sorted
  * block list, holding a fixed number of bytes; no two free chunks are ever
- * adjacent (section 2.4: a released chunk merges with its free neighbours).
+ * adjacent (section 2.1: a released chunk merges with its free neighbours).
  * Each operation of a pool's trace is applied in order:
  *
  *   allocate(id, S, flags): first fit; if no free chunk holds S bytes, the
@@ -577,7 +577,7 @@ int coop_oracle_first_fit(const uint64_t *size, const uint8_t *kind, uint64_t nu
  * merged free chunk of a release; ~0 for a failure or a no-op), the evicted
  * window [start, end) in pre-eviction indices (~0 when nothing was evicted),
  * its eviction cost, and, for an eviction, the free bytes of the pool just
- * before it (the fragmentation-rate sample of section 4.1: free memory over
+ * before it (the fragmentation-rate sample of section 4.2: free memory over
  * the memory the allocator holds).
  * ------------------------------------------------------------------------- */
 #define OP_ALLOC 0

@@ -84,7 +84,7 @@ int coop_oracle_brute_eq1(const uint64_t *size, const uint64_t *cost,
                           const uint64_t *req_sizes, const uint64_t *req_offsets,
                           uint64_t num_requests, uint64_t *out_cost);
 
-/* First fit (section 2.4; find_free_block_not_less_than in Algorithm 1):
+/* First fit (section 2.1; find_free_block_not_less_than in Algorithm 1):
  * for every request, the lowest snapshot-local index k of a free chunk
  * (kind[k] == 0) with size[k] >= S, or ~0 when the snapshot holds none.
  * S == 0 takes the first free chunk.  out[num_requests].  Same batch layout

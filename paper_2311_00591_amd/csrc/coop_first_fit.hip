@@ -1,4 +1,4 @@
-// Batched first fit (Coop, section 2.4 and Algorithm 1) for gfx950.
+// Batched first fit (Coop, section 2.1 and Algorithm 1) for gfx950.
 //
 // For every request of S bytes on a pool snapshot: the leftmost free chunk
 // (kind 0) holding at least S bytes -- where a first-fit allocator places the

@@ -120,6 +120,14 @@ constexpr uint32_t kEpochShift = 24;             // counter = epoch << 24 | tick
 constexpr uint64_t kTagMask = (1ull << 39) - 1;
 constexpr uint64_t kGraphTag = 1ull << 39;
 constexpr uint64_t kTagOdd = 0x9e3779b97f4a7c15ull;
+// The queue word's 32-bit tag: the call tag's low 31 bits, and bit 31 set
+// for graph replays (call tag bit 39), so that an eager call and a replay
+// never carry the same queue tag.
+__host__ __device__ constexpr uint32_t queue_tag(uint64_t call_tag) {
+    return static_cast<uint32_t>(call_tag & 0x7fffffffull) | ((call_tag & kGraphTag) ? 0x80000000u : 0u);
+}
+static_assert(queue_tag(kGraphTag) == 0x80000000u && queue_tag(kGraphTag - 1) == 0x7fffffffu,
+              "graph and eager queue tags differ in bit 31");
 // Queue word: call tag << 32 | chunks claimed.  A reserve chunk slot holds a
 // chunk index, kQEmpty (nothing claimed yet) or kQDone (the queue ran dry).
 constexpr uint64_t kQEmpty = ~0ull, kQDone = ~0ull - 1;
@@ -1293,7 +1301,7 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
         // same value; P.epoch holds a per-process salt.
         const uint64_t t = __hip_atomic_load(P.tag_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         P.epoch = kGraphTag | ((t * kTagOdd + P.epoch) & kTagMask);
-        P.qtag = static_cast<uint32_t>(P.epoch);
+        P.qtag = queue_tag(P.epoch);
     }
     // The queue, when there is one: workgroup 0 stamps this call's tag; claims
     // that reach the word before the stamp see an old tag and try again.
@@ -1604,7 +1612,7 @@ coop_status_t coop_window_search_enqueue(const uint64_t* size, const uint64_t* c
     if (capture == hipStreamCaptureStatusNone) {
         const uint64_t call = g_calls.fetch_add(1, std::memory_order_relaxed);
         P.epoch = call & kTagMask;
-        P.qtag = static_cast<uint32_t>(call);
+        P.qtag = queue_tag(P.epoch);
         P.tag_word = nullptr;
     } else {
         uint64_t* word = P.queue + 1;

@@ -1,4 +1,4 @@
-"""Pins the first-fit oracle (section 2.4; find_free_block_not_less_than in
+"""Pins the first-fit oracle (section 2.1; find_free_block_not_less_than in
 Algorithm 1) to things other than itself:
 
 * hand-derived worked examples (tests/golden/first_fit_examples.txt);
