@@ -65,11 +65,13 @@ typedef enum {
     COOP_ERR_INVALID = -1,   /* null pointer with a nonzero count, bad sizes */
     COOP_ERR_WORKSPACE = -2, /* workspace missing or smaller than required */
     COOP_ERR_HIP = -3,       /* a HIP launch failed; the HIP error is cleared */
-    COOP_ERR_OVERFLOW = -4   /* debug checks only: a run's total exceeds 2^64 - 1 */
+    COOP_ERR_OVERFLOW = -4,  /* debug checks only: a run's total exceeds 2^64 - 1 */
+    COOP_ERR_TOO_LARGE = -5  /* coop_window_search_static: the batch needs more
+                                scratch than the library's static array holds */
 } coop_status_t;
 
 /* Version of this ABI; bumped on any incompatible change. */
-#define COOP_ABI_VERSION 3
+#define COOP_ABI_VERSION 4
 int coop_abi_version(void);
 
 /* Human-readable text for a status code (static storage, never NULL). */
@@ -157,6 +159,41 @@ coop_status_t coop_window_search(const uint64_t *size, const uint64_t *cost,
                                  const uint64_t *req_sizes, const uint64_t *req_offsets,
                                  uint64_t num_requests, coop_window_t *out,
                                  void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * coop_window_search_static -- coop_window_search for callers that cannot
+ * allocate device memory: code under HIP graph capture that may not call
+ * hipMalloc, tight serving loops, harnesses that forbid allocation.  Same
+ * arguments, results and status codes as coop_window_search, without the
+ * workspace: the cross-workgroup state (partial keys, arrival counters, the
+ * chunk queue and the graph tag word) lives in a static device array of the
+ * library, 32 MiB on every GPU the library runs on, held until the process
+ * ends.  Its address is looked up on the first call on a device (with the
+ * stream's device current) and kept; the call then allocates nothing and
+ * never synchronises.
+ *
+ * The array holds coop_window_search_static_capacity() bytes of workspace.
+ * The search is planned with the largest partial-key budget whose workspace
+ * fits (fewer partial slots only make the kernel's chunks longer; the
+ * results are the same).  A batch that fits no plan -- roughly more than
+ * 500,000 requests, or more than 4 million snapshots -- is rejected with
+ * COOP_ERR_TOO_LARGE before anything is enqueued.  The debug checks are not
+ * run (they copy the batch back to host memory).
+ *
+ * Every call on one GPU shares that GPU's array, and the array keeps the
+ * last call's contents (no call needs it cleared: every counter carries the
+ * call's tag).  Calls that overlap in time on one GPU -- on different
+ * streams, or from different host threads without ordering -- race on it
+ * and give undefined results; calls ordered on one stream are safe.
+ */
+size_t coop_window_search_static_capacity(void);
+
+coop_status_t coop_window_search_static(const uint64_t *size, const uint64_t *cost,
+                                        const uint8_t *kind, uint64_t num_blocks,
+                                        const uint64_t *seg_offsets, uint64_t num_segments,
+                                        const uint64_t *req_sizes,
+                                        const uint64_t *req_offsets, uint64_t num_requests,
+                                        coop_window_t *out, void *stream);
 
 /*
  * First fit (section 2.1; Algorithm 1's find_free_block_not_less_than, the

@@ -26,7 +26,8 @@ INFEASIBLE = -1  # int64 view of the all-ones sentinel
 POLICY_WINDOW, POLICY_GREEDY = 0, 1  # coop_replay's eviction policies
 
 _STATUS = {0: "ok", -1: "invalid argument", -2: "workspace missing or too small",
-           -3: "HIP launch failed", -4: "a run's byte or cost total exceeds 2^64 - 1"}
+           -3: "HIP launch failed", -4: "a run's byte or cost total exceeds 2^64 - 1",
+           -5: "the batch needs more than the library's static scratch"}
 
 _lib = None
 
@@ -73,6 +74,10 @@ def load_library():
                                 ctypes.c_int32, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.coop_replay.restype = ctypes.c_int
     lib.coop_window_search.restype = ctypes.c_int
+    lib.coop_window_search_static.argtypes = [vp, vp, vp, u64, vp, u64, vp, vp, u64, vp, vp]
+    lib.coop_window_search_static.restype = ctypes.c_int
+    lib.coop_window_search_static_capacity.argtypes = []
+    lib.coop_window_search_static_capacity.restype = sz
     lib.coop_window_search_real_workspace_size.argtypes = [u64, u64, u64, ctypes.POINTER(sz)]
     lib.coop_window_search_real_workspace_size.restype = ctypes.c_int
     lib.coop_window_search_real.argtypes = [vp, vp, vp, u64, vp, u64, vp, vp, u64, vp, vp, vp,
@@ -182,6 +187,46 @@ def window_search(size, cost, kind, seg_offsets, req_sizes, req_offsets, *,
     (start, end, cost).  Asynchronous on `stream` like any torch op."""
     ws = WindowSearch(size, cost, kind, seg_offsets, req_sizes, req_offsets, out, workspace)
     return ws(stream)
+
+
+def window_search_static(size, cost, kind, seg_offsets, req_sizes, req_offsets, *,
+                         out: Optional[torch.Tensor] = None,
+                         stream: Optional[int] = None) -> torch.Tensor:
+    """coop_window_search_static: the batched search without a workspace
+    (its state lives in the library's static device array, shared by every
+    call on the GPU).  Returns int64 (Q, 3); with `out` given, nothing is
+    allocated on the device."""
+    device = size.device
+    if device.type != "cuda":
+        raise ValueError("coop window search runs on the GPU; tensors are on "
+                         f"{device} (there is no CPU fallback)")
+    size = _u64_tensor(size, "size", device)
+    cost = _u64_tensor(cost, "cost", device)
+    if kind.dtype != torch.uint8 or kind.device != device or not kind.is_contiguous():
+        raise TypeError("kind must be a contiguous uint8 tensor on the same device")
+    seg_offsets = _u64_tensor(seg_offsets, "seg_offsets", device)
+    req_sizes = _u64_tensor(req_sizes, "req_sizes", device)
+    req_offsets = _u64_tensor(req_offsets, "req_offsets", device)
+    n, b1, q = size.numel(), seg_offsets.numel(), req_sizes.numel()
+    if cost.numel() != n or kind.numel() != n:
+        raise ValueError("size, cost and kind must have the same length")
+    if b1 < 1 or req_offsets.numel() != b1:
+        raise ValueError("seg_offsets and req_offsets need num_segments + 1 entries")
+    if out is None:
+        out = torch.empty((q, 3), dtype=torch.int64, device=device)
+    if out.shape != (q, 3) or out.dtype != torch.int64 or not out.is_contiguous():
+        raise ValueError("out must be a contiguous int64 (Q, 3) tensor")
+    if stream is None:
+        stream = torch.cuda.current_stream(device).cuda_stream
+    _check(load_library().coop_window_search_static(
+        _ptr(size), _ptr(cost), _ptr(kind), n, _ptr(seg_offsets), b1 - 1, _ptr(req_sizes),
+        _ptr(req_offsets), q, _ptr(out), stream))
+    return out
+
+
+def static_capacity() -> int:
+    """Workspace bytes coop_window_search_static's static array holds."""
+    return int(load_library().coop_window_search_static_capacity())
 
 
 def real_workspace_size(num_blocks: int, num_segments: int, num_requests: int) -> int:
@@ -417,5 +462,6 @@ def to_device(pools, device="cuda"):
 __all__ = ["COOP_EVICTABLE", "COOP_FREE", "COOP_PINNED", "CoopError", "FirstFit",
            "INFEASIBLE", "LIBRARY", "POLICY_GREEDY", "POLICY_WINDOW", "Replay", "WindowSearch",
            "first_fit", "first_fit_workspace_size", "load_library", "plan_info",
-           "real_workspace_size", "replay_to_device", "replay_workspace_size", "to_device",
-           "window_search", "WindowSearchReal", "workspace_size"]
+           "real_workspace_size", "replay_to_device", "replay_workspace_size", "static_capacity",
+           "to_device", "window_search", "window_search_static", "WindowSearchReal",
+           "workspace_size"]

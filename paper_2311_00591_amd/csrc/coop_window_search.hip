@@ -71,6 +71,7 @@
 
 #include <atomic>
 #include <chrono>
+#include <mutex>
 #include <stdint.h>
 
 #include "coop.h"
@@ -1409,7 +1410,8 @@ static_assert(kGridWGs < (1ull << kEpochShift), "tickets fit the counter");
 constexpr uint64_t kQueueMinChunk = 8;         // smaller shares: no queue
 constexpr uint64_t kQueueMaxSegments = 16384;  // every workgroup scans the offsets once
 
-bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests, Plan* pl) {
+bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests, Plan* pl,
+               uint64_t partial_budget = kPartialBudget) {
     if (num_segments > (1ull << 32) || num_blocks > (1ull << 60) || num_requests > (1ull << 40))
         return false;
     const uint64_t nv = (num_blocks >> kTileLog2) + num_segments;
@@ -1441,7 +1443,7 @@ bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests
     // chunks: the partial slots a request needs.  Past the budget, chunks
     // grow instead (fewer workgroups).
     const uint64_t T = ((num_blocks + kTile - 1) >> kTileLog2) + 1;  // tiles of one snapshot, at most
-    const uint64_t cap = kPartialBudget / num_requests > 2 ? kPartialBudget / num_requests : 2;
+    const uint64_t cap = partial_budget / num_requests > 2 ? partial_budget / num_requests : 2;
     if ((T + chunk - 1) / chunk + 1 > cap) {
         const uint64_t need = (T + cap - 2) / (cap - 1);
         if (need > chunk) chunk = need;
@@ -1510,6 +1512,7 @@ const char* coop_status_string(int status) {
         case COOP_ERR_WORKSPACE: return "workspace missing or too small";
         case COOP_ERR_HIP: return "HIP launch failed";
         case COOP_ERR_OVERFLOW: return "a run's byte or cost total exceeds 2^64 - 1";
+        case COOP_ERR_TOO_LARGE: return "the batch needs more than the library's static scratch";
         default: return "unknown status";
     }
 }
@@ -1552,21 +1555,18 @@ coop_status_t coop_window_search(const uint64_t* size, const uint64_t* cost, con
 
 }  // extern "C"
 
-coop_status_t coop_window_search_enqueue(const uint64_t* size, const uint64_t* cost,
-                                         const uint8_t* kind, uint64_t num_blocks,
-                                         const uint64_t* seg_offsets, uint64_t num_segments,
-                                         const uint64_t* req_sizes, const uint64_t* req_offsets,
-                                         uint64_t num_requests, coop_window_t* out,
-                                         void* workspace, size_t workspace_bytes, void* stream,
-                                         bool check) {
-    if (num_requests == 0) return COOP_OK;
-    if (num_segments == 0) return COOP_ERR_INVALID;
-    if (num_blocks && (!size || !cost || !kind)) return COOP_ERR_INVALID;
-    if (!seg_offsets || !req_offsets || !req_sizes || !out) return COOP_ERR_INVALID;
-    Plan pl;
-    if (!make_plan(num_blocks, num_segments, num_requests, &pl)) return COOP_ERR_INVALID;
-    if (!workspace || workspace_bytes < pl.bytes) return COOP_ERR_WORKSPACE;
-    hipStream_t s = static_cast<hipStream_t>(stream);
+namespace {
+
+// Validates the host-visible arguments, runs the debug checks when asked,
+// and enqueues the search of a batch under plan pl.  The workspace holds
+// the plan's partial keys, arrival counters and queue word; tag_word is
+// the word a captured call's tags come from (inside the workspace, or at a
+// fixed place of the static scratch).
+coop_status_t launch_search(const Plan& pl, const uint64_t* size, const uint64_t* cost,
+                            const uint8_t* kind, uint64_t num_blocks, const uint64_t* seg_offsets,
+                            uint64_t num_segments, const uint64_t* req_sizes,
+                            const uint64_t* req_offsets, uint64_t num_requests, coop_window_t* out,
+                            void* workspace, uint64_t* tag_word, hipStream_t s, bool check) {
     if (check) {
         const coop_host::Batch b{size, cost, kind, num_blocks, seg_offsets, num_segments,
                                  req_offsets, num_requests, true};
@@ -1605,8 +1605,8 @@ coop_status_t coop_window_search_enqueue(const uint64_t* size, const uint64_t* c
                   (static_cast<double>(num_blocks) / kTile + static_cast<double>(num_segments));
 
     // A captured launch replays with the arguments it was recorded with, so
-    // its tag cannot come from the host: it comes from the workspace's tag
-    // word, advanced by a kernel recorded just before.
+    // its tag cannot come from the host: it comes from the tag word,
+    // advanced by a kernel recorded just before.
     hipStreamCaptureStatus capture = hipStreamCaptureStatusNone;
     if (hipStreamIsCapturing(s, &capture) != hipSuccess) return COOP_ERR_HIP;
     if (capture == hipStreamCaptureStatusNone) {
@@ -1615,16 +1615,128 @@ coop_status_t coop_window_search_enqueue(const uint64_t* size, const uint64_t* c
         P.qtag = queue_tag(P.epoch);
         P.tag_word = nullptr;
     } else {
-        uint64_t* word = P.queue + 1;
-        hipLaunchKernelGGL(window_tag_kernel, dim3(1), dim3(1), 0, s, word);
+        hipLaunchKernelGGL(window_tag_kernel, dim3(1), dim3(1), 0, s, tag_word);
         if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
         P.epoch = g_salt;
         P.qtag = 0;
-        P.tag_word = word;
+        P.tag_word = tag_word;
     }
 
     hipLaunchKernelGGL(coop_window_search_kernel, dim3(static_cast<uint32_t>(pl.grid)),
                        dim3(kThreads), 0, s, P);
     if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
     return COOP_OK;
+}
+
+// Host arguments every entry point checks before planning.
+coop_status_t check_args(const uint64_t* size, const uint64_t* cost, const uint8_t* kind,
+                         uint64_t num_blocks, const uint64_t* seg_offsets, uint64_t num_segments,
+                         const uint64_t* req_sizes, const uint64_t* req_offsets,
+                         coop_window_t* out) {
+    if (num_segments == 0) return COOP_ERR_INVALID;
+    if (num_blocks && (!size || !cost || !kind)) return COOP_ERR_INVALID;
+    if (!seg_offsets || !req_offsets || !req_sizes || !out) return COOP_ERR_INVALID;
+    return COOP_OK;
+}
+
+// ---------------------------------------------------------------------------
+// The search without a workspace argument: its cross-workgroup state lives
+// in a fixed device array of the library, one per GPU.
+// ---------------------------------------------------------------------------
+
+constexpr size_t kScratchBytes = size_t{32} << 20;
+// The first 256 bytes hold the tag word of captured calls (at the same place
+// whatever the plan); the plan's workspace follows.
+constexpr size_t kScratchTagBytes = 256;
+static __device__ __align__(256) uint64_t scratch[kScratchBytes / sizeof(uint64_t)];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of `scratch` on the stream's device.  Host code may
+// never use the array's name as an address (it names a host-side stand-in);
+// the address is looked up once per device, with that device current, and
+// kept.
+coop_status_t scratch_address(hipStream_t s, void** ptr) {
+    int dev = 0, cur = 0;
+    if (hipGetDevice(&cur) != hipSuccess) return COOP_ERR_HIP;
+    if (hipStreamGetDevice(s, &dev) != hipSuccess) return COOP_ERR_HIP;
+    if (dev < 0 || dev >= kMaxDevices) return COOP_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        if (dev != cur && hipSetDevice(dev) != hipSuccess) return COOP_ERR_HIP;
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (dev != cur) (void)hipSetDevice(cur);
+        if (e != hipSuccess || p == nullptr) {
+            (void)hipGetLastError();
+            return COOP_ERR_HIP;
+        }
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    return COOP_OK;
+}
+
+// The plan for the static scratch: the largest partial-key budget (a power
+// of two) whose workspace fits; false when none does.
+bool static_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests, Plan* pl) {
+    for (uint64_t budget = kPartialBudget; budget >= 2; budget >>= 1) {
+        if (!make_plan(num_blocks, num_segments, num_requests, pl, budget)) return false;
+        if (pl->bytes <= kScratchBytes - kScratchTagBytes) return true;
+    }
+    return false;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t coop_window_search_static_capacity(void) { return kScratchBytes - kScratchTagBytes; }
+
+coop_status_t coop_window_search_static(const uint64_t* size, const uint64_t* cost,
+                                        const uint8_t* kind, uint64_t num_blocks,
+                                        const uint64_t* seg_offsets, uint64_t num_segments,
+                                        const uint64_t* req_sizes, const uint64_t* req_offsets,
+                                        uint64_t num_requests, coop_window_t* out,
+                                        void* stream) {
+    if (num_requests == 0) return COOP_OK;
+    coop_status_t rc = check_args(size, cost, kind, num_blocks, seg_offsets, num_segments,
+                                  req_sizes, req_offsets, out);
+    if (rc != COOP_OK) return rc;
+    Plan pl;
+    if (!make_plan(num_blocks, num_segments, num_requests, &pl)) return COOP_ERR_INVALID;
+    if (!static_plan(num_blocks, num_segments, num_requests, &pl)) return COOP_ERR_TOO_LARGE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    void* base = nullptr;
+    rc = scratch_address(s, &base);
+    if (rc != COOP_OK) return rc;
+    uint64_t* tag_word = static_cast<uint64_t*>(base);
+    void* workspace = static_cast<char*>(base) + kScratchTagBytes;
+    return launch_search(pl, size, cost, kind, num_blocks, seg_offsets, num_segments, req_sizes,
+                         req_offsets, num_requests, out, workspace, tag_word, s, false);
+}
+
+}  // extern "C"
+
+coop_status_t coop_window_search_enqueue(const uint64_t* size, const uint64_t* cost,
+                                         const uint8_t* kind, uint64_t num_blocks,
+                                         const uint64_t* seg_offsets, uint64_t num_segments,
+                                         const uint64_t* req_sizes, const uint64_t* req_offsets,
+                                         uint64_t num_requests, coop_window_t* out,
+                                         void* workspace, size_t workspace_bytes, void* stream,
+                                         bool check) {
+    if (num_requests == 0) return COOP_OK;
+    const coop_status_t rc = check_args(size, cost, kind, num_blocks, seg_offsets, num_segments,
+                                        req_sizes, req_offsets, out);
+    if (rc != COOP_OK) return rc;
+    Plan pl;
+    if (!make_plan(num_blocks, num_segments, num_requests, &pl)) return COOP_ERR_INVALID;
+    if (!workspace || workspace_bytes < pl.bytes) return COOP_ERR_WORKSPACE;
+    uint64_t* tag_word = reinterpret_cast<uint64_t*>(static_cast<char*>(workspace) + pl.part_bytes) +
+                         pl.slices * num_segments + 1;
+    return launch_search(pl, size, cost, kind, num_blocks, seg_offsets, num_segments, req_sizes,
+                         req_offsets, num_requests, out, workspace, tag_word,
+                         static_cast<hipStream_t>(stream), check);
 }

@@ -167,3 +167,29 @@ def test_real_search_validates_host_arguments():
     assert call(wsb=1) == -2
     assert coop.real_workspace_size(8, 1, 1) > 0
     assert coop.real_workspace_size(8, 1, 0) == 0
+
+
+def test_static_entry_validates_and_bounds_its_scratch():
+    """coop_window_search_static: the host checks and the size limit come
+    before the scratch lookup or any launch, so no GPU is touched."""
+    lib = coop.load_library()
+    nz = 16
+
+    def call(n=4, B=1, Q=1, **null):
+        a = dict(size=nz, cost=nz, kind=nz, seg=nz, req=nz, roff=nz, out=nz)
+        a.update(null)
+        return lib.coop_window_search_static(a["size"], a["cost"], a["kind"], n, a["seg"], B,
+                                             a["req"], a["roff"], Q, a["out"], None)
+
+    assert coop.static_capacity() == (32 << 20) - 256
+    assert call(Q=0, seg=None) == 0
+    for name in ("size", "cost", "kind", "seg", "req", "roff", "out"):
+        assert call(**{name: None}) == -1, name
+    assert call(B=0) == -1
+    assert call(B=1 << 40) == -1
+    # two partial keys of 32 bytes per request no longer fit
+    assert call(Q=1 << 20) == -5
+    assert call(n=1 << 24, B=1 << 23, Q=1 << 23) == -5
+    assert lib.coop_status_string(-5) == coop._STATUS[-5].encode()
+    # a batch that fits with the full partial-key budget is planned as usual
+    assert coop.workspace_size(66_267_909, 4096, 16384) > coop.static_capacity()
