@@ -318,6 +318,17 @@ struct Params {
     uint32_t pc;           // partial slots per request (at most 2^23)
     uint64_t epoch;        // this call's tag on the arrival tickets
     const uint64_t* tag_word;  // captured calls: the workspace word the tags come from
+    // Tile records (totals of tile p >= 1 of every snapshot, written while
+    // staging): bytes of all its blocks, cost of its evictable blocks and its
+    // pinned count, at index (seg[b] >> kTileLog2) + p - 1.
+    uint64_t* rec_p;
+    uint64_t* rec_c;
+    uint32_t* rec_r;
+    // Deferred jobs: chunk parts of jobs with windows that run past the tile
+    // after the staged one, finished by coop_window_long_kernel.
+    uint64_t* defer_word;  // queue tag << 32 | entries
+    uint4* entries;        // {first unit, end unit, g, G}
+    uint32_t defer_cap;
     uint32_t slices_log2;  // request slices (a power of two): slice y takes y, y + slices, ...
     double inv_slope;      // guess of b per tile id, for the first snapshot lookup
 };
@@ -362,6 +373,7 @@ struct Smem {
     Key slot[kWaves];   // answers of wavefronts that share a request
     uint64_t slot_s[kWaves];
     uint64_t claim;     // a chunk claimed from the queue, for every wavefront
+    uint32_t defer_mark;  // the mark (hi - 1) of the last job a wavefront deferred
 };
 
 __device__ __forceinline__ uint64_t first_id(uint64_t b, uint64_t seg_b) {
@@ -433,6 +445,7 @@ __device__ __forceinline__ void cursor_advance(const Params& P, uint64_t v, Curs
 // access.
 struct Job {
     uint32_t u, y, b;  // unit, slice, snapshot (b < num_segments <= 2^32)
+    uint32_t lo, hi;   // the units of (b, y) in the current chunk; hi - 1 marks the job
     uint64_t s0, s1, q0, R, K, tiles, p;
     uint32_t g, G;     // at most pc
     bool first, last, direct;
@@ -469,6 +482,8 @@ __device__ bool next_job(const Params& P, Cursor& c, bool& have_cursor, uint64_t
         const uint64_t lo = ub > u_begin ? ub : u_begin;
         const uint64_t hi = ub + tiles < u_end ? ub + tiles : u_end;
         job.u = u;
+        job.lo = static_cast<uint32_t>(lo);
+        job.hi = static_cast<uint32_t>(hi);
         job.y = y;
         job.b = c.b;
         job.s0 = s0;
@@ -734,18 +749,30 @@ __device__ __forceinline__ uint32_t pending_start(const Smem& sm, bool packed, u
     return wave_lower_bound(i0, nA, lane, [&](uint32_t i) { return xend - sm.x[i] < S; });
 }
 
-// Finishes the pending starts [cur, nA): all lie in the staged region's last
-// run, which goes on at global block pos, where the run's prefixes are cq
-// (bytes) and cc (cost).  The wavefront walks the run 64 blocks at a time
-// (one per lane, wavefront prefix sums, the chunk kept in registers); each
-// chunk resolves a prefix of the pending starts, 64 at a time, since their
-// shortest ends are monotone.  Candidates fold into best / best_end (end
-// snapshot-local).
-__device__ void stream_pass(const Params& P, const Smem& sm, uint32_t lane, uint32_t cur, uint32_t nA,
-                            uint64_t pos, uint64_t s0, uint64_t s1, uint64_t cq, uint64_t cc,
-                            uint64_t vmask, uint64_t S, Cand& best, uint64_t& best_end) {
-    while (cur < nA && pos < s1) {
-        const uint64_t left = s1 - pos;
+// Where a wavefront's walk through the run past the staged region stands:
+// the next block pos, the run's prefixes before it (bytes cq, cost cc; in
+// the staged region's frame), the first unresolved pending start, and
+// whether the run has closed (a pinned block or the snapshot end reached).
+struct WalkState {
+    uint64_t pos, cq, cc;
+    uint32_t cur;
+    bool closed;
+};
+
+// Resolves pending starts [ws.cur, nA): all lie in the staged region's last
+// run, which goes on at global block ws.pos.  The wavefront walks the run 64
+// blocks at a time (one per lane, wavefront prefix sums, the chunk kept in
+// registers) up to block lim; each chunk resolves a prefix of the pending
+// starts, 64 at a time, since their shortest ends are monotone.  Candidates
+// fold into best / best_end (end snapshot-local).  Stops when every pending
+// start is resolved, at lim, or where the run closes.
+__device__ void walk_pass(const Params& P, const Smem& sm, uint32_t lane, uint32_t nA, uint64_t lim,
+                          uint64_t s0, uint64_t s1, uint64_t vmask, uint64_t S, WalkState& ws,
+                          Cand& best, uint64_t& best_end) {
+    uint32_t cur = ws.cur;
+    uint64_t pos = ws.pos, cq = ws.cq, cc = ws.cc;
+    while (cur < nA && pos < lim) {
+        const uint64_t left = lim - pos;
         const uint32_t m = left < 64 ? static_cast<uint32_t>(left) : 64u;
         const bool in = lane < m;
         uint8_t kd = COOP_PINNED;
@@ -793,11 +820,19 @@ __device__ void stream_pass(const Params& P, const Smem& sm, uint32_t lane, uint
             cur += n;
             if (n < 64 || cur >= nA) break;
         }
-        if (fp < m) break;  // the run closes inside this chunk
+        if (fp < m) {  // the run closes inside this chunk
+            ws.closed = true;
+            break;
+        }
         cq = lastq;
         cc = lastc;
         pos += m;
     }
+    if (pos >= s1) ws.closed = true;
+    ws.cur = cur;
+    ws.pos = pos;
+    ws.cq = cq;
+    ws.cc = cc;
 }
 
 // What staging left in LDS.
@@ -807,6 +842,8 @@ struct TileState {
     uint32_t endrun; // R at the region end
     uint64_t xend;   // X at the region end
     uint64_t xcend;  // C at the region end
+    uint64_t tq, tc; // the tile's totals (without the halo): X (bytes + 2^50 per
+    uint32_t tr;     // pinned block, modulo 2^64), C, and the pinned count
 };
 
 template <int Ctrl, int RowMask>
@@ -909,6 +946,9 @@ __device__ __forceinline__ TileState stage_tile(Smem& sm, const TileGeom& tg, ui
     const uint64_t base_x = carry.q + wi.q - t.q, base_c = carry.c + wi.c - t.c;
 
     TileState ts;
+    ts.tq = tile_tot.q;
+    ts.tc = tile_tot.c;
+    ts.tr = tile_tot.r;
     ts.packed = (bigs & ((1u << kWaves) - 1)) == 0;
     if (ts.packed) {
         const bool use_halo = hm && !(bigs >> kWaves);
@@ -995,10 +1035,11 @@ __device__ __forceinline__ Key readlane_key(const Key& k, uint32_t lane) {
 }
 
 // Stores the workgroup's key for request q: the final result once the
-// workgroup has covered the whole snapshot alone, else its partial slot.
+// workgroup has covered the whole snapshot alone (and deferred nothing),
+// else its partial slot.
 __device__ __forceinline__ void store_answer(const Params& P, const Job& job, uint64_t q, const Key& k,
-                                             uint64_t S) {
-    if (job.last && job.direct) P.out[q] = to_window(k, S);
+                                             uint64_t S, bool deferred) {
+    if (job.last && job.direct && !deferred) P.out[q] = to_window(k, S);
     else store_key_device(P.part + q * P.pc + job.g, k);
 }
 
@@ -1035,6 +1076,8 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
     const uint32_t nt = tg.nt, end = ts.end;
     const uint64_t vmask = ts.packed ? kValMask : kNone;
     const bool open = tg.t0 + end < job.s1;  // the region's last run may go on
+    // walks past the staged region stop at the end of the next tile
+    const uint64_t lim = tg.t0 + 2ull * kTile < job.s1 ? tg.t0 + 2ull * kTile : job.s1;
     const uint64_t tasks = job.K * wpr;
     const uint32_t wl2 = static_cast<uint32_t>(__builtin_ctz(wpr));
     const uint32_t lanes = 64u * wpr;
@@ -1081,7 +1124,9 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
             sm.slot_s[vw] = S;
         }
     }
-    // ---- windows that leave the staged region (the region's last run goes on)
+    // ---- windows that leave the staged region (the region's last run goes
+    // on), walked up to the end of the next tile; windows that go further
+    // are left to coop_window_long_kernel, which is told by the job's mark
     uint64_t todo = __ballot(lane < held && pend < nt);
     while (todo) {
         const uint32_t n = static_cast<uint32_t>(__builtin_ctzll(todo));
@@ -1090,8 +1135,9 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
         const uint64_t S = readlane64(s_lane, wpr == 1 ? n : static_cast<uint32_t>(vw >> wl2));
         Cand best = cand_none();
         uint64_t best_end = 0;
-        stream_pass(P, sm, lane, readlane32(pend, n), nt, tg.t0 + end, job.s0, job.s1,
-                    ts.xend & vmask, ts.xcend, vmask, S, best, best_end);
+        WalkState ws{tg.t0 + end, ts.xend & vmask, ts.xcend, readlane32(pend, n), false};
+        walk_pass(P, sm, lane, nt, lim, job.s0, job.s1, vmask, S, ws, best, best_end);
+        if (ws.cur < nt && !ws.closed && lane == 0) sm.defer_mark = job.hi - 1;
         const Key k = wave_answer(best, best_end, tl, S);
         if (wpr == 1) {
             const Key a = min_key(readlane_key(acc, n), k);
@@ -1101,9 +1147,7 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
         }
     }
     if (wpr == 1) {
-        // results of the held tasks, one per lane
-        if (job.last && lane < held)
-            store_answer(P, job, request(w + static_cast<uint64_t>(kWaves) * lane), acc, s_lane);
+        // (results of the held tasks: after the barrier that ends the tile)
         // ---- tasks past 64 per wavefront: running keys in the partial slots
         for (uint64_t vw = w + 64ull * kWaves; vw < tasks; vw += kWaves) {
             const uint64_t q = request(vw);
@@ -1125,14 +1169,18 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
                 if (open) {
                     const uint32_t cur =
                         pending_start(sm, ts.packed, nt, ts.xend, ts.endrun, S, Sc, lane);
-                    if (cur < nt)
-                        stream_pass(P, sm, lane, cur, nt, tg.t0 + end, job.s0, job.s1, ts.xend & vmask,
-                                    ts.xcend, vmask, S, best, best_end);
+                    if (cur < nt) {
+                        WalkState ws{tg.t0 + end, ts.xend & vmask, ts.xcend, cur, false};
+                        walk_pass(P, sm, lane, nt, lim, job.s0, job.s1, vmask, S, ws, best, best_end);
+                        if (ws.cur < nt && !ws.closed && lane == 0) sm.defer_mark = job.hi - 1;
+                    }
                 }
             }
             Key k = wave_answer(best, best_end, tl, S);
             if (!job.first) k = min_key(load_key_device(P.part + q * P.pc + job.g), k);
-            if (lane == 0) store_answer(P, job, q, k, S);
+            // (a result of a snapshot covered by this workgroup alone is
+            // copied to out after the barrier that ends the tile)
+            if (lane == 0) store_key_device(P.part + q * P.pc + job.g, k);
         }
     }
     // (shared requests: the wavefronts' keys stay in sm.slot for
@@ -1145,7 +1193,7 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
 // ends the tile, so every key is in place; the next tile's keys are written
 // only after the next staging barriers, which wavefront 0 reaches after this.
 __device__ __forceinline__ void reduce_shared(const Params& P, const Smem& sm, const Job& job,
-                                              uint32_t wpr, uint32_t tid, Key& acc) {
+                                              uint32_t wpr, uint32_t tid, Key& acc, bool deferred) {
     if (tid >= job.K) return;
     const uint32_t wl2 = static_cast<uint32_t>(__builtin_ctz(wpr));
     Key k = sm.slot[tid << wl2];
@@ -1153,7 +1201,7 @@ __device__ __forceinline__ void reduce_shared(const Params& P, const Smem& sm, c
     acc = job.first ? k : min_key(acc, k);
     if (job.last)
         store_answer(P, job, job.q0 + job.y + (static_cast<uint64_t>(tid) << P.slices_log2), acc,
-                     sm.slot_s[tid << wl2]);
+                     sm.slot_s[tid << wl2], deferred);
 }
 
 // After the last tile of (b, y) in the current chunk, when other chunks
@@ -1290,20 +1338,75 @@ __device__ __forceinline__ bool find_job(const Params& P, Smem& sm, uint32_t tid
     }
 }
 
+// A call replayed from a graph: its tags come from the tag word, advanced by
+// the kernel before the search on the stream, so every workgroup (of both
+// search kernels) reads the same value; P.epoch holds a per-process salt.
+__device__ __forceinline__ void graph_tags(Params& P) {
+    if (!P.tag_word) return;
+    const uint64_t t = __hip_atomic_load(P.tag_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    P.epoch = kGraphTag | ((t * kTagOdd + P.epoch) & kTagMask);
+    P.qtag = queue_tag(P.epoch);
+}
+
+// The totals of tile p >= 1 of a snapshot (one thread): bytes of all its
+// blocks (X without the 2^50 per pinned block), cost of its evictable blocks
+// and its pinned count.  Index (s0 >> kTileLog2) + p - 1 is below
+// floor(s1 / kTile) <= floor(num_blocks / kTile), and the index ranges of two
+// snapshots do not overlap: every tile past a snapshot's first has a slot of
+// its own.
+__device__ __forceinline__ void write_record(const Params& P, const Job& job, const TileState& ts) {
+    const uint64_t idx = (job.s0 >> kTileLog2) + job.p - 1;
+    if (idx >= (P.num_blocks >> kTileLog2)) return;  // (not reached with valid offsets)
+    P.rec_p[idx] = ts.tq - (static_cast<uint64_t>(ts.tr) << kValBits);
+    P.rec_c[idx] = ts.tc;
+    P.rec_r[idx] = ts.tr;
+}
+
+// After the last tile of a job with one wavefront per request: the held
+// tasks' keys (lane n of wavefront w: request w + kWaves * n) go to out, or
+// to the partial slot when other chunks hold tiles of the snapshot or a
+// wavefront deferred windows; keys of tasks past 64 per wavefront, kept in
+// the partial slots, are copied to out when the workgroup covered the whole
+// snapshot alone and deferred nothing.
+__device__ __forceinline__ void finish_held(const Params& P, const Job& job, uint32_t tid, const Key& acc,
+                                            uint64_t s_lane, bool deferred) {
+    const uint32_t lane = tid & 63u;
+    const uint32_t w = uniform(tid >> 6);
+    const uint64_t mine = job.K > w ? (job.K - w + kWaves - 1) / kWaves : 0;
+    const uint32_t held = mine < 64 ? static_cast<uint32_t>(mine) : 64u;
+    if (lane < held)
+        store_answer(P, job, job.q0 + job.y + ((w + static_cast<uint64_t>(kWaves) * lane) << P.slices_log2),
+                     acc, s_lane, deferred);
+    if (job.direct && !deferred && lane == 0) {
+        // the same lane stored these slots during the requests
+        for (uint64_t vw = w + 64ull * kWaves; vw < job.K; vw += kWaves) {
+            const uint64_t q = job.q0 + job.y + (vw << P.slices_log2);
+            P.out[q] = to_window(load_key_device(P.part + q * P.pc + job.g), ld_const(P.req_size, q));
+        }
+    }
+}
+
+// Appends the job's part of the chunk (its units, g and G) to the deferred
+// list (one thread).  The list's word carries the call's queue tag, so the
+// first append of a call restarts the count.
+__device__ void defer_job(const Params& P, const Job& job) {
+    uint64_t old = __hip_atomic_load(P.defer_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    uint64_t want;
+    do {
+        want = (old >> 32) == P.qtag ? old + 1 : (static_cast<uint64_t>(P.qtag) << 32) | 1ull;
+    } while (!__hip_atomic_compare_exchange_strong(P.defer_word, &old, want, __ATOMIC_RELAXED,
+                                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+    const uint64_t idx = (want & 0xffffffffull) - 1;
+    if (idx < P.defer_cap) P.entries[idx] = make_uint4(job.lo, job.hi, job.g, job.G);
+}
+
 __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params Pin) {
     __shared__ Smem sm;
     __shared__ uint32_t last_flag;
     const uint32_t tid = threadIdx.x;
     const uint32_t w = uniform(tid >> 6);
     Params P = Pin;
-    if (P.tag_word) {
-        // A call replayed from a graph: the tag word was advanced by the
-        // kernel before this one on the stream, so every workgroup reads the
-        // same value; P.epoch holds a per-process salt.
-        const uint64_t t = __hip_atomic_load(P.tag_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        P.epoch = kGraphTag | ((t * kTagOdd + P.epoch) & kTagMask);
-        P.qtag = queue_tag(P.epoch);
-    }
+    graph_tags(P);
     // The queue, when there is one: workgroup 0 stamps this call's tag; claims
     // that reach the word before the stamp see an old tag and try again.
     // Queued chunks are sized from the snapshots' tile counts, the same in
@@ -1320,6 +1423,7 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
         P.nchunks = P.grid + (static_cast<uint64_t>(P.units) - P.u1 + P.c2 - 1) / P.c2;
         reserve = kQEmpty;
     }
+    if (tid == 0) sm.defer_mark = kNone32;  // read after the barriers to come
     Walk wk;
     walk_chunk(P, blockIdx.x, wk);
     Cursor cur;
@@ -1372,14 +1476,201 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
         // ---- prefetch the next tile
         const TileGeom tn = has_next ? tile_geom(next) : TileGeom{tg.t0, 0u, 0u, 0u};
         issue_loads(P, tn, t, regs);
+        // ---- the tile's record, for jumps over it by coop_window_long_kernel
+        if (job.y == 0 && job.p != 0 && t == 0) write_record(P, job, ts);
         // ---- 2./3. the requests
         tile_requests(P, sm, job, tg, ts, wpr, t, acc, s_lane);
         __syncthreads();  // LDS is restaged next
-        if (wpr > 1) reduce_shared(P, sm, job, wpr, t, acc);
-        if (job.last && !job.direct) combine_partials(P, job, t, last_flag);
+        // a job some wavefront deferred keeps its keys in the partial slots
+        const bool deferred = job.last && sm.defer_mark == job.hi - 1;
+        if (wpr == 1 && job.last) finish_held(P, job, t, acc, s_lane, deferred);
+        if (wpr > 1) reduce_shared(P, sm, job, wpr, t, acc, deferred);
+        if (job.last) {
+            if (deferred) {
+                if (t == 0) defer_job(P, job);
+            } else if (!job.direct) {
+                combine_partials(P, job, t, last_flag);
+            }
+        }
         if (!has_next) break;
         job = next;
         tg = tn;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Windows longer than the staged tile and the next one
+// ---------------------------------------------------------------------------
+
+// Resolves the pending starts [cur, nA) of a staged tile whatever the length
+// of their windows (a whole wavefront).  From the region end, the run is
+// crossed tile by tile: a jump adds up the records of 64 tiles at a time and
+// skips every tile (or the unstaged rest of the tile after the staged one)
+// that holds no pinned block and does not reach S bytes for the first
+// pending start; the tile where that start's window ends, or where the run
+// closes, is then walked 64 blocks at a time (walk_pass), which resolves the
+// pending starts whose windows end there.  Then the next jump.  Each
+// pending start is resolved once; the walks cover only tiles where windows
+// end, so the cost is O(tiles of the run / 64) record loads plus the blocks
+// of the tiles holding ends, not the length of the run per tile.
+__device__ void long_pass(const Params& P, const Smem& sm, uint32_t lane, uint32_t cur, uint32_t nA,
+                          const Job& job, const TileGeom& tg, const TileState& ts, uint64_t vmask,
+                          uint64_t S, Cand& best, uint64_t& best_end) {
+    const uint64_t a = job.s0 & ~7ull;                   // tile k of the snapshot starts at a + k * kTile
+    const uint64_t rbase = (job.s0 >> kTileLog2) - 1;    // record of tile k >= 1: rbase + k
+    WalkState ws{tg.t0 + ts.end, ts.xend & vmask, ts.xcend, cur, false};
+    // the staged halo: the first blocks of tile p + 1, already in cq / cc
+    uint64_t hq = 0, hc = 0;
+    uint32_t hr = 0;
+    if (ts.end > tg.nt) {
+        const uint64_t d = ts.xend - sm.x[tg.nt];
+        hq = d & kValMask;
+        hr = static_cast<uint32_t>(d >> kValBits);
+        hc = ts.xcend - sm.xc[tg.nt];
+    }
+    bool jump = true;  // at the region end, then at every tile boundary
+    while (ws.cur < nA && !ws.closed && ws.pos < job.s1) {
+        const uint64_t k = (ws.pos - a) >> kTileLog2;  // the tile holding pos (k >= p + 1)
+        if (jump) {
+            const uint64_t base = sm.x[ws.cur] & vmask;  // bytes before the first pending start
+            const bool mid = ws.pos != a + (k << kTileLog2);  // pos inside tile p + 1, after the halo
+            for (uint64_t kk = k;; kk += 64) {
+                const uint64_t kt = kk + lane;
+                const bool inb = kt < job.tiles;
+                uint64_t rq = 0, rc = 0;
+                uint32_t rr = 1;  // past the snapshot's last tile: a wall
+                if (inb) {
+                    rq = P.rec_p[rbase + kt];
+                    rc = P.rec_c[rbase + kt];
+                    rr = P.rec_r[rbase + kt];
+                }
+                if (mid && kk == k && lane == 0) {
+                    rq -= hq;
+                    rc -= hc;
+                    rr -= hr;
+                }
+                Sums sm_{rq, rc, rr};
+                wave_inclusive_sum(sm_);  // totals through tile kt
+                // the first tile that holds a pinned block or reaches S bytes
+                const bool stop = !inb || sm_.r != 0 || ws.cq + sm_.q - base >= S;
+                const uint64_t m = __ballot(stop);
+                const uint32_t f = m ? static_cast<uint32_t>(__builtin_ctzll(m)) : 64u;
+                if (f) {
+                    ws.cq += readlane64(sm_.q, f - 1);
+                    ws.cc += readlane64(sm_.c, f - 1);
+                    const uint64_t np = a + ((kk + f) << kTileLog2);
+                    ws.pos = np < job.s1 ? np : job.s1;
+                }
+                if (f < 64) break;
+            }
+            if (ws.pos >= job.s1) break;  // the run ends at the snapshot end below S
+        }
+        // walk the tile holding pos up to its end
+        const uint64_t kw = (ws.pos - a) >> kTileLog2;
+        const uint64_t te = a + ((kw + 1) << kTileLog2);
+        walk_pass(P, sm, lane, nA, te < job.s1 ? te : job.s1, job.s0, job.s1, vmask, S, ws, best,
+                  best_end);
+        jump = true;
+    }
+}
+
+// One deferred entry: the units [lo, hi) of (snapshot b, slice y) that one
+// chunk held, and that chunk's partial slot g of G.  Every tile is staged
+// again, the pending starts of every request are resolved by long_pass and
+// folded into the request's partial slot (written by the search kernel);
+// then, as the search kernel would have: the result, or the arrival ticket
+// and the combine when the snapshot spans several chunks.
+__device__ void resolve_entry(const Params& P, Smem& sm, uint4 en, uint32_t& last_flag) {
+    const uint32_t tid = threadIdx.x;
+    const uint32_t lane = tid & 63u;
+    const uint32_t w = uniform(tid >> 6);
+    Cursor c;
+    Job job;
+    for (uint32_t u = en.x; u < en.y; ++u) {
+        const uint32_t y = static_cast<uint32_t>(div_magic(u, P.nv_magic));
+        const uint32_t v = u - y * P.num_virtual;
+        cursor_locate(P, v, c);
+        const uint64_t s1 = c.sb1 < P.num_blocks ? c.sb1 : P.num_blocks;
+        const uint64_t s0 = c.sb < s1 ? c.sb : s1;
+        const uint64_t q1 = c.rb1 < P.num_requests ? c.rb1 : P.num_requests;
+        const uint64_t q0 = c.rb < q1 ? c.rb : q1;
+        job.u = u;
+        job.lo = en.x;
+        job.hi = en.y;
+        job.y = y;
+        job.b = c.b;
+        job.s0 = s0;
+        job.s1 = s1;
+        job.q0 = q0;
+        job.R = q1 - q0;
+        job.K = job.R > y ? ((job.R - y - 1) >> P.slices_log2) + 1 : 0;
+        job.tiles = s1 > s0 ? (s1 - (s0 & ~7ull) + kTile - 1) >> kTileLog2 : 1;
+        job.p = v - first_id(c.b, c.sb);
+        job.g = en.z;
+        job.G = en.w;
+        job.first = u == en.x;
+        job.last = u + 1 == en.y;
+        job.direct = job.G == 1;
+        if (job.p >= job.tiles) continue;  // (not reached: the entry names the job's tiles)
+        const TileGeom tg = tile_geom(job);
+        TileRegs regs;
+        issue_loads(P, tg, tid, regs);
+        const TileState ts = stage_tile(sm, tg, tid, regs);
+        const uint32_t nt = tg.nt;
+        const bool open = tg.t0 + ts.end < job.s1;
+        const uint64_t vmask = ts.packed ? kValMask : kNone;
+        const uint64_t tl = tg.t0 - job.s0;
+        if (open && nt != 0) {
+            for (uint64_t vw = w; vw < job.K; vw += kWaves) {
+                const uint64_t q = job.q0 + job.y + (vw << P.slices_log2);
+                const uint64_t S = ld_const(P.req_size, q);
+                if (S == 0) continue;
+                const uint64_t Sc = S < (1ull << kValBits) ? S : (1ull << kValBits);
+                const uint32_t cur = pending_start(sm, ts.packed, nt, ts.xend, ts.endrun, S, Sc, lane);
+                if (cur >= nt) continue;
+                Cand best = cand_none();
+                uint64_t best_end = 0;
+                long_pass(P, sm, lane, cur, nt, job, tg, ts, vmask, S, best, best_end);
+                const Key k = wave_answer(best, best_end, tl, S);
+                if (lane == 0 && k.start != kNone) {
+                    // this lane alone reads and writes the slot of request q
+                    Key* slot = P.part + q * P.pc + job.g;
+                    store_key_device(slot, min_key(load_key_device(slot), k));
+                }
+            }
+        }
+        __syncthreads();  // LDS is restaged next
+    }
+    if (job.direct) {
+        if (lane == 0) {
+            for (uint64_t vw = w; vw < job.K; vw += kWaves) {
+                const uint64_t q = job.q0 + job.y + (vw << P.slices_log2);
+                P.out[q] = to_window(load_key_device(P.part + q * P.pc + job.g), ld_const(P.req_size, q));
+            }
+        }
+    } else {
+        combine_partials(P, job, tid, last_flag);
+    }
+    __syncthreads();  // last_flag and LDS are used by the next entry
+}
+
+// Finishes the jobs the search kernel deferred, after it on the stream (so
+// every tile record and partial key is in place).  With nothing deferred
+// (the list's word carries an older tag) every workgroup returns at once.
+__global__ __launch_bounds__(kThreads, 4) void coop_window_long_kernel(Params Pin) {
+    __shared__ Smem sm;
+    __shared__ uint32_t last_flag;
+    Params P = Pin;
+    graph_tags(P);
+    const uint64_t word = __hip_atomic_load(P.defer_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    uint64_t n = (word >> 32) == P.qtag ? (word & 0xffffffffull) : 0;
+    if (n > P.defer_cap) n = P.defer_cap;
+    for (uint64_t e = blockIdx.x; e < n; e += gridDim.x) {
+        const uint4 en = P.entries[e];
+        // (entries are written by this call's search kernel; the checks keep
+        // every access in bounds whatever the workspace holds)
+        if (en.x >= en.y || en.y > P.units || en.w == 0 || en.w > P.pc || en.z >= en.w) continue;
+        resolve_entry(P, sm, en, last_flag);
     }
 }
 
@@ -1398,12 +1689,18 @@ struct Plan {
     uint64_t nchunks;      // first chunks (one per workgroup) and queued chunks
     uint64_t pc;           // partial slots per request
     size_t part_bytes;     // partial keys
+    uint64_t defer_cap;    // deferred entries, at most
+    size_t off_defer;      // the deferred list's word, then its entries
+    size_t off_entries;
+    size_t off_rec;        // tile records: bytes, costs (u64), pinned counts (u32)
+    uint64_t num_rec;
     size_t bytes;          // total workspace
 };
 
 // Two workgroups of kThreads fit one CU (LDS); 256 CUs.  Workgroups past the
 // resident ones are still correct (nothing waits on another workgroup).
 constexpr uint64_t kGridWGs = 512;
+constexpr uint64_t kLongGridWGs = 512;  // workgroups of coop_window_long_kernel, at most
 constexpr uint64_t kMaxSlices = 256;
 constexpr uint64_t kSliceRequests = 512;  // requests per snapshot before slicing them
 static_assert(kGridWGs < (1ull << kEpochShift), "tickets fit the counter");
@@ -1433,6 +1730,8 @@ bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests
     while ((1ull << slices_log2) < slices) ++slices_log2;
     slices = 1ull << slices_log2;
     if (slices * nv >= (1ull << 32)) return false;
+    // deferred entries are counted in 32 bits
+    if ((num_blocks / 8186) * slices + slices * nv + kGridWGs >= (1ull << 32)) return false;
     pl->num_virtual = nv;
     pl->slices = slices;
     pl->slices_log2 = slices_log2;
@@ -1479,8 +1778,19 @@ bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests
     pl->nchunks = nchunks;
     pl->pc = pc;
     pl->part_bytes = (num_requests * pc * sizeof(Key) + 255) & ~static_cast<size_t>(255);
-    // then the arrival counters, the queue word and the tag word
-    pl->bytes = pl->part_bytes + (slices * num_segments + 2) * sizeof(uint64_t);
+    // then the arrival counters, the queue word, the tag word and the
+    // deferred list's word
+    pl->off_defer = pl->part_bytes + (slices * num_segments + 2) * sizeof(uint64_t);
+    pl->off_entries = (pl->off_defer + sizeof(uint64_t) + 15) & ~static_cast<size_t>(15);
+    // A job defers only when a window runs past the tile after the staged
+    // one, so its snapshot has at least three tiles (more than 8185
+    // blocks).  The chunk parts of such jobs number at most the jobs plus
+    // the chunk boundaries (each falls inside at most one job).
+    const uint64_t big = num_blocks / 8186 < num_segments ? num_blocks / 8186 : num_segments;
+    pl->defer_cap = nchunks + slices * big;
+    pl->num_rec = num_blocks >> kTileLog2;
+    pl->off_rec = pl->off_entries + pl->defer_cap * sizeof(uint4);
+    pl->bytes = pl->off_rec + pl->num_rec * (2 * sizeof(uint64_t) + sizeof(uint32_t));
     return true;
 }
 
@@ -1603,6 +1913,13 @@ coop_status_t launch_search(const Plan& pl, const uint64_t* size, const uint64_t
     P.slices_log2 = pl.slices_log2;
     P.inv_slope = static_cast<double>(num_segments) /
                   (static_cast<double>(num_blocks) / kTile + static_cast<double>(num_segments));
+    char* ws = static_cast<char*>(workspace);
+    P.defer_word = reinterpret_cast<uint64_t*>(ws + pl.off_defer);
+    P.entries = reinterpret_cast<uint4*>(ws + pl.off_entries);
+    P.defer_cap = static_cast<uint32_t>(pl.defer_cap);
+    P.rec_p = reinterpret_cast<uint64_t*>(ws + pl.off_rec);
+    P.rec_c = P.rec_p + pl.num_rec;
+    P.rec_r = reinterpret_cast<uint32_t*>(P.rec_c + pl.num_rec);
 
     // A captured launch replays with the arguments it was recorded with, so
     // its tag cannot come from the host: it comes from the tag word,
@@ -1623,6 +1940,11 @@ coop_status_t launch_search(const Plan& pl, const uint64_t* size, const uint64_t
     }
 
     hipLaunchKernelGGL(coop_window_search_kernel, dim3(static_cast<uint32_t>(pl.grid)),
+                       dim3(kThreads), 0, s, P);
+    if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
+    const uint64_t long_grid = pl.defer_cap < kLongGridWGs ? (pl.defer_cap ? pl.defer_cap : 1)
+                                                           : kLongGridWGs;
+    hipLaunchKernelGGL(coop_window_long_kernel, dim3(static_cast<uint32_t>(long_grid)),
                        dim3(kThreads), 0, s, P);
     if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
     return COOP_OK;

@@ -117,6 +117,91 @@ def test_runs_longer_than_the_staged_region():
     assert_parity(pools, gpu_search(pools), "long runs")
 
 
+def test_one_run_of_2_24_blocks_with_parameters_at_both_ends():
+    """The pool layout of section 3.5: unevictable parameters at the two ends
+    of the pool, everything between them one pinned-free run of about 2^24
+    blocks.  Requests from one block to the whole run: most tiles' windows
+    run far past the tile after theirs and are finished by the jumps over
+    tile records."""
+    _announce("one run of 2^24 blocks")
+    rng = np.random.default_rng(16)
+    n = 1 << 24
+    lo, hi = np.log(512.0), np.log(64.0 * (1 << 20))
+    size = ((np.exp(lo + rng.random(n) * (hi - lo)) + 511) // 512 * 512).astype(np.uint64)
+    kind = np.where(rng.random(n) < 0.2, 0, 1).astype(np.uint8)
+    kind[:37] = 2
+    kind[-53:] = 2
+    cost = np.floor(np.exp(rng.random(n) * np.log(1e12))).astype(np.uint64)
+    run = int(size[37:-53].sum())
+    mean = int(size.mean())
+    reqs = [512, mean, 100 * mean, 5000 * mean, 1 << 40, run // 16, run // 4, run // 2,
+            run - (1 << 30), run - 512, run, run + 1]
+    pools = _pools([(size, cost, kind)], [reqs])
+    got = gpu_search(pools)
+    assert_parity(pools, got, "one run of 2^24 blocks")
+    check_results(pools, got, sample=range(5))  # (whole-run windows take minutes in Python)
+
+
+def test_long_runs_mixed_batch():
+    """Snapshots of 1 to 30 tiles with few pinned blocks, one to nine
+    requests each (shared requests and one wavefront per request), windows
+    from one block to whole runs: jobs deferred whole, in part, split over
+    chunks and held by one workgroup."""
+    _announce("long runs, mixed batch")
+    rng = np.random.default_rng(17)
+    snaps, reqs = [], []
+    for s in range(40):
+        n = int(rng.integers(1, 30 * TILE))
+        size = (rng.integers(1, 64, size=n) * 512).astype(np.uint64)
+        kind = np.where(rng.random(n) < 0.2, 0, 1).astype(np.uint8)
+        if s % 3 == 0:
+            kind[:3] = 2
+            kind[-2:] = 2
+        elif s % 3 == 1:
+            kind[rng.integers(0, n, size=int(rng.integers(1, 5)))] = 2
+        if s % 5 == 0:  # large blocks first, small ones after
+            size[: n // 2] *= np.uint64(997)
+        cost = rng.integers(0, 10**6, size=n).astype(np.uint64)
+        snaps.append((size, cost, kind))
+        tot = int(size[kind < 2].sum())
+        r = [int(x) for x in rng.integers(1, max(2, tot), size=int(rng.integers(0, 5)))]
+        r += [tot // 2, tot, tot + 1, 1, 0][: int(rng.integers(1, 6))]
+        reqs.append(r)
+    pools = _pools(snaps, reqs)
+    got = gpu_search(pools)
+    assert_parity(pools, got, "long runs, mixed batch")
+    check_results(pools, got)
+
+
+def test_long_runs_with_more_than_64_requests_per_wavefront():
+    """A three-tile run with 20,000 requests among 40 one-request snapshots:
+    each wavefront holds more than 64 of the big snapshot's requests, whose
+    running keys live in the partial slots, and their long windows are
+    deferred."""
+    _announce("long runs, > 64 requests per wavefront")
+    rng = np.random.default_rng(18)
+    n = 3 * TILE + 1000
+    size = (rng.integers(1, 64, size=n) * 512).astype(np.uint64)
+    kind = np.where(rng.random(n) < 0.2, 0, 1).astype(np.uint8)
+    kind[0] = kind[-1] = 2
+    cost = rng.integers(0, 10**6, size=n).astype(np.uint64)
+    tot = int(size[1:-1].sum())
+    snaps = [(size, cost, kind)]
+    reqs = [[int(x) for x in rng.integers(1, tot + 2, size=20000)]]
+    for _ in range(40):
+        m = int(rng.integers(1, 100))
+        snaps.append(((rng.integers(1, 64, size=m) * 512).astype(np.uint64),
+                      rng.integers(0, 100, size=m).astype(np.uint64),
+                      rng.choice([0, 1, 1, 2], size=m).astype(np.uint8)))
+        reqs.append([int(rng.integers(1, 1 << 16))])
+    pools = _pools(snaps, reqs)
+    import paper_2311_00591_amd as coop
+    info = coop.plan_info(pools.num_blocks, pools.num_segments, pools.num_requests)
+    assert 20000 / info["slices"] > 512, info
+    got = gpu_search(pools)
+    assert_parity(pools, got, "long runs, > 64 requests per wavefront")
+
+
 def test_degenerate_snapshots():
     _announce("degenerate snapshots")
     z = np.zeros(0, dtype=np.uint64)
