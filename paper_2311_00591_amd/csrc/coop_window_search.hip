@@ -318,20 +318,43 @@ struct Params {
     uint32_t pc;           // partial slots per request (at most 2^23)
     uint64_t epoch;        // this call's tag on the arrival tickets
     const uint64_t* tag_word;  // captured calls: the workspace word the tags come from
-    // Tile records (totals of tile p >= 1 of every snapshot, written while
-    // staging): bytes of all its blocks, cost of its evictable blocks and its
-    // pinned count, at index (seg[b] >> kTileLog2) + p - 1.
-    uint64_t* rec_p;
-    uint64_t* rec_c;
-    uint32_t* rec_r;
-    // Deferred jobs: chunk parts of jobs with windows that run past the tile
-    // after the staged one, finished by coop_window_long_kernel.
-    uint64_t* defer_word;  // queue tag << 32 | entries
-    uint4* entries;        // {first unit, end unit, g, G}
-    uint32_t defer_cap;
+    uint32_t defer_cap;    // deferred entries, at most (the arrays: see Ext)
     uint32_t slices_log2;  // request slices (a power of two): slice y takes y, y + slices, ...
     double inv_slope;      // guess of b per tile id, for the first snapshot lookup
 };
+
+// The workspace after the queue word, laid out the same way by the host
+// (make_plan): the tag word, the deferred list's word (queue tag << 32 |
+// entries), the deferred entries {first unit, end unit, g, G} (16-byte
+// aligned), the tile records of tile p >= 1 of every snapshot at index
+// (seg[b] >> kTileLog2) + p - 1 (bytes of all its blocks, cost of its
+// evictable blocks, its pinned count, and the call tag that marks it
+// complete), written by coop_window_long_kernel, and one deferral bit per
+// partial slot (bit q * pc + g: request q left windows to
+// coop_window_long_kernel in its chunk part g).  Derived where needed rather
+// than passed, to keep the kernels' uniform state small.
+struct Ext {
+    uint64_t* defer_word;
+    uint4* entries;
+    uint64_t* rec_p;
+    uint64_t* rec_c;
+    uint64_t* rec_r;
+    uint64_t* rec_tag;
+    uint32_t* bits;
+};
+
+__device__ __forceinline__ Ext ext_of(const Params& P) {
+    Ext e;
+    e.defer_word = P.queue + 2;
+    e.entries = reinterpret_cast<uint4*>((reinterpret_cast<uintptr_t>(P.queue + 3) + 15) & ~uintptr_t{15});
+    e.rec_p = reinterpret_cast<uint64_t*>(e.entries + P.defer_cap);
+    const uint64_t nrec = P.num_blocks >> kTileLog2;
+    e.rec_c = e.rec_p + nrec;
+    e.rec_r = e.rec_c + nrec;
+    e.rec_tag = e.rec_r + nrec;
+    e.bits = reinterpret_cast<uint32_t*>(e.rec_tag + nrec);
+    return e;
+}
 
 // A read of an array the kernel never writes (offsets, request sizes)
 // through the constant address space: uniform indices then become scalar
@@ -771,17 +794,28 @@ __device__ void walk_pass(const Params& P, const Smem& sm, uint32_t lane, uint32
                           Cand& best, uint64_t& best_end) {
     uint32_t cur = ws.cur;
     uint64_t pos = ws.pos, cq = ws.cq, cc = ws.cc;
-    while (cur < nA && pos < lim) {
-        const uint64_t left = lim - pos;
-        const uint32_t m = left < 64 ? static_cast<uint32_t>(left) : 64u;
-        const bool in = lane < m;
-        uint8_t kd = COOP_PINNED;
-        uint64_t sz = 0, ct = 0;
-        if (in) {
-            kd = P.kind[pos + lane];
-            sz = P.size[pos + lane];
-            ct = P.cost[pos + lane];
+    // the blocks of the chunk at pos; the next chunk's are loaded before
+    // this one is processed
+    auto load = [&](uint64_t at, uint32_t m, uint32_t& kd, uint64_t& sz, uint64_t& ct) {
+        kd = COOP_PINNED;
+        sz = 0;
+        ct = 0;
+        if (lane < m) {
+            kd = P.kind[at + lane];
+            sz = P.size[at + lane];
+            ct = P.cost[at + lane];
         }
+    };
+    uint32_t m = pos < lim ? (lim - pos < 64 ? static_cast<uint32_t>(lim - pos) : 64u) : 0u;
+    uint32_t kd;
+    uint64_t sz, ct;
+    load(pos, m, kd, sz, ct);
+    while (cur < nA && pos < lim) {
+        const uint64_t npos = pos + m;
+        const uint32_t nm = npos < lim ? (lim - npos < 64 ? static_cast<uint32_t>(lim - npos) : 64u) : 0u;
+        uint32_t nkd;
+        uint64_t nsz, nct;
+        load(npos, nm, nkd, nsz, nct);
         const uint64_t pinned = __ballot(kd >= COOP_PINNED);
         const uint32_t fp = pinned ? static_cast<uint32_t>(__builtin_ctzll(pinned)) : 64u;  // <= m
         const bool valid = lane < fp;
@@ -791,7 +825,10 @@ __device__ void walk_pass(const Params& P, const Smem& sm, uint32_t lane, uint32
         const uint32_t lastl = fp ? fp - 1 : 0;
         const uint64_t lastq = fp ? readlane64(q, lastl) : cq;
         const uint64_t lastc = fp ? readlane64(c, lastl) : cc;
-        for (;;) {
+        // no window from the first pending start ends in this chunk: none
+        // from a later one does either (ends are monotone)
+        const bool none = fp == 0 || lastq - (sm.x[cur] & vmask) < S;
+        for (; !none;) {
             const uint32_t i = cur + lane;
             const bool act = i < nA;
             const uint32_t ii = act ? i : nA - 1;
@@ -826,7 +863,11 @@ __device__ void walk_pass(const Params& P, const Smem& sm, uint32_t lane, uint32
         }
         cq = lastq;
         cc = lastc;
-        pos += m;
+        pos = npos;
+        m = nm;
+        kd = nkd;
+        sz = nsz;
+        ct = nct;
     }
     if (pos >= s1) ws.closed = true;
     ws.cur = cur;
@@ -1057,6 +1098,14 @@ __device__ __forceinline__ Key wave_answer(const Cand& best, uint64_t best_end, 
 
 __device__ __forceinline__ Key min_key(const Key& a, const Key& b) { return key_less(b, a) ? b : a; }
 
+// Request q has windows past the walk's limit (one lane): its bit for the
+// chunk part, and the job's mark.
+__device__ __forceinline__ void defer_request(const Params& P, Smem& sm, const Job& job, uint64_t q) {
+    const uint64_t bit = q * P.pc + job.g;
+    atomicOr(ext_of(P).bits + (bit >> 5), 1u << (bit & 31u));
+    sm.defer_mark = job.hi - 1;
+}
+
 // The shortest-window search of one tile for every request of the job's
 // slice (see the file comment, steps 2 and 3).  Wavefront w takes tasks
 // w, w + kWaves, ...; task vw is slice vw % wpr of request vw / wpr.  The
@@ -1137,7 +1186,7 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
         uint64_t best_end = 0;
         WalkState ws{tg.t0 + end, ts.xend & vmask, ts.xcend, readlane32(pend, n), false};
         walk_pass(P, sm, lane, nt, lim, job.s0, job.s1, vmask, S, ws, best, best_end);
-        if (ws.cur < nt && !ws.closed && lane == 0) sm.defer_mark = job.hi - 1;
+        if (ws.cur < nt && !ws.closed && lane == 0) defer_request(P, sm, job, request(vw));
         const Key k = wave_answer(best, best_end, tl, S);
         if (wpr == 1) {
             const Key a = min_key(readlane_key(acc, n), k);
@@ -1172,7 +1221,7 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
                     if (cur < nt) {
                         WalkState ws{tg.t0 + end, ts.xend & vmask, ts.xcend, cur, false};
                         walk_pass(P, sm, lane, nt, lim, job.s0, job.s1, vmask, S, ws, best, best_end);
-                        if (ws.cur < nt && !ws.closed && lane == 0) sm.defer_mark = job.hi - 1;
+                        if (ws.cur < nt && !ws.closed && lane == 0) defer_request(P, sm, job, q);
                     }
                 }
             }
@@ -1348,20 +1397,6 @@ __device__ __forceinline__ void graph_tags(Params& P) {
     P.qtag = queue_tag(P.epoch);
 }
 
-// The totals of tile p >= 1 of a snapshot (one thread): bytes of all its
-// blocks (X without the 2^50 per pinned block), cost of its evictable blocks
-// and its pinned count.  Index (s0 >> kTileLog2) + p - 1 is below
-// floor(s1 / kTile) <= floor(num_blocks / kTile), and the index ranges of two
-// snapshots do not overlap: every tile past a snapshot's first has a slot of
-// its own.
-__device__ __forceinline__ void write_record(const Params& P, const Job& job, const TileState& ts) {
-    const uint64_t idx = (job.s0 >> kTileLog2) + job.p - 1;
-    if (idx >= (P.num_blocks >> kTileLog2)) return;  // (not reached with valid offsets)
-    P.rec_p[idx] = ts.tq - (static_cast<uint64_t>(ts.tr) << kValBits);
-    P.rec_c[idx] = ts.tc;
-    P.rec_r[idx] = ts.tr;
-}
-
 // After the last tile of a job with one wavefront per request: the held
 // tasks' keys (lane n of wavefront w: request w + kWaves * n) go to out, or
 // to the partial slot when other chunks hold tiles of the snapshot or a
@@ -1390,14 +1425,15 @@ __device__ __forceinline__ void finish_held(const Params& P, const Job& job, uin
 // list (one thread).  The list's word carries the call's queue tag, so the
 // first append of a call restarts the count.
 __device__ void defer_job(const Params& P, const Job& job) {
-    uint64_t old = __hip_atomic_load(P.defer_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const Ext e = ext_of(P);
+    uint64_t old = __hip_atomic_load(e.defer_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     uint64_t want;
     do {
         want = (old >> 32) == P.qtag ? old + 1 : (static_cast<uint64_t>(P.qtag) << 32) | 1ull;
-    } while (!__hip_atomic_compare_exchange_strong(P.defer_word, &old, want, __ATOMIC_RELAXED,
+    } while (!__hip_atomic_compare_exchange_strong(e.defer_word, &old, want, __ATOMIC_RELAXED,
                                                    __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
     const uint64_t idx = (want & 0xffffffffull) - 1;
-    if (idx < P.defer_cap) P.entries[idx] = make_uint4(job.lo, job.hi, job.g, job.G);
+    if (idx < P.defer_cap) e.entries[idx] = make_uint4(job.lo, job.hi, job.g, job.G);
 }
 
 __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params Pin) {
@@ -1476,8 +1512,6 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
         // ---- prefetch the next tile
         const TileGeom tn = has_next ? tile_geom(next) : TileGeom{tg.t0, 0u, 0u, 0u};
         issue_loads(P, tn, t, regs);
-        // ---- the tile's record, for jumps over it by coop_window_long_kernel
-        if (job.y == 0 && job.p != 0 && t == 0) write_record(P, job, ts);
         // ---- 2./3. the requests
         tile_requests(P, sm, job, tg, ts, wpr, t, acc, s_lane);
         __syncthreads();  // LDS is restaged next
@@ -1502,6 +1536,60 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
 // Windows longer than the staged tile and the next one
 // ---------------------------------------------------------------------------
 
+// Totals of blocks [from, to) (a whole wavefront): bytes of all blocks,
+// cost of the evictable ones, the pinned count.
+__device__ Sums stream_totals(const Params& P, uint64_t from, uint64_t to, uint32_t lane) {
+    Sums t{0, 0, 0};
+    for (uint64_t at = from + lane; at < to; at += 64) {
+        const uint32_t k = P.kind[at];
+        t.q += P.size[at];
+        t.c += k == COOP_EVICTABLE ? P.cost[at] : 0;
+        t.r += k >= COOP_PINNED ? 1u : 0u;
+    }
+    for (int o = 32; o >= 1; o >>= 1) {
+        t.q += __shfl_xor(t.q, o, 64);
+        t.c += __shfl_xor(t.c, o, 64);
+        t.r += __shfl_xor(t.r, o, 64);
+    }
+    return t;
+}
+
+// Bytes of blocks [from, to) before the first pinned one (a whole wavefront).
+__device__ uint64_t bytes_before_pinned(const Params& P, uint64_t from, uint64_t to, uint32_t lane) {
+    uint64_t bytes = 0;
+    for (uint64_t at0 = from; at0 < to; at0 += 64) {
+        const uint64_t at = at0 + lane;
+        const bool in = at < to;
+        const uint32_t k = in ? P.kind[at] : 0u;
+        uint64_t v = in ? P.size[at] : 0;
+        const uint64_t pm = __ballot(in && k >= COOP_PINNED);
+        const uint32_t f = pm ? static_cast<uint32_t>(__builtin_ctzll(pm)) : 64u;
+        v = lane < f ? v : 0;
+        for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+        bytes += v;
+        if (pm) break;
+    }
+    return bytes;
+}
+
+// Publishes the record of tile p >= 1 of the job's snapshot from what
+// staging computed (one thread): the totals as device-scope stores, then,
+// once they have completed, the call's tag, which is read first.
+__device__ void publish_record(const Params& P, const Job& job, const TileState& ts) {
+    const uint64_t idx = (job.s0 >> kTileLog2) + job.p - 1;
+    if (job.p == 0 || idx >= (P.num_blocks >> kTileLog2)) return;
+    const Ext e = ext_of(P);
+    __hip_atomic_store(e.rec_p + idx, ts.tq - (static_cast<uint64_t>(ts.tr) << kValBits),
+                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(e.rec_c + idx, ts.tc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(e.rec_r + idx, static_cast<uint64_t>(ts.tr), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0);  // the totals have reached the device-coherent level
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __hip_atomic_store(e.rec_tag + idx, P.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Resolves the pending starts [cur, nA) of a staged tile whatever the length
 // of their windows (a whole wavefront).  From the region end, the run is
 // crossed tile by tile: a jump adds up the records of 64 tiles at a time and
@@ -1518,6 +1606,7 @@ __device__ void long_pass(const Params& P, const Smem& sm, uint32_t lane, uint32
                           uint64_t S, Cand& best, uint64_t& best_end) {
     const uint64_t a = job.s0 & ~7ull;                   // tile k of the snapshot starts at a + k * kTile
     const uint64_t rbase = (job.s0 >> kTileLog2) - 1;    // record of tile k >= 1: rbase + k
+    const Ext e = ext_of(P);
     WalkState ws{tg.t0 + ts.end, ts.xend & vmask, ts.xcend, cur, false};
     // the staged halo: the first blocks of tile p + 1, already in cq / cc
     uint64_t hq = 0, hc = 0;
@@ -1539,10 +1628,30 @@ __device__ void long_pass(const Params& P, const Smem& sm, uint32_t lane, uint32
                 const bool inb = kt < job.tiles;
                 uint64_t rq = 0, rc = 0;
                 uint32_t rr = 1;  // past the snapshot's last tile: a wall
+                bool miss = false;
                 if (inb) {
-                    rq = P.rec_p[rbase + kt];
-                    rc = P.rec_c[rbase + kt];
-                    rr = P.rec_r[rbase + kt];
+                    // a record is complete once its tag is this call's
+                    const uint64_t tag =
+                        __hip_atomic_load(e.rec_tag + rbase + kt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if (tag == P.epoch) {
+                        rq = __hip_atomic_load(e.rec_p + rbase + kt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        rc = __hip_atomic_load(e.rec_c + rbase + kt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        rr = static_cast<uint32_t>(
+                            __hip_atomic_load(e.rec_r + rbase + kt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+                    } else {
+                        miss = true;
+                    }
+                }
+                // records not published (yet): the wavefront sums those tiles itself
+                for (uint64_t mm = __ballot(miss); mm; mm &= mm - 1) {
+                    const uint32_t j = static_cast<uint32_t>(__builtin_ctzll(mm));
+                    const uint64_t t0 = a + ((kk + j) << kTileLog2);
+                    const Sums t = stream_totals(P, t0, t0 + kTile < job.s1 ? t0 + kTile : job.s1, lane);
+                    if (lane == j) {
+                        rq = t.q;
+                        rc = t.c;
+                        rr = t.r;
+                    }
                 }
                 if (mid && kk == k && lane == 0) {
                     rq -= hq;
@@ -1561,9 +1670,23 @@ __device__ void long_pass(const Params& P, const Smem& sm, uint32_t lane, uint32
                     const uint64_t np = a + ((kk + f) << kTileLog2);
                     ws.pos = np < job.s1 ? np : job.s1;
                 }
-                if (f < 64) break;
+                if (f < 64) {
+                    // The run closes in tile kk + f when it holds a pinned
+                    // block: if the bytes before that block do not reach S
+                    // for the first pending start, no later one reaches S
+                    // either (the tile after the staged one is walked, since
+                    // the halo may hold pinned blocks before the run starts).
+                    const uint64_t kf = kk + f;
+                    if (kf < job.tiles && (kf != k || !mid) && readlane32(rr, f) != 0) {
+                        const uint64_t t0 = a + (kf << kTileLog2);
+                        const uint64_t fb =
+                            bytes_before_pinned(P, t0, t0 + kTile < job.s1 ? t0 + kTile : job.s1, lane);
+                        if (ws.cq + fb - base < S) ws.closed = true;
+                    }
+                    break;
+                }
             }
-            if (ws.pos >= job.s1) break;  // the run ends at the snapshot end below S
+            if (ws.closed || ws.pos >= job.s1) break;  // no pending start reaches S in the run
         }
         // walk the tile holding pos up to its end
         const uint64_t kw = (ws.pos - a) >> kTileLog2;
@@ -1574,12 +1697,59 @@ __device__ void long_pass(const Params& P, const Smem& sm, uint32_t lane, uint32
     }
 }
 
+// Unit u of a deferred entry as a job (tile p of snapshot b for slice y,
+// the entry's chunk part g of G); false if u names no tile.
+__device__ bool entry_job(const Params& P, uint4 en, uint32_t u, Cursor& c, Job& job) {
+    const uint32_t y = static_cast<uint32_t>(div_magic(u, P.nv_magic));
+    const uint32_t v = u - y * P.num_virtual;
+    cursor_locate(P, v, c);
+    const uint64_t s1 = c.sb1 < P.num_blocks ? c.sb1 : P.num_blocks;
+    const uint64_t s0 = c.sb < s1 ? c.sb : s1;
+    const uint64_t q1 = c.rb1 < P.num_requests ? c.rb1 : P.num_requests;
+    const uint64_t q0 = c.rb < q1 ? c.rb : q1;
+    job.u = u;
+    job.lo = en.x;
+    job.hi = en.y;
+    job.y = y;
+    job.b = c.b;
+    job.s0 = s0;
+    job.s1 = s1;
+    job.q0 = q0;
+    job.R = q1 - q0;
+    job.K = job.R > y ? ((job.R - y - 1) >> P.slices_log2) + 1 : 0;
+    job.tiles = s1 > s0 ? (s1 - (s0 & ~7ull) + kTile - 1) >> kTileLog2 : 1;
+    job.p = v - first_id(c.b, c.sb);
+    job.g = en.z;
+    job.G = en.w;
+    job.first = u == en.x;
+    job.last = u + 1 == en.y;
+    job.direct = job.G == 1;
+    return job.p < job.tiles;
+}
+
+// The records of the tiles past the first that a deferred entry names: each
+// tile is staged and its totals published (a whole workgroup).
+__device__ void publish_entry_records(const Params& P, Smem& sm, uint4 en) {
+    Cursor c;
+    Job job;
+    for (uint32_t u = en.x; u < en.y; ++u) {
+        if (!entry_job(P, en, u, c, job) || job.p == 0) continue;
+        const TileGeom tg = tile_geom(job);
+        TileRegs regs;
+        issue_loads(P, tg, threadIdx.x, regs);
+        const TileState ts = stage_tile(sm, tg, threadIdx.x, regs);
+        if (threadIdx.x == 0) publish_record(P, job, ts);
+    }
+}
+
 // One deferred entry: the units [lo, hi) of (snapshot b, slice y) that one
 // chunk held, and that chunk's partial slot g of G.  Every tile is staged
-// again, the pending starts of every request are resolved by long_pass and
-// folded into the request's partial slot (written by the search kernel);
-// then, as the search kernel would have: the result, or the arrival ticket
-// and the combine when the snapshot spans several chunks.
+// again.  For each request whose deferral bit is set, the tile's pending
+// starts are cut into kWaves equal parts, one per wavefront, each resolved
+// by long_pass; the wavefronts' answers and the request's partial slot
+// (written by the search kernel) are combined.  Then, as the search kernel
+// would have: the results, or the arrival ticket and the combine when the
+// snapshot spans several chunks; the deferral bits are cleared.
 __device__ void resolve_entry(const Params& P, Smem& sm, uint4 en, uint32_t& last_flag) {
     const uint32_t tid = threadIdx.x;
     const uint32_t lane = tid & 63u;
@@ -1587,31 +1757,7 @@ __device__ void resolve_entry(const Params& P, Smem& sm, uint4 en, uint32_t& las
     Cursor c;
     Job job;
     for (uint32_t u = en.x; u < en.y; ++u) {
-        const uint32_t y = static_cast<uint32_t>(div_magic(u, P.nv_magic));
-        const uint32_t v = u - y * P.num_virtual;
-        cursor_locate(P, v, c);
-        const uint64_t s1 = c.sb1 < P.num_blocks ? c.sb1 : P.num_blocks;
-        const uint64_t s0 = c.sb < s1 ? c.sb : s1;
-        const uint64_t q1 = c.rb1 < P.num_requests ? c.rb1 : P.num_requests;
-        const uint64_t q0 = c.rb < q1 ? c.rb : q1;
-        job.u = u;
-        job.lo = en.x;
-        job.hi = en.y;
-        job.y = y;
-        job.b = c.b;
-        job.s0 = s0;
-        job.s1 = s1;
-        job.q0 = q0;
-        job.R = q1 - q0;
-        job.K = job.R > y ? ((job.R - y - 1) >> P.slices_log2) + 1 : 0;
-        job.tiles = s1 > s0 ? (s1 - (s0 & ~7ull) + kTile - 1) >> kTileLog2 : 1;
-        job.p = v - first_id(c.b, c.sb);
-        job.g = en.z;
-        job.G = en.w;
-        job.first = u == en.x;
-        job.last = u + 1 == en.y;
-        job.direct = job.G == 1;
-        if (job.p >= job.tiles) continue;  // (not reached: the entry names the job's tiles)
+        if (!entry_job(P, en, u, c, job)) continue;  // (not reached: the entry names the job's tiles)
         const TileGeom tg = tile_geom(job);
         TileRegs regs;
         issue_loads(P, tg, tid, regs);
@@ -1621,52 +1767,93 @@ __device__ void resolve_entry(const Params& P, Smem& sm, uint4 en, uint32_t& las
         const uint64_t vmask = ts.packed ? kValMask : kNone;
         const uint64_t tl = tg.t0 - job.s0;
         if (open && nt != 0) {
-            for (uint64_t vw = w; vw < job.K; vw += kWaves) {
-                const uint64_t q = job.q0 + job.y + (vw << P.slices_log2);
-                const uint64_t S = ld_const(P.req_size, q);
-                if (S == 0) continue;
-                const uint64_t Sc = S < (1ull << kValBits) ? S : (1ull << kValBits);
-                const uint32_t cur = pending_start(sm, ts.packed, nt, ts.xend, ts.endrun, S, Sc, lane);
-                if (cur >= nt) continue;
-                Cand best = cand_none();
-                uint64_t best_end = 0;
-                long_pass(P, sm, lane, cur, nt, job, tg, ts, vmask, S, best, best_end);
-                const Key k = wave_answer(best, best_end, tl, S);
-                if (lane == 0 && k.start != kNone) {
-                    // this lane alone reads and writes the slot of request q
+            // tasks (request r, part): parts = kWaves / (the requests, rounded
+            // up to a power of two, at most kWaves); wavefront w takes task
+            // t0 + w of each round
+            uint32_t k2 = 1;
+            while (k2 < job.K && k2 < kWaves) k2 <<= 1;
+            const uint32_t parts = kWaves / k2;
+            for (uint64_t t0 = 0; t0 < job.K * parts; t0 += kWaves) {
+                const uint64_t t = t0 + w;
+                const uint64_t r = t / parts;
+                const uint32_t part = static_cast<uint32_t>(t % parts);
+                Key k = key_none();
+                if (r < job.K) {
+                    const uint64_t q = job.q0 + job.y + (r << P.slices_log2);
+                    const uint64_t bit = q * P.pc + job.g;
+                    // (only this entry changes the bit)
+                    const uint32_t word = uniform(ext_of(P).bits[bit >> 5]);
+                    const uint64_t S = ld_const(P.req_size, q);
+                    if (((word >> (bit & 31u)) & 1u) && S != 0) {
+                        const uint64_t Sc = S < (1ull << kValBits) ? S : (1ull << kValBits);
+                        const uint32_t cur =
+                            pending_start(sm, ts.packed, nt, ts.xend, ts.endrun, S, Sc, lane);
+                        if (cur < nt) {
+                            const uint32_t len = nt - cur;
+                            const uint32_t c0 = cur + len * part / parts;
+                            const uint32_t c1 = cur + len * (part + 1) / parts;
+                            Cand best = cand_none();
+                            uint64_t best_end = 0;
+                            if (c0 < c1)
+                                long_pass(P, sm, lane, c0, c1, job, tg, ts, vmask, S, best, best_end);
+                            k = wave_answer(best, best_end, tl, S);
+                        }
+                    }
+                }
+                if (parts > 1) {
+                    if (lane == 0) sm.slot[w] = k;
+                    __syncthreads();
+                    for (uint32_t i = 1; i < parts; ++i) k = min_key(k, sm.slot[w + i]);
+                }
+                // part 0's wavefront folds the request's key into its slot;
+                // the same lane does so for request r on every tile
+                if (part == 0 && r < job.K && lane == 0 && k.start != kNone) {
+                    const uint64_t q = job.q0 + job.y + (r << P.slices_log2);
                     Key* slot = P.part + q * P.pc + job.g;
                     store_key_device(slot, min_key(load_key_device(slot), k));
                 }
+                if (parts > 1) __syncthreads();  // sm.slot is written again
             }
         }
         __syncthreads();  // LDS is restaged next
     }
-    if (job.direct) {
-        if (lane == 0) {
-            for (uint64_t vw = w; vw < job.K; vw += kWaves) {
-                const uint64_t q = job.q0 + job.y + (vw << P.slices_log2);
-                P.out[q] = to_window(load_key_device(P.part + q * P.pc + job.g), ld_const(P.req_size, q));
-            }
-        }
-    } else {
-        combine_partials(P, job, tid, last_flag);
+    // every slot write has completed before any thread reads
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __syncthreads();
+    for (uint64_t r = tid; r < job.K; r += kThreads) {
+        const uint64_t q = job.q0 + job.y + (r << P.slices_log2);
+        const uint64_t bit = q * P.pc + job.g;
+        atomicAnd(ext_of(P).bits + (bit >> 5), ~(1u << (bit & 31u)));
+        if (job.direct)
+            P.out[q] = to_window(load_key_device(P.part + q * P.pc + job.g), ld_const(P.req_size, q));
     }
+    if (!job.direct) combine_partials(P, job, tid, last_flag);
     __syncthreads();  // last_flag and LDS are used by the next entry
 }
 
 // Finishes the jobs the search kernel deferred, after it on the stream (so
 // every tile record and partial key is in place).  With nothing deferred
 // (the list's word carries an older tag) every workgroup returns at once.
-__global__ __launch_bounds__(kThreads, 4) void coop_window_long_kernel(Params Pin) {
+__global__ __launch_bounds__(kThreads, 2) void coop_window_long_kernel(Params Pin) {
     __shared__ Smem sm;
     __shared__ uint32_t last_flag;
     Params P = Pin;
     graph_tags(P);
-    const uint64_t word = __hip_atomic_load(P.defer_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const Ext ex = ext_of(P);
+    const uint64_t word = __hip_atomic_load(ex.defer_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     uint64_t n = (word >> 32) == P.qtag ? (word & 0xffffffffull) : 0;
     if (n > P.defer_cap) n = P.defer_cap;
+    // first the tile records of every entry (a tile whose record is not out
+    // yet when a jump needs it is summed by that wavefront), then the entries
     for (uint64_t e = blockIdx.x; e < n; e += gridDim.x) {
-        const uint4 en = P.entries[e];
+        const uint4 en = ex.entries[e];
+        if (en.x >= en.y || en.y > P.units || en.w == 0 || en.w > P.pc || en.z >= en.w) continue;
+        publish_entry_records(P, sm, en);
+    }
+    for (uint64_t e = blockIdx.x; e < n; e += gridDim.x) {
+        const uint4 en = ex.entries[e];
         // (entries are written by this call's search kernel; the checks keep
         // every access in bounds whatever the workspace holds)
         if (en.x >= en.y || en.y > P.units || en.w == 0 || en.w > P.pc || en.z >= en.w) continue;
@@ -1692,15 +1879,16 @@ struct Plan {
     uint64_t defer_cap;    // deferred entries, at most
     size_t off_defer;      // the deferred list's word, then its entries
     size_t off_entries;
-    size_t off_rec;        // tile records: bytes, costs (u64), pinned counts (u32)
+    size_t off_rec;        // tile records: bytes, costs, pinned counts, tags (u64 each)
     uint64_t num_rec;
+    size_t off_bits;       // deferral bits, one per partial slot
     size_t bytes;          // total workspace
 };
 
 // Two workgroups of kThreads fit one CU (LDS); 256 CUs.  Workgroups past the
 // resident ones are still correct (nothing waits on another workgroup).
 constexpr uint64_t kGridWGs = 512;
-constexpr uint64_t kLongGridWGs = 512;  // workgroups of coop_window_long_kernel, at most
+constexpr uint64_t kLongGridWGs = 256;  // workgroups of coop_window_long_kernel (one per CU), at most
 constexpr uint64_t kMaxSlices = 256;
 constexpr uint64_t kSliceRequests = 512;  // requests per snapshot before slicing them
 static_assert(kGridWGs < (1ull << kEpochShift), "tickets fit the counter");
@@ -1782,6 +1970,9 @@ bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests
     // deferred list's word
     pl->off_defer = pl->part_bytes + (slices * num_segments + 2) * sizeof(uint64_t);
     pl->off_entries = (pl->off_defer + sizeof(uint64_t) + 15) & ~static_cast<size_t>(15);
+    // (the kernels derive these offsets from the queue word's address: see
+    // Ext; the workspace is 256-byte aligned, so aligning offsets aligns
+    // addresses)
     // A job defers only when a window runs past the tile after the staged
     // one, so its snapshot has at least three tiles (more than 8185
     // blocks).  The chunk parts of such jobs number at most the jobs plus
@@ -1790,7 +1981,9 @@ bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests
     pl->defer_cap = nchunks + slices * big;
     pl->num_rec = num_blocks >> kTileLog2;
     pl->off_rec = pl->off_entries + pl->defer_cap * sizeof(uint4);
-    pl->bytes = pl->off_rec + pl->num_rec * (2 * sizeof(uint64_t) + sizeof(uint32_t));
+    pl->off_bits = pl->off_rec + pl->num_rec * 4 * sizeof(uint64_t);
+    // (+32: the layout stays inside even if the workspace is only 8-byte aligned)
+    pl->bytes = pl->off_bits + (num_requests * pc + 31) / 32 * sizeof(uint32_t) + 32;
     return true;
 }
 
@@ -1913,13 +2106,7 @@ coop_status_t launch_search(const Plan& pl, const uint64_t* size, const uint64_t
     P.slices_log2 = pl.slices_log2;
     P.inv_slope = static_cast<double>(num_segments) /
                   (static_cast<double>(num_blocks) / kTile + static_cast<double>(num_segments));
-    char* ws = static_cast<char*>(workspace);
-    P.defer_word = reinterpret_cast<uint64_t*>(ws + pl.off_defer);
-    P.entries = reinterpret_cast<uint4*>(ws + pl.off_entries);
     P.defer_cap = static_cast<uint32_t>(pl.defer_cap);
-    P.rec_p = reinterpret_cast<uint64_t*>(ws + pl.off_rec);
-    P.rec_c = P.rec_p + pl.num_rec;
-    P.rec_r = reinterpret_cast<uint32_t*>(P.rec_c + pl.num_rec);
 
     // A captured launch replays with the arguments it was recorded with, so
     // its tag cannot come from the host: it comes from the tag word,
