@@ -95,6 +95,7 @@ constexpr uint32_t kMaxSteps = ((kTile + kStage + 63) / 64 + 1) / 4 * 4 + 2;
 // positions a lane reads past the starts once they are used up.
 constexpr uint32_t kXN = ((kStage + 2 > kTile + kMaxSteps + 1 ? kStage + 2 : kTile + kMaxSteps + 1) +
                           7) / 8 * 8;
+static_assert((kXN + kMaxSteps) % 2 == 0 && kXN % 2 == 0, "the LDS arrays stay 16-byte aligned");
 constexpr uint32_t kValBits = 50;
 constexpr uint64_t kValMask = (1ull << kValBits) - 1;
 // With every block below 2^37 bytes, any staged prefix (at most kStage < 2^13
@@ -388,7 +389,10 @@ __device__ __forceinline__ void chunk_range(const Params& P, uint64_t c, uint64_
 }
 
 struct Smem {
-    uint64_t x[kXN];    // keys R << 50 | P, or plain P in a tile with a huge block
+    // keys R << 50 | P (or plain P in a tile with a huge block), then the end
+    // keys a merge may read past the sentinel; 16-byte aligned (as is xc,
+    // which follows at a multiple of 16 bytes) for 16-byte staging stores
+    __attribute__((aligned(16))) uint64_t x[kXN + kMaxSteps];
     uint64_t xc[kXN];   // C
     uint16_t run[kXN];  // R, kept only in a tile with a huge block
     Sums wsum[kWaves];  // per-wavefront totals of the tile
@@ -645,11 +649,16 @@ __device__ __forceinline__ uint32_t merge_steps(uint32_t total, uint32_t lanes) 
 // iff D < 2^50, i.e. both ends have the same run id; D is then its byte
 // count.  Windows are ranked by (cost, D), which orders them as (cost,
 // bytes - S).  Steps past the lane's slice repeat work of the next lane
-// (harmless: equal windows), and starts past nA are ignored.  X[nB + 1] must
-// be kEndKey, which every target is below: the end index never passes it.
+// (harmless: equal windows).  A lane may take starts past nA (boundaries of
+// the halo): their windows are real windows of the snapshot, the shortest
+// from that start within the staged region, so scoring them is harmless too.
+// X[nB + 1] must be kEndKey, above every target, and so must the kMaxSteps
+// keys after it: a lane that has taken the start nB + 1 (the sentinel itself)
+// can take nothing more, and its end index runs on through those keys.  Only
+// the start is kept (as a byte offset, pA + pB growing by 8 a step gives the
+// end pointer); the caller finds the winner's end again (merged_answer).
 __device__ __forceinline__ void merge_pass(const Smem& sm, uint32_t nA, uint32_t nB, uint32_t d,
-                                           uint32_t L, uint64_t Sc, Cand& best,
-                                           uint32_t& best_end) {
+                                           uint32_t L, uint64_t Sc, Cand& best) {
     // diagonal split: the number of starts among the first d merge elements
     uint32_t lo = d > nB ? d - nB : 0, hi = d < nA ? d : nA;
     while (lo < hi) {
@@ -659,36 +668,32 @@ __device__ __forceinline__ void merge_pass(const Smem& sm, uint32_t nA, uint32_t
         lo = before ? mid + 1 : lo;
         hi = before ? hi : mid;
     }
-    uint32_t pA = lo * 8u, pB = (d - lo + 1) * 8u;  // byte offsets of X[a] and of X[b + 1]
-    const uint32_t endA = nA * 8u;
+    uint32_t pA = lo * 8u;
+    const uint32_t sum0 = (d + 1) * 8u;  // pA + pB before the first step; grows by 8 a step
     const int64_t sc = static_cast<int64_t>(Sc);
     uint64_t bc = kNone, bd = kNone;
-    uint32_t bpa = kNone32, bpb = 0;
+    uint32_t bpa = kNone32;
     for (uint32_t k = 0; k < L; k += 2) {
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
+        for (uint32_t u = 0; u < 2; ++u) {
+            const uint32_t pB = sum0 + (k + u) * 8u - pA;
             const uint64_t xa = lds_u64(sm.x, pA), kb = lds_u64(sm.x, pB);
             const uint64_t ca = lds_u64(sm.xc, pA), cb = lds_u64(sm.xc, pB);
             const uint64_t D = kb - xa;
             const bool takeA = static_cast<int64_t>(D) >= sc;
-            const bool valid = takeA & (pA < endA) & (D < (1ull << kValBits));
+            const bool valid = takeA & (D < (1ull << kValBits));
             const uint64_t cost = cb - ca;
             const bool better = valid & ((cost < bc) | ((cost == bc) & (D < bd)));
             bc = better ? cost : bc;
             bd = better ? D : bd;
             bpa = better ? pA : bpa;
-            bpb = better ? pB : bpb;
             pA += takeA ? 8u : 0u;
-            pB += takeA ? 0u : 8u;
         }
     }
     // Within a lane starts are met in increasing order, so strict comparison
     // kept the lowest start among equal (cost, bytes).
     const Cand c{bc, bpa == kNone32 ? kNone : bd - Sc, bpa == kNone32 ? kNone32 : bpa / 8u};
-    if (cand_less(c, best)) {
-        best = c;
-        best_end = bpb / 8u;
-    }
+    if (cand_less(c, best)) best = c;
 }
 
 // Plain prefixes (a tile with a huge block): starts g, g + lanes, ... below
@@ -1002,12 +1007,34 @@ __device__ __forceinline__ TileState stage_tile(Smem& sm, const TileGeom& tg, ui
         ts.xcend = use_halo ? all_tot.c : tile_tot.c;
         ts.endrun = static_cast<uint32_t>(ts.xend >> kValBits);
         if (i0 + kItems <= nt) {
+            // Lanes 64 bytes apart would put the 16-byte stores of a
+            // wavefront on a few LDS banks: lane t stores its four pairs in
+            // the order (q + t) & 3, which spreads the wavefront over all of
+            // them.
+            ulonglong2 px[kItems / 2], pc[kItems / 2];
 #pragma unroll
-            for (uint32_t j = 0; j < kItems; j += 2) {
-                *reinterpret_cast<ulonglong2*>(&sm.x[i0 + j]) =
-                    ulonglong2{base_x + r.sz[j], base_x + r.sz[j + 1]};
-                *reinterpret_cast<ulonglong2*>(&sm.xc[i0 + j]) =
-                    ulonglong2{base_c + r.ct[j], base_c + r.ct[j + 1]};
+            for (uint32_t q = 0; q < kItems / 2; ++q) {
+                px[q] = ulonglong2{base_x + r.sz[2 * q], base_x + r.sz[2 * q + 1]};
+                pc[q] = ulonglong2{base_c + r.ct[2 * q], base_c + r.ct[2 * q + 1]};
+            }
+            const uint32_t rot = tid & 3u;
+            if (rot & 1u) {
+                const ulonglong2 tx = px[0], tc = pc[0];
+#pragma unroll
+                for (uint32_t q = 0; q < 3; ++q) { px[q] = px[q + 1]; pc[q] = pc[q + 1]; }
+                px[3] = tx; pc[3] = tc;
+            }
+            if (rot & 2u) {
+                ulonglong2 tx = px[0], tc = pc[0];
+                px[0] = px[2]; pc[0] = pc[2]; px[2] = tx; pc[2] = tc;
+                tx = px[1]; tc = pc[1];
+                px[1] = px[3]; pc[1] = pc[3]; px[3] = tx; pc[3] = tc;
+            }
+#pragma unroll
+            for (uint32_t q = 0; q < kItems / 2; ++q) {
+                const uint32_t at = i0 + 2 * ((q + rot) & 3u);
+                *reinterpret_cast<ulonglong2*>(&sm.x[at]) = px[q];
+                *reinterpret_cast<ulonglong2*>(&sm.xc[at]) = pc[q];
             }
         } else {
 #pragma unroll
@@ -1045,6 +1072,7 @@ __device__ __forceinline__ TileState stage_tile(Smem& sm, const TileGeom& tg, ui
         sm.run[ts.end] = static_cast<uint16_t>(ts.endrun);
         sm.x[ts.end + 1] = kEndKey;  // sentinel end key
     }
+    if (tid < kMaxSteps) sm.x[ts.end + 2 + tid] = kEndKey;  // what a merge reads past the sentinel
     __syncthreads();
     return ts;
 }
@@ -1097,6 +1125,19 @@ __device__ __forceinline__ Key wave_answer(const Cand& best, uint64_t best_end, 
 }
 
 __device__ __forceinline__ Key min_key(const Key& a, const Key& b) { return key_less(b, a) ? b : a; }
+
+// The wavefront's answer from the merge of a packed region: the
+// lexicographic minimum of the lanes' windows; its end is the first end key
+// at or above the winner's target (a wavefront search; every lane active).
+__device__ __forceinline__ Key merged_answer(const Smem& sm, const Cand& best, uint64_t tl, uint64_t S,
+                                             uint64_t Sc, uint32_t end, uint32_t lane) {
+    const Cand m = wave_argmin_packed(best);
+    if (m.start == kNone32) return key_none();
+    const uint64_t target = sm.x[m.start] + Sc;
+    const uint32_t e = wave_lower_bound(m.start + 1, end + 1, lane,
+                                        [&](uint32_t k) { return sm.x[k] >= target; });
+    return Key{m.cost, m.excess + S, tl + m.start, tl + e};
+}
 
 // Request q has windows past the walk's limit (one lane): its bit for the
 // chunk part, and the job's mark.
@@ -1151,7 +1192,7 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
                 const uint32_t total = nt + end;
                 const uint32_t L = merge_steps(total, lanes);
                 const uint32_t d = gl * L < total ? gl * L : total;
-                merge_pass(sm, nt, end, d, L, Sc, best, e32);
+                merge_pass(sm, nt, end, d, L, Sc, best);
             } else {
                 plain_pass(sm, nt, end, gl, lanes, S, best, e32);
             }
@@ -1163,7 +1204,8 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
             }
         }
         // in-region windows of a packed region: excess below 2^50
-        Key k = ts.packed ? wave_answer<true>(best, best_end, tl, S)
+        Key k = ts.packed ? merged_answer(sm, best, tl, S, S < (1ull << kValBits) ? S : (1ull << kValBits),
+                                          end, lane)
                           : wave_answer(best, best_end, tl, S);
         if (wpr == 1) {
             k = min_key(readlane_key(acc, n), k);
@@ -1203,6 +1245,7 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
             const uint64_t S = ld_const(P.req_size, q);
             Cand best = cand_none();
             uint64_t best_end = 0;
+            Key km = key_none();
             if (S != 0 && nt != 0) {
                 const uint64_t Sc = S < (1ull << kValBits) ? S : (1ull << kValBits);
                 uint32_t e32 = 0;
@@ -1210,7 +1253,9 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
                     const uint32_t total = nt + end;
                     const uint32_t L = merge_steps(total, 64u);
                     const uint32_t d = lane * L < total ? lane * L : total;
-                    merge_pass(sm, nt, end, d, L, Sc, best, e32);
+                    Cand bm = cand_none();
+                    merge_pass(sm, nt, end, d, L, Sc, bm);
+                    km = merged_answer(sm, bm, tl, S, Sc, end, lane);
                 } else {
                     plain_pass(sm, nt, end, lane, 64u, S, best, e32);
                 }
@@ -1225,7 +1270,7 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
                     }
                 }
             }
-            Key k = wave_answer(best, best_end, tl, S);
+            Key k = min_key(km, wave_answer(best, best_end, tl, S));
             if (!job.first) k = min_key(load_key_device(P.part + q * P.pc + job.g), k);
             // (a result of a snapshot covered by this workgroup alone is
             // copied to out after the barrier that ends the tile)
