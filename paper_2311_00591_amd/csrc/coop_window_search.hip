@@ -112,6 +112,12 @@ static_assert(kStage < (1u << 16), "pinned counts fit 16 bits");
 constexpr uint64_t kNone = ~0ull;
 constexpr uint32_t kNone32 = ~0u;
 constexpr uint32_t kMaxWpr = 8;                  // wavefronts that may share one request
+constexpr uint32_t kWalkCap = 1024;              // blocks a wavefront walks past a staged region
+// The fewest blocks of a snapshot whose windows can run past a walk: the
+// walk stops before the snapshot end only if more than kTile + kHaloCap +
+// kWalkCap blocks follow the tile start, which is at most 7 blocks before
+// the snapshot start.
+constexpr uint64_t kDeferMin = kTile + kHaloCap + kWalkCap - 6;
 constexpr uint64_t kPartialBudget = 1ull << 23;  // partial keys (32 B each) before chunks grow
 constexpr uint32_t kEpochShift = 24;             // counter = epoch << 24 | tickets
 // Call tags (40 bits).  An eager call takes the next value of a host counter
@@ -329,18 +335,16 @@ struct Params {
 // entries), the deferred entries {first unit, end unit, g, G} (16-byte
 // aligned), the tile records of tile p >= 1 of every snapshot at index
 // (seg[b] >> kTileLog2) + p - 1 (bytes of all its blocks, cost of its
-// evictable blocks, its pinned count, and the call tag that marks it
-// complete), written by coop_window_long_kernel, and one deferral bit per
-// partial slot (bit q * pc + g: request q left windows to
-// coop_window_long_kernel in its chunk part g).  Derived where needed rather
-// than passed, to keep the kernels' uniform state small.
+// evictable blocks, its pinned count; written by the search kernel, read by
+// coop_window_long_kernel), and one deferral bit per partial slot (bit q * pc + g: request
+// q left windows to coop_window_long_kernel in its chunk part g).  Derived
+// where needed rather than passed, to keep the kernels' uniform state small.
 struct Ext {
     uint64_t* defer_word;
     uint4* entries;
     uint64_t* rec_p;
     uint64_t* rec_c;
     uint64_t* rec_r;
-    uint64_t* rec_tag;
     uint32_t* bits;
 };
 
@@ -352,8 +356,7 @@ __device__ __forceinline__ Ext ext_of(const Params& P) {
     const uint64_t nrec = P.num_blocks >> kTileLog2;
     e.rec_c = e.rec_p + nrec;
     e.rec_r = e.rec_c + nrec;
-    e.rec_tag = e.rec_r + nrec;
-    e.bits = reinterpret_cast<uint32_t*>(e.rec_tag + nrec);
+    e.bits = reinterpret_cast<uint32_t*>(e.rec_r + nrec);
     return e;
 }
 
@@ -1098,6 +1101,30 @@ __device__ __forceinline__ Key load_key_device(Key* p) {
                __hip_atomic_load(&p->end, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)};
 }
 
+// Deferred entries, tile records and deferral bits are handed from one
+// workgroup to another (of the same kernel or of the next one on the
+// stream, possibly on another XCD) the same way: device-scope atomic
+// stores and loads.  A plain load can return a copy of the line that a
+// cache took before the writer's store (measured: entries of one call
+// read back as zeros by the long kernel).
+__device__ __forceinline__ void store_entry_device(uint4* p, const uint4& v) {
+    uint64_t* w = reinterpret_cast<uint64_t*>(p);
+    __hip_atomic_store(w, static_cast<uint64_t>(v.x) | (static_cast<uint64_t>(v.y) << 32), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(w + 1, static_cast<uint64_t>(v.z) | (static_cast<uint64_t>(v.w) << 32), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ uint4 load_entry_device(uint4* p) {
+    uint64_t* w = reinterpret_cast<uint64_t*>(p);
+    const uint64_t a = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint64_t b = __hip_atomic_load(w + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // every lane reads the same entry: taking the words from the first lane
+    // keeps the control flow that depends on them scalar
+    return make_uint4(uniform(static_cast<uint32_t>(a)), uniform(static_cast<uint32_t>(a >> 32)),
+                      uniform(static_cast<uint32_t>(b)), uniform(static_cast<uint32_t>(b >> 32)));
+}
+
 __device__ __forceinline__ Key readlane_key(const Key& k, uint32_t lane) {
     return Key{readlane64(k.cost, lane), readlane64(k.bytes, lane), readlane64(k.start, lane),
                readlane64(k.end, lane)};
@@ -1166,8 +1193,8 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
     const uint32_t nt = tg.nt, end = ts.end;
     const uint64_t vmask = ts.packed ? kValMask : kNone;
     const bool open = tg.t0 + end < job.s1;  // the region's last run may go on
-    // walks past the staged region stop at the end of the next tile
-    const uint64_t lim = tg.t0 + 2ull * kTile < job.s1 ? tg.t0 + 2ull * kTile : job.s1;
+    // walks past the staged region stop kWalkCap blocks past its end
+    const uint64_t lim = tg.t0 + end + kWalkCap < job.s1 ? tg.t0 + end + kWalkCap : job.s1;
     const uint64_t tasks = job.K * wpr;
     const uint32_t wl2 = static_cast<uint32_t>(__builtin_ctz(wpr));
     const uint32_t lanes = 64u * wpr;
@@ -1478,7 +1505,21 @@ __device__ void defer_job(const Params& P, const Job& job) {
     } while (!__hip_atomic_compare_exchange_strong(e.defer_word, &old, want, __ATOMIC_RELAXED,
                                                    __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
     const uint64_t idx = (want & 0xffffffffull) - 1;
-    if (idx < P.defer_cap) e.entries[idx] = make_uint4(job.lo, job.hi, job.g, job.G);
+    if (idx < P.defer_cap) store_entry_device(e.entries + idx, make_uint4(job.lo, job.hi, job.g, job.G));
+}
+
+// The record of tile p >= 1 of the job's snapshot, from what staging
+// computed (one thread): bytes of all its blocks, cost of its evictable
+// blocks, its pinned count.  Every unit of the tile writes the same values;
+// coop_window_long_kernel, next on the stream, reads them.
+__device__ __forceinline__ void publish_record(const Params& P, const Job& job, const TileState& ts) {
+    const uint64_t idx = (job.s0 >> kTileLog2) + job.p - 1;
+    if (job.p == 0 || idx >= (P.num_blocks >> kTileLog2)) return;
+    const Ext e = ext_of(P);
+    __hip_atomic_store(e.rec_p + idx, ts.tq - (static_cast<uint64_t>(ts.tr) << kValBits), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(e.rec_c + idx, ts.tc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(e.rec_r + idx, static_cast<uint64_t>(ts.tr), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params Pin) {
@@ -1549,6 +1590,7 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
         const bool has_next = find_job(P, sm, t, cur, have_cursor, wk, reserve, job.u + 1, next);
         // ---- 1. stage the tile whose blocks are in (or on their way to) regs
         const TileState ts = stage_tile(sm, tg, t, regs);
+        if (t == 0 && job.p != 0) publish_record(P, job, ts);
         asm volatile("" : "+v"(s_lane));
         if (job.first) acc = key_none();
         // ---- keep a chunk in reserve (no vector load is in flight here, so
@@ -1578,168 +1620,297 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
 }
 
 // ---------------------------------------------------------------------------
-// Windows longer than the staged tile and the next one
+// Windows that end more than kWalkCap blocks past the staged region
 // ---------------------------------------------------------------------------
+//
+// coop_window_long_kernel runs after the search kernel on the stream, so it
+// sees every tile record and every deferred entry of the call; no
+// workgroup of it waits for another.  Each workgroup takes deferred
+// entries and stages their tiles again.  For every request that deferred,
+// the pending starts of a tile are resolved stretch by stretch: the
+// workgroup sums the tile records forward from the region end, 512 tiles a
+// round, up to the first tile that holds a pinned block or where the window
+// of the first pending start ends; that tile (from the region end on, if the
+// region reaches into it) is staged into a second LDS buffer as plain byte
+// and cost prefixes, cut at its first pinned block, and the byte targets the
+// pending starts still need past the stretch start are merged with its
+// prefixes as the in-region merge does.  Starts whose windows end further go
+// on to the next stretch.  Every value that decides a barrier's path (the
+// tile, the stretch, the next pending start) comes from LDS, the same for
+// every wavefront.
 
-// Totals of blocks [from, to) (a whole wavefront): bytes of all blocks,
-// cost of the evictable ones, the pinned count.
-__device__ Sums stream_totals(const Params& P, uint64_t from, uint64_t to, uint32_t lane) {
-    Sums t{0, 0, 0};
-    for (uint64_t at = from + lane; at < to; at += 64) {
-        const uint32_t k = P.kind[at];
-        t.q += P.size[at];
-        t.c += k == COOP_EVICTABLE ? P.cost[at] : 0;
-        t.r += k >= COOP_PINNED ? 1u : 0u;
-    }
-    for (int o = 32; o >= 1; o >>= 1) {
-        t.q += __shfl_xor(t.q, o, 64);
-        t.c += __shfl_xor(t.c, o, 64);
-        t.r += __shfl_xor(t.r, o, 64);
-    }
-    return t;
+struct Sums3 {
+    uint64_t q, c, r;
+};
+
+__device__ __forceinline__ Sums3 add3(const Sums3& a, const Sums3& b) {
+    return Sums3{a.q + b.q, a.c + b.c, a.r + b.r};
 }
 
-// Bytes of blocks [from, to) before the first pinned one (a whole wavefront).
-__device__ uint64_t bytes_before_pinned(const Params& P, uint64_t from, uint64_t to, uint32_t lane) {
-    uint64_t bytes = 0;
-    for (uint64_t at0 = from; at0 < to; at0 += 64) {
-        const uint64_t at = at0 + lane;
-        const bool in = at < to;
-        const uint32_t k = in ? P.kind[at] : 0u;
-        uint64_t v = in ? P.size[at] : 0;
-        const uint64_t pm = __ballot(in && k >= COOP_PINNED);
-        const uint32_t f = pm ? static_cast<uint32_t>(__builtin_ctzll(pm)) : 64u;
-        v = lane < f ? v : 0;
-        for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-        bytes += v;
-        if (pm) break;
-    }
-    return bytes;
+template <int Ctrl, int RowMask>
+__device__ __forceinline__ void sum3_step(Sums3& s) {
+    s.q += dpp64<Ctrl, RowMask>(s.q, 0);
+    s.c += dpp64<Ctrl, RowMask>(s.c, 0);
+    s.r += dpp64<Ctrl, RowMask>(s.r, 0);
 }
 
-// Publishes the record of tile p >= 1 of the job's snapshot from what
-// staging computed (one thread): the totals as device-scope stores, then,
-// once they have completed, the call's tag, which is read first.
-__device__ void publish_record(const Params& P, const Job& job, const TileState& ts) {
-    const uint64_t idx = (job.s0 >> kTileLog2) + job.p - 1;
-    if (job.p == 0 || idx >= (P.num_blocks >> kTileLog2)) return;
-    const Ext e = ext_of(P);
-    __hip_atomic_store(e.rec_p + idx, ts.tq - (static_cast<uint64_t>(ts.tr) << kValBits),
-                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(e.rec_c + idx, ts.tc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(e.rec_r + idx, static_cast<uint64_t>(ts.tr), __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_AGENT);
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    __builtin_amdgcn_s_waitcnt(0);  // the totals have reached the device-coherent level
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    __hip_atomic_store(e.rec_tag + idx, P.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+__device__ __forceinline__ void wave_inclusive_sum3(Sums3& s) {
+    sum3_step<kRowShr1, 0xf>(s);
+    sum3_step<kRowShr2, 0xf>(s);
+    sum3_step<kRowShr4, 0xf>(s);
+    sum3_step<kRowShr8, 0xf>(s);
+    sum3_step<kRowBcast15, 0xa>(s);
+    sum3_step<kRowBcast31, 0xc>(s);
 }
 
-// Resolves the pending starts [cur, nA) of a staged tile whatever the length
-// of their windows (a whole wavefront).  From the region end, the run is
-// crossed tile by tile: a jump adds up the records of 64 tiles at a time and
-// skips every tile (or the unstaged rest of the tile after the staged one)
-// that holds no pinned block and does not reach S bytes for the first
-// pending start; the tile where that start's window ends, or where the run
-// closes, is then walked 64 blocks at a time (walk_pass), which resolves the
-// pending starts whose windows end there.  Then the next jump.  Each
-// pending start is resolved once; the walks cover only tiles where windows
-// end, so the cost is O(tiles of the run / 64) record loads plus the blocks
-// of the tiles holding ends, not the length of the run per tile.
-__device__ void long_pass(const Params& P, const Smem& sm, uint32_t lane, uint32_t cur, uint32_t nA,
-                          const Job& job, const TileGeom& tg, const TileState& ts, uint64_t vmask,
-                          uint64_t S, Cand& best, uint64_t& best_end) {
-    const uint64_t a = job.s0 & ~7ull;                   // tile k of the snapshot starts at a + k * kTile
-    const uint64_t rbase = (job.s0 >> kTileLog2) - 1;    // record of tile k >= 1: rbase + k
-    const Ext e = ext_of(P);
-    WalkState ws{tg.t0 + ts.end, ts.xend & vmask, ts.xcend, cur, false};
-    // the staged halo: the first blocks of tile p + 1, already in cq / cc
-    uint64_t hq = 0, hc = 0;
-    uint32_t hr = 0;
-    if (ts.end > tg.nt) {
-        const uint64_t d = ts.xend - sm.x[tg.nt];
-        hq = d & kValMask;
-        hr = static_cast<uint32_t>(d >> kValBits);
-        hc = ts.xcend - sm.xc[tg.nt];
-    }
-    bool jump = true;  // at the region end, then at every tile boundary
-    while (ws.cur < nA && !ws.closed && ws.pos < job.s1) {
-        const uint64_t k = (ws.pos - a) >> kTileLog2;  // the tile holding pos (k >= p + 1)
-        if (jump) {
-            const uint64_t base = sm.x[ws.cur] & vmask;  // bytes before the first pending start
-            const bool mid = ws.pos != a + (k << kTileLog2);  // pos inside tile p + 1, after the halo
-            for (uint64_t kk = k;; kk += 64) {
-                const uint64_t kt = kk + lane;
-                const bool inb = kt < job.tiles;
-                uint64_t rq = 0, rc = 0;
-                uint32_t rr = 1;  // past the snapshot's last tile: a wall
-                bool miss = false;
-                if (inb) {
-                    // a record is complete once its tag is this call's
-                    const uint64_t tag =
-                        __hip_atomic_load(e.rec_tag + rbase + kt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    if (tag == P.epoch) {
-                        rq = __hip_atomic_load(e.rec_p + rbase + kt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        rc = __hip_atomic_load(e.rec_c + rbase + kt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        rr = static_cast<uint32_t>(
-                            __hip_atomic_load(e.rec_r + rbase + kt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-                    } else {
-                        miss = true;
-                    }
-                }
-                // records not published (yet): the wavefront sums those tiles itself
-                for (uint64_t mm = __ballot(miss); mm; mm &= mm - 1) {
-                    const uint32_t j = static_cast<uint32_t>(__builtin_ctzll(mm));
-                    const uint64_t t0 = a + ((kk + j) << kTileLog2);
-                    const Sums t = stream_totals(P, t0, t0 + kTile < job.s1 ? t0 + kTile : job.s1, lane);
-                    if (lane == j) {
-                        rq = t.q;
-                        rc = t.c;
-                        rr = t.r;
-                    }
-                }
-                if (mid && kk == k && lane == 0) {
-                    rq -= hq;
-                    rc -= hc;
-                    rr -= hr;
-                }
-                Sums sm_{rq, rc, rr};
-                wave_inclusive_sum(sm_);  // totals through tile kt
-                // the first tile that holds a pinned block or reaches S bytes
-                const bool stop = !inb || sm_.r != 0 || ws.cq + sm_.q - base >= S;
-                const uint64_t m = __ballot(stop);
-                const uint32_t f = m ? static_cast<uint32_t>(__builtin_ctzll(m)) : 64u;
-                if (f) {
-                    ws.cq += readlane64(sm_.q, f - 1);
-                    ws.cc += readlane64(sm_.c, f - 1);
-                    const uint64_t np = a + ((kk + f) << kTileLog2);
-                    ws.pos = np < job.s1 ? np : job.s1;
-                }
-                if (f < 64) {
-                    // The run closes in tile kk + f when it holds a pinned
-                    // block: if the bytes before that block do not reach S
-                    // for the first pending start, no later one reaches S
-                    // either (the tile after the staged one is walked, since
-                    // the halo may hold pinned blocks before the run starts).
-                    const uint64_t kf = kk + f;
-                    if (kf < job.tiles && (kf != k || !mid) && readlane32(rr, f) != 0) {
-                        const uint64_t t0 = a + (kf << kTileLog2);
-                        const uint64_t fb =
-                            bytes_before_pinned(P, t0, t0 + kTile < job.s1 ? t0 + kTile : job.s1, lane);
-                        if (ws.cq + fb - base < S) ws.closed = true;
-                    }
-                    break;
-                }
-            }
-            if (ws.closed || ws.pos >= job.s1) break;  // no pending start reaches S in the run
+// Boundaries of a staged stretch past the region (a tile at most) and the
+// end keys a merge may read past its last one.
+constexpr uint32_t kEndPad = 64;
+constexpr uint32_t kEndN = kTile + 2 + kEndPad;
+
+// The long kernel's second LDS buffer: the stretch's byte and cost
+// prefixes (entry 0 is the stretch start), and scratch for workgroup
+// reductions and broadcasts.
+struct EndSmem {
+    uint64_t pb[kEndN];
+    uint64_t cb[kEndN];
+    Sums3 wtot[kWaves];
+    uint32_t wpin[kWaves];
+    Key slot[kWaves];
+    uint64_t found;     // the tile the search stopped at
+    uint64_t fq, fc;    // bytes and cost from the region end to that tile's start
+};
+
+// Where the run of a staged region's last run goes on past the region end:
+// the first tile t >= kmin that holds a pinned block past the region end or
+// whose end is at least `need` bytes past it (whole workgroup; every thread
+// gets the same result, through LDS).  Tile records are summed forward from
+// tile kmin, kThreads of them a round; `carry` holds the bytes, cost and
+// pinned count from the region end to the start of tile kmin.  Returns
+// tiles when no tile qualifies; else the tile, with the bytes and cost from
+// the region end to its start in fq, fc.
+__device__ uint64_t find_tile(const Ext& e, EndSmem& es, int64_t rb, uint64_t nrec, uint64_t tiles,
+                              uint64_t kmin, Sums3 carry, uint64_t need, uint64_t& fq, uint64_t& fc) {
+    const uint32_t tid = threadIdx.x;
+    const uint32_t lane = tid & 63u;
+    const uint32_t w = uniform(tid >> 6);
+    for (uint64_t t0 = kmin;; t0 += kThreads) {
+        const uint64_t t = t0 + tid;
+        Sums3 v{0, 0, 1};  // past the snapshot's last tile: a wall
+        if (t < tiles) {
+            const int64_t i = rb + static_cast<int64_t>(t);
+            v = i < 0 || static_cast<uint64_t>(i) >= nrec
+                    ? Sums3{0, 0, 0}
+                    : Sums3{__hip_atomic_load(e.rec_p + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT),
+                            __hip_atomic_load(e.rec_c + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT),
+                            __hip_atomic_load(e.rec_r + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)};
         }
-        // walk the tile holding pos up to its end
-        const uint64_t kw = (ws.pos - a) >> kTileLog2;
-        const uint64_t te = a + ((kw + 1) << kTileLog2);
-        walk_pass(P, sm, lane, nA, te < job.s1 ? te : job.s1, job.s0, job.s1, vmask, S, ws, best,
-                  best_end);
-        jump = true;
+        Sums3 s = v;
+        wave_inclusive_sum3(s);
+        if (lane == 63) es.wtot[w] = s;
+        __syncthreads();
+        Sums3 before = carry, tot = carry;
+        for (uint32_t k = 0; k < kWaves; ++k) {
+            const Sums3 x = es.wtot[k];
+            if (k < w) before = add3(before, x);
+            tot = add3(tot, x);
+        }
+        const Sums3 incl = add3(before, s);  // region end to the end of tile t
+        const bool stop = incl.r != 0 || incl.q >= need;
+        const uint64_t m = __ballot(stop);
+        if (lane == 0) es.wpin[w] = m ? w * 64u + static_cast<uint32_t>(__builtin_ctzll(m)) : kNone32;
+        __syncthreads();
+        uint32_t first = kNone32;
+        for (uint32_t k = 0; k < kWaves; ++k) first = es.wpin[k] < first ? es.wpin[k] : first;
+        if (first != kNone32 && tid == first) {
+            es.found = t;
+            es.fq = incl.q - v.q;
+            es.fc = incl.c - v.c;
+        }
+        __syncthreads();
+        if (first != kNone32) {
+            const uint64_t k = es.found;
+            fq = es.fq;
+            fc = es.fc;
+            __syncthreads();  // es is written again by the next search
+            return k < tiles ? k : tiles;
+        }
+        carry = tot;
     }
+}
+
+// Stages blocks [bs, be) (at most kTile) as byte and cost prefixes from the
+// stretch start (whole workgroup); returns the blocks before the first
+// pinned one (boundaries [0, m] are usable).  The kEndPad keys after
+// boundary m are set above every target.
+__device__ uint32_t stage_stretch(const Params& P, EndSmem& es, uint64_t bs, uint64_t be, uint32_t tid) {
+    const uint32_t lane = tid & 63u;
+    const uint32_t w = uniform(tid >> 6);
+    const uint32_t n = static_cast<uint32_t>(be - bs);
+    const uint32_t i0 = tid * kItems;
+    uint64_t sq[kItems], sc[kItems];
+    Sums3 t{0, 0, 0};
+    uint32_t fp = kNone32;
+#pragma unroll
+    for (uint32_t j = 0; j < kItems; ++j) {
+        const uint32_t i = i0 + j;
+        uint64_t s = 0, c = 0;
+        if (i < n) {
+            const uint32_t k = P.kind[bs + i];
+            s = P.size[bs + i];
+            c = k == COOP_EVICTABLE ? P.cost[bs + i] : 0;
+            if (k >= COOP_PINNED && fp == kNone32) fp = i;
+        }
+        t.q += s;
+        t.c += c;
+        sq[j] = t.q;
+        sc[j] = t.c;
+    }
+    Sums3 wi = t;
+    wave_inclusive_sum3(wi);
+    for (int o = 32; o >= 1; o >>= 1) {
+        const uint32_t x = __shfl_xor(fp, o, 64);
+        fp = x < fp ? x : fp;
+    }
+    if (lane == 63) es.wtot[w] = wi;
+    if (lane == 0) es.wpin[w] = fp;
+    __syncthreads();
+    Sums3 carry{0, 0, 0};
+    uint32_t first = n;
+    for (uint32_t k = 0; k < kWaves; ++k) {
+        if (k < w) carry = add3(carry, es.wtot[k]);
+        first = es.wpin[k] < first ? es.wpin[k] : first;
+    }
+    const uint64_t bq = carry.q + wi.q - t.q, bc = carry.c + wi.c - t.c;
+#pragma unroll
+    for (uint32_t j = 0; j < kItems; ++j) {
+        if (i0 + j < n) {
+            es.pb[i0 + j + 1] = bq + sq[j];
+            es.cb[i0 + j + 1] = bc + sc[j];
+        }
+    }
+    if (tid == 0) {
+        es.pb[0] = 0;
+        es.cb[0] = 0;
+    }
+    __syncthreads();  // the prefixes past the first pinned block are overwritten next
+    if (tid < kEndPad + 1) es.pb[first + 1 + tid] = kNone;
+    __syncthreads();
+    return first;
+}
+
+// This thread's slice of the merge of the pending starts [cur, nA) of the
+// staged region with the stretch's boundaries 1..m.  Start i still needs
+// T_i = S - G - (bytes from i to the region end) past the stretch start (G:
+// the bytes from the region end to the stretch start); it is taken at the
+// first boundary whose prefix reaches T_i, which ends its shortest window.
+// Candidates fold into best / best_end (end snapshot-local).
+__device__ void stretch_merge(const Smem& sm, const EndSmem& es, const TileState& ts, uint64_t vmask,
+                              uint32_t cur, uint32_t nA, uint32_t m, uint64_t S, uint64_t G, uint64_t GC,
+                              uint64_t bs_local, uint32_t tid, Cand& best, uint64_t& best_end) {
+    const uint32_t na = nA - cur, total = na + m;
+    const uint32_t L = merge_steps(total, kThreads);
+    const uint32_t d = tid * L < total ? tid * L : total;
+    auto target = [&](uint32_t i) -> uint64_t {
+        return i < na ? S - G - ((ts.xend - sm.x[cur + i]) & vmask) : kNone;
+    };
+    uint32_t lo = d > m ? d - m : 0, hi = d < na ? d : na;
+    while (lo < hi) {
+        const uint32_t mid = (lo + hi) >> 1;
+        const bool before = target(mid) <= es.pb[d - mid];
+        lo = before ? mid + 1 : lo;
+        hi = before ? hi : mid;
+    }
+    uint32_t ia = lo, ib = d - lo + 1;
+    uint64_t bc = kNone, bx = kNone;
+    uint32_t bi = kNone32, bk = 0;
+    for (uint32_t s = 0; s < L; ++s) {
+        const uint64_t T = target(ia), key = es.pb[ib];
+        const bool take = key >= T;
+        const bool valid = take & (ia < na) & (ib <= m);
+        const uint64_t cost = (ts.xcend - sm.xc[cur + (ia < na ? ia : 0)]) + GC + es.cb[ib];
+        const uint64_t ex = key - T;
+        const bool better = valid & ((cost < bc) | ((cost == bc) & (ex < bx)));
+        bc = better ? cost : bc;
+        bx = better ? ex : bx;
+        bi = better ? cur + ia : bi;
+        bk = better ? ib : bk;
+        ia += take ? 1u : 0u;
+        ib += take ? 0u : 1u;
+    }
+    if (bi != kNone32) {
+        const Cand c{bc, bx, bi};
+        if (cand_less(c, best)) {
+            best = c;
+            best_end = bs_local + bk;
+        }
+    }
+}
+
+// The windows of the pending starts of a staged tile that end more than
+// kWalkCap blocks past the region (whole workgroup; every thread gets the
+// workgroup's key).
+__device__ Key far_windows(const Params& P, const Smem& sm, EndSmem& es, const Job& job,
+                           const TileGeom& tg, const TileState& ts, uint64_t S) {
+    const uint32_t tid = threadIdx.x;
+    const uint32_t lane = tid & 63u;
+    const uint32_t w = uniform(tid >> 6);
+    const uint32_t nA = tg.nt;
+    const uint64_t vmask = ts.packed ? kValMask : kNone;
+    const uint64_t Sc = S < (1ull << kValBits) ? S : (1ull << kValBits);
+    uint32_t cur = pending_start(sm, ts.packed, nA, ts.xend, ts.endrun, S, Sc, lane);
+    Cand best = cand_none();
+    uint64_t best_end = 0;
+    if (cur < nA) {
+        const Ext e = ext_of(P);
+        const uint64_t a = job.s0 & ~7ull;                       // tile k starts at a + k * kTile
+        const int64_t rb = static_cast<int64_t>(job.s0 >> kTileLog2) - 1;  // record of tile k: rb + k
+        const uint64_t nrec = P.num_blocks >> kTileLog2;
+        // the staged part of tile p + 1 (the halo): bytes, cost, pinned count;
+        // from the region end to the start of tile p + 1 is minus these
+        uint64_t hq = 0, hc = 0, hr = 0;
+        if (ts.end > nA) {
+            const uint64_t dd = ts.xend - sm.x[nA];
+            hq = dd & kValMask;
+            hr = dd >> kValBits;
+            hc = ts.xcend - sm.xc[nA];
+        }
+        const uint64_t ge = tg.t0 + ts.end;  // global index of the region end
+        uint64_t kmin = job.p + 1;
+        Sums3 carry{0 - hq, 0 - hc, 0 - hr};  // region end to the start of tile kmin
+        for (;;) {
+            const uint64_t need = S - ((ts.xend - sm.x[cur]) & vmask);
+            uint64_t fq, fc;
+            const uint64_t k = find_tile(e, es, rb, nrec, job.tiles, kmin, carry, need, fq, fc);
+            if (k >= job.tiles) break;  // the run ends with the snapshot, below `need` bytes
+            const uint64_t ks = a + (k << kTileLog2), ke = ks + kTile;
+            const uint64_t bs = ks > ge ? ks : ge, be = ke < job.s1 ? ke : job.s1;
+            // bytes and cost from the region end to the stretch start
+            const uint64_t G = k == job.p + 1 ? 0 : fq;
+            const uint64_t GC = k == job.p + 1 ? 0 : fc;
+            const uint32_t m = stage_stretch(P, es, bs, be, tid);
+            const bool closed = m < be - bs || be == job.s1;
+            stretch_merge(sm, es, ts, vmask, cur, nA, m, S, G, GC, bs - job.s0, tid, best, best_end);
+            // the first start whose window ends past this stretch
+            const uint64_t last = es.pb[m], es_last_c = es.cb[m];
+            const uint32_t nxt = wave_lower_bound(cur, nA, lane, [&](uint32_t i) {
+                return S - G - ((ts.xend - sm.x[i]) & vmask) > last;
+            });
+            __syncthreads();  // the stretch buffer is restaged next
+            if (closed || nxt >= nA) break;
+            // the stretch reached the end of tile k with no pinned block
+            carry = Sums3{G + last, GC + es_last_c, 0};
+            cur = nxt;
+            kmin = k + 1;
+        }
+    }
+    const Key wk = wave_answer(best, best_end, tg.t0 - job.s0, S);
+    if (lane == 0) es.slot[w] = wk;
+    __syncthreads();
+    Key k = es.slot[0];
+    for (uint32_t i = 1; i < kWaves; ++i) k = min_key(k, es.slot[i]);
+    __syncthreads();  // es.slot is written again by the next call
+    return k;
 }
 
 // Unit u of a deferred entry as a job (tile p of snapshot b for slice y,
@@ -1772,33 +1943,15 @@ __device__ bool entry_job(const Params& P, uint4 en, uint32_t u, Cursor& c, Job&
     return job.p < job.tiles;
 }
 
-// The records of the tiles past the first that a deferred entry names: each
-// tile is staged and its totals published (a whole workgroup).
-__device__ void publish_entry_records(const Params& P, Smem& sm, uint4 en) {
-    Cursor c;
-    Job job;
-    for (uint32_t u = en.x; u < en.y; ++u) {
-        if (!entry_job(P, en, u, c, job) || job.p == 0) continue;
-        const TileGeom tg = tile_geom(job);
-        TileRegs regs;
-        issue_loads(P, tg, threadIdx.x, regs);
-        const TileState ts = stage_tile(sm, tg, threadIdx.x, regs);
-        if (threadIdx.x == 0) publish_record(P, job, ts);
-    }
-}
-
 // One deferred entry: the units [lo, hi) of (snapshot b, slice y) that one
 // chunk held, and that chunk's partial slot g of G.  Every tile is staged
-// again.  For each request whose deferral bit is set, the tile's pending
-// starts are cut into kWaves equal parts, one per wavefront, each resolved
-// by long_pass; the wavefronts' answers and the request's partial slot
-// (written by the search kernel) are combined.  Then, as the search kernel
-// would have: the results, or the arrival ticket and the combine when the
-// snapshot spans several chunks; the deferral bits are cleared.
-__device__ void resolve_entry(const Params& P, Smem& sm, uint4 en, uint32_t& last_flag) {
+// again, and for each request whose deferral bit is set its far windows
+// (far_windows) are folded into the request's partial slot, which the
+// search kernel wrote.  Then, as the search kernel would have: the results,
+// or the arrival ticket and the combine when the snapshot spans several
+// chunks; the deferral bits are cleared.
+__device__ void resolve_entry(const Params& P, Smem& sm, EndSmem& es, uint4 en, uint32_t& last_flag) {
     const uint32_t tid = threadIdx.x;
-    const uint32_t lane = tid & 63u;
-    const uint32_t w = uniform(tid >> 6);
     Cursor c;
     Job job;
     for (uint32_t u = en.x; u < en.y; ++u) {
@@ -1807,57 +1960,21 @@ __device__ void resolve_entry(const Params& P, Smem& sm, uint4 en, uint32_t& las
         TileRegs regs;
         issue_loads(P, tg, tid, regs);
         const TileState ts = stage_tile(sm, tg, tid, regs);
-        const uint32_t nt = tg.nt;
-        const bool open = tg.t0 + ts.end < job.s1;
-        const uint64_t vmask = ts.packed ? kValMask : kNone;
-        const uint64_t tl = tg.t0 - job.s0;
-        if (open && nt != 0) {
-            // tasks (request r, part): parts = kWaves / (the requests, rounded
-            // up to a power of two, at most kWaves); wavefront w takes task
-            // t0 + w of each round
-            uint32_t k2 = 1;
-            while (k2 < job.K && k2 < kWaves) k2 <<= 1;
-            const uint32_t parts = kWaves / k2;
-            for (uint64_t t0 = 0; t0 < job.K * parts; t0 += kWaves) {
-                const uint64_t t = t0 + w;
-                const uint64_t r = t / parts;
-                const uint32_t part = static_cast<uint32_t>(t % parts);
-                Key k = key_none();
-                if (r < job.K) {
-                    const uint64_t q = job.q0 + job.y + (r << P.slices_log2);
-                    const uint64_t bit = q * P.pc + job.g;
-                    // (only this entry changes the bit)
-                    const uint32_t word = uniform(ext_of(P).bits[bit >> 5]);
-                    const uint64_t S = ld_const(P.req_size, q);
-                    if (((word >> (bit & 31u)) & 1u) && S != 0) {
-                        const uint64_t Sc = S < (1ull << kValBits) ? S : (1ull << kValBits);
-                        const uint32_t cur =
-                            pending_start(sm, ts.packed, nt, ts.xend, ts.endrun, S, Sc, lane);
-                        if (cur < nt) {
-                            const uint32_t len = nt - cur;
-                            const uint32_t c0 = cur + len * part / parts;
-                            const uint32_t c1 = cur + len * (part + 1) / parts;
-                            Cand best = cand_none();
-                            uint64_t best_end = 0;
-                            if (c0 < c1)
-                                long_pass(P, sm, lane, c0, c1, job, tg, ts, vmask, S, best, best_end);
-                            k = wave_answer(best, best_end, tl, S);
-                        }
-                    }
-                }
-                if (parts > 1) {
-                    if (lane == 0) sm.slot[w] = k;
-                    __syncthreads();
-                    for (uint32_t i = 1; i < parts; ++i) k = min_key(k, sm.slot[w + i]);
-                }
-                // part 0's wavefront folds the request's key into its slot;
-                // the same lane does so for request r on every tile
-                if (part == 0 && r < job.K && lane == 0 && k.start != kNone) {
-                    const uint64_t q = job.q0 + job.y + (r << P.slices_log2);
+        if (tg.t0 + ts.end < job.s1 && tg.nt != 0) {  // the region's last run may go on
+            for (uint64_t r = 0; r < job.K; ++r) {
+                const uint64_t q = job.q0 + job.y + (r << P.slices_log2);
+                const uint64_t bit = q * P.pc + job.g;
+                // (only this entry changes the bit)
+                const uint32_t word = uniform(__hip_atomic_load(ext_of(P).bits + (bit >> 5), __ATOMIC_RELAXED,
+                                                                __HIP_MEMORY_SCOPE_AGENT));
+                const uint64_t S = ld_const(P.req_size, q);
+                if (!((word >> (bit & 31u)) & 1u) || S == 0) continue;
+                const Key k = far_windows(P, sm, es, job, tg, ts, S);
+                // the same thread folds the request's key on every tile
+                if (tid == 0 && k.start != kNone) {
                     Key* slot = P.part + q * P.pc + job.g;
                     store_key_device(slot, min_key(load_key_device(slot), k));
                 }
-                if (parts > 1) __syncthreads();  // sm.slot is written again
             }
         }
         __syncthreads();  // LDS is restaged next
@@ -1878,31 +1995,31 @@ __device__ void resolve_entry(const Params& P, Smem& sm, uint4 en, uint32_t& las
     __syncthreads();  // last_flag and LDS are used by the next entry
 }
 
-// Finishes the jobs the search kernel deferred, after it on the stream (so
-// every tile record and partial key is in place).  With nothing deferred
-// (the list's word carries an older tag) every workgroup returns at once.
+// Finishes the jobs the search kernel deferred, after it on the stream.
+// With nothing deferred (the list's word carries an older tag) every
+// workgroup returns at once.  One workgroup per CU (the second LDS buffer);
+// no workgroup waits for another.
 __global__ __launch_bounds__(kThreads, 2) void coop_window_long_kernel(Params Pin) {
     __shared__ Smem sm;
+    __shared__ EndSmem es;
     __shared__ uint32_t last_flag;
     Params P = Pin;
     graph_tags(P);
     const Ext ex = ext_of(P);
     const uint64_t word = __hip_atomic_load(ex.defer_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    uint64_t n = (word >> 32) == P.qtag ? (word & 0xffffffffull) : 0;
+    // The loop bound and the entry words are wave-uniform values in scalar
+    // registers: loop control that the compiler saw as divergent put a
+    // reload of the bound under a partial execution mask and ended the loop
+    // early for some workgroups.
+    uint32_t n = (uniform(static_cast<uint32_t>(word >> 32)) == P.qtag) ? uniform(static_cast<uint32_t>(word)) : 0u;
     if (n > P.defer_cap) n = P.defer_cap;
-    // first the tile records of every entry (a tile whose record is not out
-    // yet when a jump needs it is summed by that wavefront), then the entries
-    for (uint64_t e = blockIdx.x; e < n; e += gridDim.x) {
-        const uint4 en = ex.entries[e];
-        if (en.x >= en.y || en.y > P.units || en.w == 0 || en.w > P.pc || en.z >= en.w) continue;
-        publish_entry_records(P, sm, en);
-    }
-    for (uint64_t e = blockIdx.x; e < n; e += gridDim.x) {
-        const uint4 en = ex.entries[e];
+    if (n == 0) return;
+    for (uint32_t e = blockIdx.x; e < n; e += gridDim.x) {
+        const uint4 en = load_entry_device(ex.entries + e);
         // (entries are written by this call's search kernel; the checks keep
         // every access in bounds whatever the workspace holds)
         if (en.x >= en.y || en.y > P.units || en.w == 0 || en.w > P.pc || en.z >= en.w) continue;
-        resolve_entry(P, sm, en, last_flag);
+        resolve_entry(P, sm, es, en, last_flag);
     }
 }
 
@@ -1924,7 +2041,7 @@ struct Plan {
     uint64_t defer_cap;    // deferred entries, at most
     size_t off_defer;      // the deferred list's word, then its entries
     size_t off_entries;
-    size_t off_rec;        // tile records: bytes, costs, pinned counts, tags (u64 each)
+    size_t off_rec;        // tile records: bytes, costs, pinned counts (u64 each)
     uint64_t num_rec;
     size_t off_bits;       // deferral bits, one per partial slot
     size_t bytes;          // total workspace
@@ -1964,7 +2081,7 @@ bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests
     slices = 1ull << slices_log2;
     if (slices * nv >= (1ull << 32)) return false;
     // deferred entries are counted in 32 bits
-    if ((num_blocks / 8186) * slices + slices * nv + kGridWGs >= (1ull << 32)) return false;
+    if ((num_blocks / kDeferMin) * slices + slices * nv + kGridWGs >= (1ull << 32)) return false;
     pl->num_virtual = nv;
     pl->slices = slices;
     pl->slices_log2 = slices_log2;
@@ -2018,15 +2135,15 @@ bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests
     // (the kernels derive these offsets from the queue word's address: see
     // Ext; the workspace is 256-byte aligned, so aligning offsets aligns
     // addresses)
-    // A job defers only when a window runs past the tile after the staged
-    // one, so its snapshot has at least three tiles (more than 8185
-    // blocks).  The chunk parts of such jobs number at most the jobs plus
-    // the chunk boundaries (each falls inside at most one job).
-    const uint64_t big = num_blocks / 8186 < num_segments ? num_blocks / 8186 : num_segments;
+    // A job defers only when a window runs more than kWalkCap blocks past
+    // its staged region, so its snapshot has at least kDeferMin blocks.
+    // The chunk parts of such jobs number at most the jobs plus the chunk
+    // boundaries (each falls inside at most one job).
+    const uint64_t big = num_blocks / kDeferMin < num_segments ? num_blocks / kDeferMin : num_segments;
     pl->defer_cap = nchunks + slices * big;
     pl->num_rec = num_blocks >> kTileLog2;
     pl->off_rec = pl->off_entries + pl->defer_cap * sizeof(uint4);
-    pl->off_bits = pl->off_rec + pl->num_rec * 4 * sizeof(uint64_t);
+    pl->off_bits = pl->off_rec + pl->num_rec * 3 * sizeof(uint64_t);
     // (+32: the layout stays inside even if the workspace is only 8-byte aligned)
     pl->bytes = pl->off_bits + (num_requests * pc + 31) / 32 * sizeof(uint32_t) + 32;
     return true;

@@ -60,14 +60,15 @@ def test_workspace_size_depends_on_counts_only():
     # partial storage is bounded: 2^23 keys of 32 bytes, one counter per
     # (request slice, snapshot) -- at most 256 slices -- the queue, tag and
     # deferred-list words, a deferred entry (16 bytes) per chunk and per
-    # (slice, snapshot of three tiles or more), a 32-byte record per tile and
-    # a deferral bit per partial key
+    # (slice, snapshot that can defer), a 24-byte record per tile and a
+    # deferral bit per partial key
     p = coop.plan_info(1 << 30, 1, 1 << 20)
     keys = (1 << 20) * p["partial_slots"]
     assert keys <= 1 << 23
+    nrec = (1 << 30) >> 12
     assert coop.workspace_size(1 << 30, 1, 1 << 20) <= (
         keys * 32 + 256 * 8 + 24 + 256 + 16 * (p["chunks_max"] + 256) + 16
-        + 32 * ((1 << 30) >> 12) + keys // 8 + 64)
+        + 24 * nrec + keys // 8 + 64)
     lib = coop.load_library()
     assert lib.coop_window_search_workspace_size(1, 1, 1, None) == -1
     out = ctypes.c_size_t()
