@@ -1080,6 +1080,23 @@ __device__ __forceinline__ TileState stage_tile(Smem& sm, const TileGeom& tg, ui
     return ts;
 }
 
+// A ticket on a tagged counter (tag << shift | arrivals), which an earlier
+// call may have left with its own tag: the first arrival of this call swaps
+// in tag | 1; every later one, once it sees this call's tag, adds 1, so
+// arrivals that come together queue at the atomic unit instead of retrying
+// compare-and-swaps.  The count stays below 2^shift.  Returns the ticket,
+// from 1.
+__device__ uint64_t take_ticket(uint64_t* ctr, uint64_t tag, uint32_t shift) {
+    uint64_t old = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    while ((old >> shift) != tag) {
+        if (__hip_atomic_compare_exchange_strong(ctr, &old, (tag << shift) | 1ull, __ATOMIC_RELAXED,
+                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+            return 1;
+    }
+    const uint64_t prev = __hip_atomic_fetch_add(ctr, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return (prev & ((1ull << shift) - 1)) + 1;
+}
+
 // Partial keys are read by whichever workgroup takes a snapshot's last
 // ticket, possibly on another XCD, and the XCDs' L2 caches are not coherent
 // with each other.  They are written and read with device-scope relaxed
@@ -1337,13 +1354,7 @@ __device__ void combine_partials(const Params& P, const Job& job, uint32_t tid, 
     __syncthreads();
     if (tid == 0) {
         uint64_t* ctr = P.counters + static_cast<uint64_t>(job.y) * P.num_segments + job.b;
-        uint64_t old = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        uint64_t want;
-        do {
-            want = (old >> kEpochShift) == P.epoch ? old + 1 : (P.epoch << kEpochShift) | 1ull;
-        } while (!__hip_atomic_compare_exchange_strong(ctr, &old, want, __ATOMIC_RELAXED,
-                                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-        last_flag = (want & ((1ull << kEpochShift) - 1)) == job.G;
+        last_flag = take_ticket(ctr, P.epoch, kEpochShift) == job.G;
     }
     __syncthreads();
     if (!last_flag) return;
@@ -1498,13 +1509,7 @@ __device__ __forceinline__ void finish_held(const Params& P, const Job& job, uin
 // first append of a call restarts the count.
 __device__ void defer_job(const Params& P, const Job& job) {
     const Ext e = ext_of(P);
-    uint64_t old = __hip_atomic_load(e.defer_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    uint64_t want;
-    do {
-        want = (old >> 32) == P.qtag ? old + 1 : (static_cast<uint64_t>(P.qtag) << 32) | 1ull;
-    } while (!__hip_atomic_compare_exchange_strong(e.defer_word, &old, want, __ATOMIC_RELAXED,
-                                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-    const uint64_t idx = (want & 0xffffffffull) - 1;
+    const uint64_t idx = take_ticket(e.defer_word, P.qtag, 32) - 1;
     if (idx < P.defer_cap) store_entry_device(e.entries + idx, make_uint4(job.lo, job.hi, job.g, job.G));
 }
 
