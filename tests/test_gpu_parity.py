@@ -99,6 +99,55 @@ def test_tile_edges_and_ragged_tails():
     assert_parity(pools, gpu_search(pools), "tile edges")
 
 
+def _clustered_kinds(rng, n, pinned_mean, open_mean):
+    """Alternating pinned and open stretches of geometric lengths; inside an
+    open stretch a fifth of the blocks are free."""
+    kind = np.empty(n, dtype=np.uint8)
+    i, pinned = 0, bool(rng.random() < 0.5)
+    while i < n:
+        m = int(rng.geometric(1.0 / (pinned_mean if pinned else open_mean)))
+        kind[i:i + m] = 2 if pinned else np.where(rng.random(min(m, n - i)) < 0.2, 0, 1)
+        i += m
+        pinned = not pinned
+    return kind
+
+
+def test_clustered_pinned_stretches():
+    """Clustered pinned stretches of mean length 1.2 to 40 between open runs
+    of mean length 2 to 30, stretches across tile edges and the start of the
+    halo, snapshots almost all pinned, long open runs between dense pinned
+    clusters (windows that leave the staged region), and costs from a tiny
+    range so that ties decide by the start."""
+    _announce("clustered pinned stretches")
+    rng = np.random.default_rng(19)
+    snaps, reqs = [], []
+    for s in range(36):
+        n = int(rng.integers(1, 5 * TILE + 300))
+        pm, om = [(2, 6), (3.3, 7.8), (8, 4), (40, 10), (1.2, 30), (2, 2)][s % 6]
+        kind = _clustered_kinds(rng, n, pm, om)
+        if s % 4 == 0:  # pinned across tile edges and the start of the halo
+            for e in range(TILE, n, TILE):
+                kind[max(0, e - 5):min(n, e + 7)] = 2
+        if s % 9 == 4:  # almost all pinned
+            kind[:] = 2
+            kind[rng.integers(0, n, size=max(1, n // 50))] = 1
+        if s % 7 == 3 and n > 3 * TILE:  # a long open run between dense clusters
+            a = int(rng.integers(0, n - 2 * TILE))
+            kind[a:a + 2 * TILE] = np.where(rng.random(2 * TILE) < 0.2, 0, 1)
+        size = (rng.integers(1, 64, size=n) * 512).astype(np.uint64)
+        hi = 4 if s % 2 else 10**6
+        cost = rng.integers(0, hi, size=n).astype(np.uint64)
+        snaps.append((size, cost, kind))
+        tot = int(size[kind < 2].sum())
+        mean = int(size.mean())
+        reqs.append([1, 512, mean, 4 * mean, 50 * mean, 3000 * mean, tot // 3, tot,
+                     int(rng.integers(1, max(2, tot)))])
+    pools = _pools(snaps, reqs)
+    got = gpu_search(pools)
+    assert_parity(pools, got, "clustered pinned stretches")
+    check_results(pools, got)
+
+
 def test_runs_longer_than_the_staged_region():
     """One pin-free run far longer than tile + halo: windows of thousands of
     blocks cross many tiles and are finished by the streaming pass."""
