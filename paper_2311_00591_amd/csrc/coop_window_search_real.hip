@@ -29,7 +29,8 @@
 //      for each chunk it stages packed byte/pinned-count keys and cost
 //      prefixes of up to 2561 indices (the chunk and the blocks after it)
 //      in LDS, then runs every request of the group that shares the
-//      snapshot as a merge path (see the kernel).  A window [i, k) is valid
+//      snapshot as a merge path, each on its own wavefronts (see the
+//      kernel).  A window [i, k) is valid
 //      iff it holds no pinned block; its cost is C[k] - C[i].  Each
 //      wavefront's minimum is kept per request in LDS; their least goes to
 //      the request's partial slot.
@@ -63,12 +64,15 @@ constexpr uint32_t kPackBits = 51;
 constexpr uint64_t kPackOne = 1ull << kPackBits;
 static_assert(kStage < (1u << (63 - kPackBits)), "packed keys stay below 2^63");
 constexpr uint64_t kEndKey = ~0ull;  // above every target: stops every merge
-// Every lane walks the same number of merge steps, at most this many; a lane
-// whose slice ends earlier goes on into its neighbour's (the same windows
-// again) or past the end keys, into this many more sentinel keys.
-constexpr uint32_t kPadSteps = 32;
-static_assert(kPadSteps >= (kChunk + kStage + kThreads - 1) / kThreads, "padding covers a slice");
-constexpr uint32_t kStageBatch = 11;            // staged indices per thread whose loads go together
+// Every lane of a request walks the same number of merge steps, at most this
+// many (one wavefront's share of a chunk's merge); a lane whose slice ends
+// earlier goes on into its neighbour's (the same windows again) or past the
+// end keys, into this many more sentinel keys.
+constexpr uint32_t kPadSteps = 80;
+static_assert(kPadSteps >= (kChunk + kStage + 63) / 64, "padding covers a wavefront's slice");
+constexpr uint32_t kSThreads = 512;             // threads of a search workgroup
+constexpr uint32_t kSWaves = kSThreads / 64;
+constexpr uint32_t kStageBatch = 5;             // staged indices per thread whose loads go together
 constexpr uint32_t kMaxGroup = 16;              // requests per search workgroup
 constexpr uint32_t kTargetGroups = 4096;        // search workgroups aimed for
 constexpr uint64_t kResidentUnits = 512;        // search workgroups the chip holds at once
@@ -495,8 +499,9 @@ __device__ void walk_global(const Prefix& pf, uint64_t i, uint64_t i_end, uint64
 
 // The merge path of NR requests over one staged chunk, interleaved so that
 // their chains of LDS reads overlap: targets Y[i] + S (starts i < nA) against
-// end keys Y[1..nB].  Each lane bisects its diagonal (a fixed 12 rounds: the
-// range is at most nA + 1 <= 2049) and walks the same number of steps; a
+// end keys Y[1..nB], split over `lanes` lanes (this one is lane gl).  Each
+// lane bisects its diagonal (a fixed 12 rounds: the range is at most
+// nA + 1 <= 2049) and walks the same number of steps; a
 // start meets, when it is merged, the first end key at or above its target,
 // the end of its shortest window, and is scored on the spot (valid iff the
 // keys differ by less than 2^51: no pinned block between).  mine[r] receives
@@ -504,11 +509,10 @@ __device__ void walk_global(const Prefix& pf, uint64_t i, uint64_t i_end, uint64
 template <int NR>
 __device__ __forceinline__ void merge_requests(const uint64_t* Y, const U128* Cr, uint32_t nA,
                                                uint32_t nB, const uint64_t (&S)[NR], uint64_t c0,
-                                               Best (&mine)[NR]) {
-    const uint32_t tid = threadIdx.x;
+                                               uint32_t gl, uint32_t lanes, Best (&mine)[NR]) {
     const uint32_t M = nA + nB;
-    const uint32_t Ls = (M + kThreads - 1) / kThreads;
-    const uint32_t d = tid * Ls < M ? tid * Ls : M;
+    const uint32_t Ls = (M + lanes - 1) / lanes;
+    const uint32_t d = gl * Ls < M ? gl * Ls : M;
     uint32_t lo[NR], hi[NR];
 #pragma unroll
     for (int r = 0; r < NR; ++r) {
@@ -575,13 +579,15 @@ __device__ __forceinline__ void merge_requests(const uint64_t* Y, const U128* Cr
 // number of steps, scoring each start it takes on the spot.  Starts whose
 // target lies above every staged end key (windows reaching past hi) are
 // walked from the global prefixes, as are whole chunks whose bytes or
-// request break the packed-key bounds.  Each wavefront keeps its own least
-// window per request, so a request costs no barrier; the wavefronts' minima
-// meet once per unit.
-__global__ __launch_bounds__(kThreads) void real_search_kernel(Prefix pf, SearchArgs A) {
+// request break the packed-key bounds.  A request's merge is split over
+// wpr wavefronts (one when a snapshot has eight requests or more in the
+// workgroup, so that each lane's bisection serves a long slice), and every
+// wavefront keeps its own least window per request, so a request costs no
+// barrier; the wavefronts' minima meet once per unit.
+__global__ __launch_bounds__(kSThreads, 4) void real_search_kernel(Prefix pf, SearchArgs A) {
     __shared__ uint64_t Y[kStage + 1 + kPadSteps + 1];
     __shared__ U128 Cr[kStage + 1 + kPadSteps + 1];
-    __shared__ Best bestw[kWaves][kMaxGroup];
+    __shared__ Best bestw[kSWaves][kMaxGroup];
     __shared__ int big_flag;
     const uint32_t tid = threadIdx.x, lane = tid & 63u, w = tid >> 6;
     for (uint64_t L = blockIdx.x; L < A.units; L += gridDim.x) {
@@ -595,6 +601,15 @@ __global__ __launch_bounds__(kThreads) void real_search_kernel(Prefix pf, Search
             const uint64_t s0 = A.seg[b], nend = A.seg[b + 1], nb = nend - s0;
             // slice g of the snapshot's starts (nb * g fits: nb < 2^40, g < 2^10)
             const uint64_t a = s0 + nb * g / A.parts, e = s0 + nb * (g + 1) / A.parts;
+            // The m requests [r, rend) of snapshot b: wpr wavefronts per
+            // request (a power of two, wpr * m <= kSWaves when m allows),
+            // conc requests at once; wavefront w serves requests j with
+            // j % conc == w / wpr, on lanes gl of `lanes`.
+            const uint32_t m = static_cast<uint32_t>(rend - r);
+            uint32_t wpr = 1;
+            while (wpr < kSWaves && 2 * wpr * m <= kSWaves) wpr *= 2;
+            const uint32_t conc = kSWaves / wpr, slot = w / wpr;
+            const uint32_t gl = (w % wpr) * 64u + lane, lanes = 64u * wpr;
             for (uint64_t c0 = a; c0 < e; c0 += kChunk) {
                 const uint64_t c1 = c0 + kChunk < e ? c0 + kChunk : e;
                 const uint64_t hi = c0 + kStage < nend ? c0 + kStage : nend;  // staged [c0, hi]
@@ -610,12 +625,12 @@ __global__ __launch_bounds__(kThreads) void real_search_kernel(Prefix pf, Search
                 // more could wrap the staged byte count: P(x + 1) - P(x) is
                 // checked in the same pass.
                 bool big = false;
-                for (uint64_t xb = c0 + tid; xb <= hi; xb += kStageBatch * kThreads) {
+                for (uint64_t xb = c0 + tid; xb <= hi; xb += kStageBatch * kSThreads) {
                     uint64_t pv[kStageBatch], pn[kStageBatch], rv[kStageBatch];
                     U128 cv[kStageBatch];
 #pragma unroll
                     for (uint32_t j = 0; j < kStageBatch; ++j) {
-                        const uint64_t xj = xb + j * kThreads;
+                        const uint64_t xj = xb + j * kSThreads;
                         const uint64_t x = xj < hi ? xj : hi;
                         const uint64_t xn = x < hi ? x + 1 : x;
                         pv[j] = pf.P(x);
@@ -625,7 +640,7 @@ __global__ __launch_bounds__(kThreads) void real_search_kernel(Prefix pf, Search
                     }
 #pragma unroll
                     for (uint32_t j = 0; j < kStageBatch; ++j) {
-                        const uint64_t x = xb + j * kThreads;
+                        const uint64_t x = xb + j * kSThreads;
                         if (x <= hi) {
                             const uint64_t pr = pv[j] - pbase;
                             big |= (pr >= kPackOne) | (pn[j] - pv[j] >= kPackOne);
@@ -644,7 +659,7 @@ __global__ __launch_bounds__(kThreads) void real_search_kernel(Prefix pf, Search
                 const uint64_t span = packed_chunk ? Y[nB] & (kPackOne - 1) : 0;
                 // starts whose target is above every staged end key: their windows
                 // end past hi (or nowhere); a suffix of the chunk, walked globally
-                // (true when some start of the chunk was walked globally)
+                // by the request's lanes (true when some start was walked)
                 auto pending = [&](uint64_t S, Best& mine) -> bool {
                     if (hi >= nend) return false;
                     uint32_t plo = 0, phi = nA;
@@ -655,8 +670,8 @@ __global__ __launch_bounds__(kThreads) void real_search_kernel(Prefix pf, Search
                     }
                     const uint64_t np = nA - plo;
                     if (np) {
-                        const uint64_t per = (np + kThreads - 1) / kThreads;
-                        const uint64_t q0 = c0 + plo + tid * per;
+                        const uint64_t per = (np + lanes - 1) / lanes;
+                        const uint64_t q0 = c0 + plo + gl * per;
                         walk_global(pf, q0 < c1 ? q0 : c1, q0 + per < c1 ? q0 + per : c1, nend, S,
                                     mine);
                     }
@@ -665,45 +680,46 @@ __global__ __launch_bounds__(kThreads) void real_search_kernel(Prefix pf, Search
                 auto fast = [&](uint64_t S) {
                     return S != 0 && packed_chunk && S <= kPackOne - span;
                 };
-                for (uint64_t rr = r; rr < rend;) {
-                    const uint64_t S0 = A.req_sizes[rr];
-                    const bool pair = rr + 1 < rend;
-                    const uint64_t S1 = pair ? A.req_sizes[rr + 1] : 0;
+                // this wavefront's least window of request j into its slot
+                auto keep = [&](uint32_t j, const Best& best) {
+                    if (lane == 0 && best_less(best, bestw[w][r + j - r0])) bestw[w][r + j - r0] = best;
+                };
+                // Requests j and j + conc go together: when both are packed,
+                // their merges are interleaved (independent chains of LDS reads).
+                for (uint32_t j = slot; j < m; j += 2 * conc) {
+                    const uint64_t S0 = A.req_sizes[r + j];
+                    const bool pair = j + conc < m;
+                    const uint64_t S1 = pair ? A.req_sizes[r + j + conc] : 0;
                     if (pair && fast(S0) && fast(S1)) {
-                        // two requests' merges interleaved: independent chains of LDS reads
                         const uint64_t SS[2] = {S0, S1};
                         Best m2[2] = {best_none(), best_none()};
-                        merge_requests<2>(Y, Cr, nA, nB, SS, c0, m2);
+                        merge_requests<2>(Y, Cr, nA, nB, SS, c0, gl, lanes, m2);
 #pragma unroll
-                        for (uint32_t j = 0; j < 2; ++j) {
-                            const bool walked = pending(SS[j], m2[j]);
-                            const Best m = to_local(
-                                walked ? wave_min(m2[j]) : wave_min_chunk(m2[j], c0), s0);
-                            if (lane == 0 && best_less(m, bestw[w][rr + j - r0]))
-                                bestw[w][rr + j - r0] = m;
+                        for (uint32_t u = 0; u < 2; ++u) {
+                            const bool walked = pending(SS[u], m2[u]);
+                            keep(j + u * conc, to_local(walked ? wave_min(m2[u]) : wave_min_chunk(m2[u], c0), s0));
                         }
-                        rr += 2;
                         continue;
                     }
-                    if (S0 != 0) {
+                    for (uint32_t u = 0; u < (pair ? 2u : 1u); ++u) {
+                        const uint64_t S = u ? S1 : S0;
+                        if (S == 0) continue;
                         Best mine = best_none();
-                        if (fast(S0)) {
-                            const uint64_t SS[1] = {S0};
+                        if (fast(S)) {
+                            const uint64_t SS[1] = {S};
                             Best m1[1] = {best_none()};
-                            merge_requests<1>(Y, Cr, nA, nB, SS, c0, m1);
+                            merge_requests<1>(Y, Cr, nA, nB, SS, c0, gl, lanes, m1);
                             mine = m1[0];
-                            pending(S0, mine);
+                            pending(S, mine);
                         } else {
                             // the packed keys would not decide correctly: global walk
-                            const uint64_t per = (nA + kThreads - 1) / kThreads;
-                            const uint64_t i0 = c0 + tid * per;
+                            const uint64_t per = (nA + lanes - 1) / lanes;
+                            const uint64_t i0 = c0 + gl * per;
                             walk_global(pf, i0 < c1 ? i0 : c1, i0 + per < c1 ? i0 + per : c1,
-                                        nend, S0, mine);
+                                        nend, S, mine);
                         }
-                        const Best m = to_local(wave_min(mine), s0);
-                        if (lane == 0 && best_less(m, bestw[w][rr - r0])) bestw[w][rr - r0] = m;
+                        keep(j + u * conc, to_local(wave_min(mine), s0));
                     }
-                    rr += 1;
                 }
             }
             r = rend;
@@ -711,7 +727,7 @@ __global__ __launch_bounds__(kThreads) void real_search_kernel(Prefix pf, Search
         __syncthreads();
         if (tid < r1 - r0) {
             Best m = bestw[0][tid];
-            for (uint32_t v = 1; v < kWaves; ++v)
+            for (uint32_t v = 1; v < kSWaves; ++v)
                 if (best_less(bestw[v][tid], m)) m = bestw[v][tid];
             A.slots[(r0 + tid) * A.parts + g] = m;
         }
@@ -850,7 +866,7 @@ coop_status_t coop_window_search_real(const uint64_t* size, const double* h, con
     const SearchArgs A{seg_offsets, num_segments, req_sizes, req_offsets, num_requests,
                        l.group, l.parts, l.units, slots};
     const uint32_t search_grid = static_cast<uint32_t>(l.units < (1u << 20) ? l.units : (1u << 20));
-    hipLaunchKernelGGL(real_search_kernel, dim3(search_grid), dim3(kThreads), 0, s, pf, A);
+    hipLaunchKernelGGL(real_search_kernel, dim3(search_grid), dim3(kSThreads), 0, s, pf, A);
     if (hipGetLastError() != hipSuccess) return COOP_ERR_HIP;
     const uint32_t reduce_grid = static_cast<uint32_t>((num_requests + kThreads - 1) / kThreads);
     hipLaunchKernelGGL(real_reduce_kernel, dim3(reduce_grid), dim3(kThreads), 0, s, A, out);
