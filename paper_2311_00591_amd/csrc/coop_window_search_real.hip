@@ -270,43 +270,38 @@ __global__ __launch_bounds__(kThreads, 4) void real_tile_kernel(
         if (tile_bad) all.r |= kBadTile;
         __syncthreads();
         run = add_tri(run, Tri{inc.p - mine.p, sub128(inc.c, mine.c), inc.r - mine.r});
-        uint64_t op[kItems], oc_lo[kItems], oc_hi[kItems];
-        uint16_t orr[kItems];
-#pragma unroll
-        for (uint32_t u = 0; u < kItems; ++u) {
-            op[u] = run.p;
-            oc_lo[u] = run.c.lo;
-            oc_hi[u] = run.c.hi;
-            orr[u] = static_cast<uint16_t>(run.r);
-            run.p += sz[u];
-            run.c = add128(run.c, cq[u]);
-            run.r += (pin >> u) & 1u;
-        }
+        // each pair of prefixes goes out as soon as it is known, so that few
+        // of them are held in registers at once
         if (full) {  // the workspace arrays are 256-byte aligned
+            uint32_t rw[kItems / 2];
 #pragma unroll
             for (uint32_t v = 0; v < kItems / 2; ++v) {
-                reinterpret_cast<ulonglong2*>(pl + base)[v] = ulonglong2{op[2 * v], op[2 * v + 1]};
-                reinterpret_cast<ulonglong2*>(cl_lo + base)[v] =
-                    ulonglong2{oc_lo[2 * v], oc_lo[2 * v + 1]};
-                reinterpret_cast<ulonglong2*>(cl_hi + base)[v] =
-                    ulonglong2{oc_hi[2 * v], oc_hi[2 * v + 1]};
+                const Tri a = run;
+                run.p += sz[2 * v];
+                run.c = add128(run.c, cq[2 * v]);
+                run.r += (pin >> (2 * v)) & 1u;
+                reinterpret_cast<ulonglong2*>(pl + base)[v] = ulonglong2{a.p, run.p};
+                reinterpret_cast<ulonglong2*>(cl_lo + base)[v] = ulonglong2{a.c.lo, run.c.lo};
+                reinterpret_cast<ulonglong2*>(cl_hi + base)[v] = ulonglong2{a.c.hi, run.c.hi};
+                rw[v] = static_cast<uint32_t>(a.r & 0xffffu) | (static_cast<uint32_t>(run.r & 0xffffu) << 16);
+                run.p += sz[2 * v + 1];
+                run.c = add128(run.c, cq[2 * v + 1]);
+                run.r += (pin >> (2 * v + 1)) & 1u;
             }
-            uint4 r8;
-            r8.x = orr[0] | (static_cast<uint32_t>(orr[1]) << 16);
-            r8.y = orr[2] | (static_cast<uint32_t>(orr[3]) << 16);
-            r8.z = orr[4] | (static_cast<uint32_t>(orr[5]) << 16);
-            r8.w = orr[6] | (static_cast<uint32_t>(orr[7]) << 16);
-            *reinterpret_cast<uint4*>(rl + base) = r8;
+            *reinterpret_cast<uint4*>(rl + base) = make_uint4(rw[0], rw[1], rw[2], rw[3]);
         } else {
 #pragma unroll
             for (uint32_t u = 0; u < kItems; ++u) {
                 const uint64_t k = base + u;
                 if (k <= n) {
-                    pl[k] = op[u];
-                    cl_lo[k] = oc_lo[u];
-                    cl_hi[k] = oc_hi[u];
-                    rl[k] = orr[u];
+                    pl[k] = run.p;
+                    cl_lo[k] = run.c.lo;
+                    cl_hi[k] = run.c.hi;
+                    rl[k] = static_cast<uint16_t>(run.r);
                 }
+                run.p += sz[u];
+                run.c = add128(run.c, cq[u]);
+                run.r += (pin >> u) & 1u;
             }
         }
         if (tid == 0) tot[t] = all;
