@@ -1100,10 +1100,11 @@ __device__ uint64_t take_ticket(uint64_t* ctr, uint64_t tag, uint32_t shift) {
 // Partial keys are read by whichever workgroup takes a snapshot's last
 // ticket, possibly on another XCD, and the XCDs' L2 caches are not coherent
 // with each other.  They are written and read with device-scope relaxed
-// atomics, which act at the device-coherent level: publishing them then
-// needs only the writes to have completed before the ticket is taken, and
-// no cache write-back or invalidation (which a device-scope fence would
-// cost on every combine, for the whole L2).
+// atomics, which act at the device-coherent level (stores written through,
+// loads served from there): publishing them needs only the writes to have
+// completed before the ticket is taken, and no L2 write-back, which a
+// release on every writer would cost on every combine.  The reader issues
+// its loads only after its ticket has come back, behind an acquire.
 __device__ __forceinline__ void store_key_device(Key* p, const Key& k) {
     __hip_atomic_store(&p->cost, k.cost, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(&p->bytes, k.bytes, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1358,6 +1359,10 @@ __device__ void combine_partials(const Params& P, const Job& job, uint32_t tid, 
     }
     __syncthreads();
     if (!last_flag) return;
+    // The last arrival reads what the others published: an agent-scope
+    // acquire, so that no line its CU cached earlier is read (the partial
+    // keys are read with device-scope atomics anyway).
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     // tpr threads per request (a power of two within a wavefront), each
     // taking every tpr-th slot; then a shuffle reduction inside the group
     uint32_t tpr = 64;
