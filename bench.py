@@ -136,9 +136,9 @@ def source_digest(source=None):
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_traffic(workload_name):
-    """HBM bytes per launch from the committed rocprofv3 counter summary of
-    this kernel and workload, if it was taken on the current kernel source."""
+def _profile_record(workload_name):
+    """This workload's entry of the committed rocprofv3 counter summary
+    (profiles/pmc_traffic.json), if it was taken on the current kernel source."""
     path = os.path.join(ROOT, "profiles", "pmc_traffic.json")
     if not os.path.exists(path):
         return None
@@ -147,7 +147,33 @@ def measured_traffic(workload_name):
     rec = data.get(workload_name)
     if not rec or rec.get("source_digest") != source_digest():
         return None
-    return rec.get("bytes_per_launch")
+    return rec
+
+
+def measured_traffic(workload_name):
+    """HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, calibrated) from the
+    committed counter summary, if it was taken on the current kernel source."""
+    rec = _profile_record(workload_name)
+    return rec.get("bytes_per_launch") if rec else None
+
+
+# Issue peak of the vector ALU: 256 CUs x 4 SIMDs x 2.4 GHz, a wave64
+# instruction occupying a 16-lane SIMD for 4 cycles.
+PEAK_VALU_ISSUE = 256 * 4 * 2.4e9 / 4
+
+
+def valu_issue(workload_name, block_queries, t):
+    """The search kernel's VALU roofline: its wavefront instructions per
+    launch (SQ_INSTS_VALU from the committed counter summary, current kernel
+    source only) over this run's time per call, against the issue peak."""
+    rec = _profile_record(workload_name)
+    if not rec or not rec.get("valu_insts_per_launch"):
+        return None
+    n = rec["valu_insts_per_launch"]
+    return {"bound": "valu_issue", "achieved": n / t, "peak": PEAK_VALU_ISSUE,
+            "unit": "wavefront instructions/s", "frac": n / t / PEAK_VALU_ISSUE,
+            "insts_per_launch": n, "insts_per_block_query": n / block_queries,
+            "source": rec.get("profile")}
 
 
 def cpu_baseline(pools, target_s, op="window", h=None):
@@ -362,6 +388,7 @@ def bench_window_config(k, args, dev, cpu_budget, steps, warmup):
     else:
         roofline = dict(hbm, alu=alu)
     roofline["kernel"] = KERNEL
+    roofline["valu_issue"] = valu_issue(spec.name, block_queries, t)
     single = None
     if args.medians:
         n_each = max(20, steps)
