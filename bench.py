@@ -65,7 +65,7 @@ def parse():
     ap.add_argument("--policy", choices=["window", "greedy"], default="window",
                     help="replay eviction policy timed by --op replay: Coop's sliding window "
                          "or the DTR-style greedy baseline")
-    ap.add_argument("--op", choices=["window", "first_fit", "replay", "real"], default="window",
+    ap.add_argument("--op", choices=["window", "first_fit", "replay", "real", "long"], default="window",
                     help="window: the eviction-window search; first_fit: the free-chunk "
                          "lookup that precedes it; replay: Algorithm 1 over training traces "
                          "(--config picks the trace set)")
@@ -446,6 +446,8 @@ def main():
 
     if args.op == "replay":
         return bench_replay(args, dev)
+    if args.op == "long":
+        return bench_long(args, dev)
     import workloads
     if args.op in ("first_fit", "real"):
         k = HEADLINE_CONFIG if args.config is None else args.config
@@ -503,6 +505,74 @@ def main():
         "kernel_source": source_digest(),
     }
     print(json.dumps(rec), flush=True)
+
+
+LONG_METRIC = "long-window search on one 2^24-block pinned-free run: microseconds per request"
+
+
+def bench_long(args, dev):
+    """Windows far longer than a tile: one pool of 2^24 blocks laid out as
+    section 3.5 describes (parameters pinned at both ends, one pinned-free
+    run between them), four request sets (workloads.long_run), each timed as
+    `steps` calls after `warmup`, with parity against the oracle on every
+    request.  Prints one JSON line; `value` is the spread set's microseconds
+    per request."""
+    import torch
+
+    import oracle
+    import paper_2311_00591_amd as coop
+    import workloads
+
+    sets = {}
+    digest = None
+    for name in workloads.LONG_RUN_SETS:
+        pools = workloads.long_run(request_set=name)
+        batch_dev_bytes = 17 * pools.num_blocks + 16 * pools.num_segments + 8 * pools.num_requests
+        copies = args.copies or max(1, -(-2 * INFINITY_CACHE_BYTES // batch_dev_bytes) + 1)
+        base = coop.to_device(pools, dev)
+        out = torch.empty((pools.num_requests, 3), dtype=torch.int64, device=dev)
+        ws = torch.empty(max(coop.workspace_size(pools.num_blocks, pools.num_segments,
+                                                 pools.num_requests), 1), dtype=torch.uint8, device=dev)
+        calls = [coop.WindowSearch(*(base if c == 0 else tuple(x.clone() for x in base)),
+                                   out=out, workspace=ws) for c in range(copies)]
+        torch.cuda.synchronize()
+        stream = torch.cuda.current_stream(dev)
+        sh = stream.cuda_stream
+        parity = None
+        if not args.no_parity:
+            calls[0].launch(sh)
+            torch.cuda.synchronize()
+            got = out.cpu().numpy().view(np.uint64)
+            want = oracle.window_search(*pools.arrays(), threads=_threads())
+            parity = bool(np.array_equal(got, want))
+        for i in range(args.warmup):
+            calls[i % copies].launch(sh)
+        torch.cuda.synchronize()
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record(stream)
+        for i in range(args.steps):
+            calls[i % copies].launch(sh)
+        stop.record(stream)
+        torch.cuda.synchronize()
+        ms = start.elapsed_time(stop) / args.steps
+        sets[name] = {"requests": pools.num_requests, "ms_per_call": ms,
+                      "us_per_request": ms * 1e3 / pools.num_requests,
+                      "request_bytes": [int(x) for x in pools.req_sizes],
+                      "parity_vs_oracle": parity, "resident_copies": copies,
+                      "input_sha256": pools.digest()[:16]}
+        digest = digest or pools.digest()[:16]
+        del calls, base, out, ws
+        torch.cuda.empty_cache()
+    head = sets["spread"]
+    print(json.dumps({
+        "metric": LONG_METRIC, "value": head["us_per_request"], "unit": "us/request",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": head["ms_per_call"],
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "u64",
+        "data": "synthetic",
+        "config": {"workload": "one snapshot of 2^24 blocks, parameters pinned at both ends, "
+                               "16 requests from one block to the whole run (workloads.long_run)"},
+        "sets": sets, "parity_vs_oracle": all(v["parity_vs_oracle"] is not False for v in sets.values()),
+        "kernel_source": source_digest()}), flush=True)
 
 
 def bench_first_fit(args, pools, spec, dev, k):

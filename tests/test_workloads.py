@@ -85,3 +85,26 @@ def test_real_costs():
     c = p.cost[ev].astype(np.float64)
     assert (h[ev] <= c).all() and (h[ev] >= c / 4096 * (1 - 1e-15)).all()
     assert np.mean(h[ev] != np.floor(h[ev])) > 0.9
+
+
+def test_long_run_pool_layout():
+    """workloads.long_run: one snapshot, parameters pinned at both ends and
+    one pinned-free run between them; the spread set ends with the whole run
+    and the half set asks for half of it; the same seed gives the same pool."""
+    for name in workloads.LONG_RUN_SETS:
+        p = workloads.long_run(n=1 << 14, request_set=name)
+        assert p.num_segments == 1 and p.num_blocks == 1 << 14
+        k = p.kind
+        assert (k[:37] == workloads.PINNED).all() and (k[-53:] == workloads.PINNED).all()
+        assert (k[37:-53] < workloads.PINNED).all()
+        run = int(p.size[37:-53].sum())
+        req = [int(x) for x in p.req_sizes]
+        if name == "spread":
+            assert len(req) == 16 and req[-1] == run and req[0] == 512
+        if name == "half":
+            assert req == [run // 2]
+        if name == "whole":
+            assert req == [run]
+        assert (p.size % 512 == 0).all() and (p.size >= 512).all()
+    a, b = workloads.long_run(n=1 << 12), workloads.long_run(n=1 << 12)
+    assert a.digest() == b.digest()

@@ -290,3 +290,36 @@ def real_costs(pools: Pools, seed: int = 0, max_staleness: int = 4096) -> np.nda
     h = pools.cost.astype(np.float64) / s
     h[pools.kind != EVICTABLE] = 0.0
     return h
+
+
+# One pool laid out as section 3.5 describes: unevictable parameters at both
+# ends, everything between them one pinned-free run of activations.
+LONG_RUN_SETS = ("spread", "small", "half", "whole")
+
+
+def long_run(seed: int = 16, n: int = 1 << 24, request_set: str = "spread") -> Pools:
+    """One snapshot of n blocks: sizes log-uniform on [512 B, 64 MiB] (rounded
+    up to 512 B), a fifth of the blocks free, the first 37 and last 53 pinned
+    (the parameters), costs log-uniform on [1, 1e12).  Request sets, in bytes
+    of the run between the parameters: "spread" (16: one block, the mean
+    block, 100 and 5000 mean blocks, k/12 of the run for k = 1..11, the whole
+    run), "small" (16, geometric from 512 B to 5000 mean blocks), "half" (one
+    request, half the run), "whole" (one request, the whole run)."""
+    rng = np.random.default_rng(seed)
+    lo, hi = np.log(512.0), np.log(64.0 * (1 << 20))
+    size = ((np.exp(lo + rng.random(n) * (hi - lo)) + 511) // 512 * 512).astype(np.uint64)
+    kind = np.where(rng.random(n) < 0.2, FREE, EVICTABLE).astype(np.uint8)
+    kind[:37] = PINNED
+    kind[-53:] = PINNED
+    cost = np.floor(np.exp(rng.random(n) * np.log(1e12))).astype(np.uint64)
+    run = int(size[37:-53].sum())
+    mean = int(size.mean())
+    sets = {
+        "spread": [512, mean, 100 * mean, 5000 * mean] + [run * k // 12 for k in range(1, 12)] + [run],
+        "small": [int(x) for x in np.geomspace(512, 5000 * mean, 16)],
+        "half": [run // 2],
+        "whole": [run],
+    }
+    req = np.array(sets[request_set], dtype=np.uint64)
+    return Pools(size, cost, kind, np.array([0, n], dtype=np.uint64), req,
+                 np.array([0, len(req)], dtype=np.uint64))
