@@ -1859,9 +1859,11 @@ __device__ void stretch_merge(const Smem& sm, const EndSmem& es, const TileState
 
 // The windows of the pending starts of a staged tile that end more than
 // kWalkCap blocks past the region (whole workgroup; every thread gets the
-// workgroup's key).
+// workgroup's key).  run_left: the bytes from the region end to the end of
+// its last run, kNone until a search of this tile has reached that end; a
+// request that needs more is answered at once.
 __device__ Key far_windows(const Params& P, const Smem& sm, EndSmem& es, const Job& job,
-                           const TileGeom& tg, const TileState& ts, uint64_t S) {
+                           const TileGeom& tg, const TileState& ts, uint64_t S, uint64_t& run_left) {
     const uint32_t tid = threadIdx.x;
     const uint32_t lane = tid & 63u;
     const uint32_t w = uniform(tid >> 6);
@@ -1871,7 +1873,9 @@ __device__ Key far_windows(const Params& P, const Smem& sm, EndSmem& es, const J
     uint32_t cur = pending_start(sm, ts.packed, nA, ts.xend, ts.endrun, S, Sc, lane);
     Cand best = cand_none();
     uint64_t best_end = 0;
-    if (cur < nA) {
+    // a window from the first pending start needs more bytes past the region
+    // end than the run has left there: none from any later start either
+    if (cur < nA && (run_left == kNone || S - ((ts.xend - sm.x[cur]) & vmask) <= run_left)) {
         const Ext e = ext_of(P);
         const uint64_t a = job.s0 & ~7ull;                       // tile k starts at a + k * kTile
         const int64_t rb = static_cast<int64_t>(job.s0 >> kTileLog2) - 1;  // record of tile k: rb + k
@@ -1892,7 +1896,10 @@ __device__ Key far_windows(const Params& P, const Smem& sm, EndSmem& es, const J
             const uint64_t need = S - ((ts.xend - sm.x[cur]) & vmask);
             uint64_t fq, fc;
             const uint64_t k = find_tile(e, es, rb, nrec, job.tiles, kmin, carry, need, fq, fc);
-            if (k >= job.tiles) break;  // the run ends with the snapshot, below `need` bytes
+            if (k >= job.tiles) {  // the run ends with the snapshot, below `need` bytes
+                run_left = fq;
+                break;
+            }
             const uint64_t ks = a + (k << kTileLog2), ke = ks + kTile;
             const uint64_t bs = ks > ge ? ks : ge, be = ke < job.s1 ? ke : job.s1;
             // bytes and cost from the region end to the stretch start
@@ -1907,6 +1914,7 @@ __device__ Key far_windows(const Params& P, const Smem& sm, EndSmem& es, const J
                 return S - G - ((ts.xend - sm.x[i]) & vmask) > last;
             });
             __syncthreads();  // the stretch buffer is restaged next
+            if (closed) run_left = G + last;  // the run ends in this stretch
             if (closed || nxt >= nA) break;
             // the stretch reached the end of tile k with no pinned block
             carry = Sums3{G + last, GC + es_last_c, 0};
@@ -1964,12 +1972,30 @@ __device__ void resolve_entry(const Params& P, Smem& sm, EndSmem& es, uint4 en, 
     const uint32_t tid = threadIdx.x;
     Cursor c;
     Job job;
+    // Bytes from the region end to the end of its last run, once a request
+    // has found that end (the same for every request of the tile), and the
+    // previous tile's staged halo, which carry it to the entry's next tile.
+    uint64_t run_left = kNone;
+    uint32_t prev_halo = 0;
+    uint64_t prev_p = kNone;
     for (uint32_t u = en.x; u < en.y; ++u) {
         if (!entry_job(P, en, u, c, job)) continue;  // (not reached: the entry names the job's tiles)
         const TileGeom tg = tile_geom(job);
         TileRegs regs;
         issue_loads(P, tg, tid, regs);
         const TileState ts = stage_tile(sm, tg, tid, regs);
+        // The previous region ended at boundary prev_halo of this tile: with
+        // no pinned block between the two region ends, the run goes on and
+        // has the bytes between them fewer left.
+        if (run_left != kNone && prev_p + 1 == job.p && ts.packed && prev_halo <= tg.nt) {
+            const uint64_t d = ts.xend - sm.x[prev_halo];
+            const uint64_t between = d & kValMask;
+            run_left = (d >> kValBits) == 0 && run_left >= between ? run_left - between : kNone;
+        } else {
+            run_left = kNone;
+        }
+        prev_p = job.p;
+        prev_halo = ts.end - tg.nt;
         if (tg.t0 + ts.end < job.s1 && tg.nt != 0) {  // the region's last run may go on
             for (uint64_t r = 0; r < job.K; ++r) {
                 const uint64_t q = job.q0 + job.y + (r << P.slices_log2);
@@ -1979,7 +2005,7 @@ __device__ void resolve_entry(const Params& P, Smem& sm, EndSmem& es, uint4 en, 
                                                                 __HIP_MEMORY_SCOPE_AGENT));
                 const uint64_t S = ld_const(P.req_size, q);
                 if (!((word >> (bit & 31u)) & 1u) || S == 0) continue;
-                const Key k = far_windows(P, sm, es, job, tg, ts, S);
+                const Key k = far_windows(P, sm, es, job, tg, ts, S, run_left);
                 // the same thread folds the request's key on every tile
                 if (tid == 0 && k.start != kNone) {
                     Key* slot = P.part + q * P.pc + job.g;

@@ -222,6 +222,39 @@ def test_long_runs_mixed_batch():
     check_results(pools, got)
 
 
+def test_long_runs_cut_by_pinned_blocks():
+    """Runs of 2 to 12 tiles separated by single pinned blocks placed at tile
+    edges, inside the 256-block halo and mid-tile, with requests at each
+    run's exact byte total, one byte more, and between: a tile whose windows
+    cannot close in its run learns where the run ends, and what it learned
+    must not carry past a pinned block into the next run."""
+    _announce("long runs cut by pinned blocks")
+    rng = np.random.default_rng(21)
+    snaps, reqs = [], []
+    for s in range(12):
+        cuts, pos = [], 0
+        for _ in range(int(rng.integers(2, 5))):
+            pos += int(rng.integers(2, 13)) * TILE + [0, 1, 100, 255, 256, 2048][int(rng.integers(0, 6))]
+            cuts.append(pos)
+        n = pos + int(rng.integers(1, 3 * TILE))
+        size = (rng.integers(1, 64, size=n) * 512).astype(np.uint64)
+        kind = np.where(rng.random(n) < 0.2, 0, 1).astype(np.uint8)
+        kind[np.array(cuts)] = 2
+        cost = rng.integers(0, 10**6, size=n).astype(np.uint64)
+        snaps.append((size, cost, kind))
+        bounds = [0] + cuts + [n]
+        runs = [int(size[a + (a > 0):b].sum()) for a, b in zip(bounds[:-1], bounds[1:])]
+        r = []
+        for t in runs:
+            r += [t, t + 1, t // 2, t - 512]
+        r += [max(runs) + 1, int(rng.integers(1, max(runs)))]
+        reqs.append(r)
+    pools = _pools(snaps, reqs)
+    got = gpu_search(pools)
+    assert_parity(pools, got, "long runs cut by pinned blocks")
+    check_results(pools, got)
+
+
 def test_long_runs_with_more_than_64_requests_per_wavefront():
     """A three-tile run with 20,000 requests among 40 one-request snapshots:
     each wavefront holds more than 64 of the big snapshot's requests, whose
