@@ -1871,11 +1871,14 @@ __device__ Key far_windows(const Params& P, const Smem& sm, EndSmem& es, const J
     const uint64_t vmask = ts.packed ? kValMask : kNone;
     const uint64_t Sc = S < (1ull << kValBits) ? S : (1ull << kValBits);
     uint32_t cur = pending_start(sm, ts.packed, nA, ts.xend, ts.endrun, S, Sc, lane);
+    // No pending start, or a window from the first one needs more bytes past
+    // the region end than the run has left there (none from a later start
+    // either): no window (the same in every thread).
+    if (cur >= nA || (run_left != kNone && S - ((ts.xend - sm.x[cur]) & vmask) > run_left))
+        return key_none();
     Cand best = cand_none();
     uint64_t best_end = 0;
-    // a window from the first pending start needs more bytes past the region
-    // end than the run has left there: none from any later start either
-    if (cur < nA && (run_left == kNone || S - ((ts.xend - sm.x[cur]) & vmask) <= run_left)) {
+    {
         const Ext e = ext_of(P);
         const uint64_t a = job.s0 & ~7ull;                       // tile k starts at a + k * kTile
         const int64_t rb = static_cast<int64_t>(job.s0 >> kTileLog2) - 1;  // record of tile k: rb + k
