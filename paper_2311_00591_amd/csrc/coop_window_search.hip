@@ -1857,13 +1857,21 @@ __device__ void stretch_merge(const Smem& sm, const EndSmem& es, const TileState
     }
 }
 
+// The blocks [bs, be) whose prefixes the stretch buffer holds (bs = kNone:
+// none), and m, the boundaries before the first pinned one.
+struct Staged {
+    uint64_t bs, be;
+    uint32_t m;
+};
+
 // The windows of the pending starts of a staged tile that end more than
 // kWalkCap blocks past the region (whole workgroup; every thread gets the
 // workgroup's key).  run_left: the bytes from the region end to the end of
 // its last run, kNone until a search of this tile has reached that end; a
 // request that needs more is answered at once.
 __device__ Key far_windows(const Params& P, const Smem& sm, EndSmem& es, const Job& job,
-                           const TileGeom& tg, const TileState& ts, uint64_t S, uint64_t& run_left) {
+                           const TileGeom& tg, const TileState& ts, uint64_t S, uint64_t& run_left,
+                           Staged& staged) {
     const uint32_t tid = threadIdx.x;
     const uint32_t lane = tid & 63u;
     const uint32_t w = uniform(tid >> 6);
@@ -1908,7 +1916,14 @@ __device__ Key far_windows(const Params& P, const Smem& sm, EndSmem& es, const J
             // bytes and cost from the region end to the stretch start
             const uint64_t G = k == job.p + 1 ? 0 : fq;
             const uint64_t GC = k == job.p + 1 ? 0 : fc;
-            const uint32_t m = stage_stretch(P, es, bs, be, tid);
+            // (the buffer's content depends on [bs, be) alone: a tile's last
+            // stretch is often the next tile's first)
+            if (staged.bs != bs || staged.be != be) {
+                staged.m = stage_stretch(P, es, bs, be, tid);
+                staged.bs = bs;
+                staged.be = be;
+            }
+            const uint32_t m = staged.m;
             const bool closed = m < be - bs || be == job.s1;
             stretch_merge(sm, es, ts, vmask, cur, nA, m, S, G, GC, bs - job.s0, tid, best, best_end);
             // the first start whose window ends past this stretch
@@ -1971,7 +1986,8 @@ __device__ bool entry_job(const Params& P, uint4 en, uint32_t u, Cursor& c, Job&
 // search kernel wrote.  Then, as the search kernel would have: the results,
 // or the arrival ticket and the combine when the snapshot spans several
 // chunks; the deferral bits are cleared.
-__device__ void resolve_entry(const Params& P, Smem& sm, EndSmem& es, uint4 en, uint32_t& last_flag) {
+__device__ void resolve_entry(const Params& P, Smem& sm, EndSmem& es, uint4 en, uint32_t& last_flag,
+                              Staged& staged) {
     const uint32_t tid = threadIdx.x;
     Cursor c;
     Job job;
@@ -2008,7 +2024,7 @@ __device__ void resolve_entry(const Params& P, Smem& sm, EndSmem& es, uint4 en, 
                                                                 __HIP_MEMORY_SCOPE_AGENT));
                 const uint64_t S = ld_const(P.req_size, q);
                 if (!((word >> (bit & 31u)) & 1u) || S == 0) continue;
-                const Key k = far_windows(P, sm, es, job, tg, ts, S, run_left);
+                const Key k = far_windows(P, sm, es, job, tg, ts, S, run_left, staged);
                 // the same thread folds the request's key on every tile
                 if (tid == 0 && k.start != kNone) {
                     Key* slot = P.part + q * P.pc + job.g;
@@ -2053,12 +2069,13 @@ __global__ __launch_bounds__(kThreads, 2) void coop_window_long_kernel(Params Pi
     uint32_t n = (uniform(static_cast<uint32_t>(word >> 32)) == P.qtag) ? uniform(static_cast<uint32_t>(word)) : 0u;
     if (n > P.defer_cap) n = P.defer_cap;
     if (n == 0) return;
+    Staged staged{kNone, 0, 0};
     for (uint32_t e = blockIdx.x; e < n; e += gridDim.x) {
         const uint4 en = load_entry_device(ex.entries + e);
         // (entries are written by this call's search kernel; the checks keep
         // every access in bounds whatever the workspace holds)
         if (en.x >= en.y || en.y > P.units || en.w == 0 || en.w > P.pc || en.z >= en.w) continue;
-        resolve_entry(P, sm, es, en, last_flag);
+        resolve_entry(P, sm, es, en, last_flag, staged);
     }
 }
 
