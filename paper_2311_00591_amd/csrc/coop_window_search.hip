@@ -1676,6 +1676,7 @@ __device__ __forceinline__ void wave_inclusive_sum3(Sums3& s) {
 // Boundaries of a staged stretch past the region (a tile at most) and the
 // end keys a merge may read past its last one.
 constexpr uint32_t kEndPad = 64;
+constexpr uint32_t kFarCache = 64;
 constexpr uint32_t kEndN = kTile + 2 + kEndPad;
 
 // The long kernel's second LDS buffer: the stretch's byte and cost
@@ -1689,6 +1690,10 @@ struct EndSmem {
     Key slot[kWaves];
     uint64_t found;     // the tile the search stopped at
     uint64_t fq, fc;    // bytes and cost from the region end to that tile's start
+    // Where the first record search of request far_q's last tile stopped:
+    // the region end far_ge (global), the tile far_k and the bytes and cost
+    // from far_ge to its start (slot q % kFarCache).
+    uint64_t far_q[kFarCache], far_ge[kFarCache], far_k[kFarCache], far_b[kFarCache], far_c[kFarCache];
 };
 
 // Where the run of a staged region's last run goes on past the region end:
@@ -1864,14 +1869,22 @@ struct Staged {
     uint32_t m;
 };
 
+// From the previous tile of the entry to this one: the previous region end
+// (global; kNone when there is no previous tile), and, when no pinned block
+// lies between the two region ends (same_run), the bytes and cost between.
+struct Between {
+    uint64_t prev_ge, q, c;
+    bool same_run;
+};
+
 // The windows of the pending starts of a staged tile that end more than
 // kWalkCap blocks past the region (whole workgroup; every thread gets the
 // workgroup's key).  run_left: the bytes from the region end to the end of
 // its last run, kNone until a search of this tile has reached that end; a
 // request that needs more is answered at once.
 __device__ Key far_windows(const Params& P, const Smem& sm, EndSmem& es, const Job& job,
-                           const TileGeom& tg, const TileState& ts, uint64_t S, uint64_t& run_left,
-                           Staged& staged) {
+                           const TileGeom& tg, const TileState& ts, uint64_t q, uint64_t S,
+                           uint64_t& run_left, Staged& staged, const Between& bt) {
     const uint32_t tid = threadIdx.x;
     const uint32_t lane = tid & 63u;
     const uint32_t w = uniform(tid >> 6);
@@ -1903,10 +1916,30 @@ __device__ Key far_windows(const Params& P, const Smem& sm, EndSmem& es, const J
         const uint64_t ge = tg.t0 + ts.end;  // global index of the region end
         uint64_t kmin = job.p + 1;
         Sums3 carry{0 - hq, 0 - hc, 0 - hr};  // region end to the start of tile kmin
+        // The previous tile's first pending start lies earlier in the same
+        // run, so this tile's first window ends no earlier: its search may
+        // start where that one stopped (past this region), with the sums
+        // from there less the bytes and cost between the two region ends
+        // (no pinned block there, nor before that tile).
+        const uint32_t slot = static_cast<uint32_t>(q % kFarCache);
+        if (bt.same_run && es.far_q[slot] == q && es.far_ge[slot] == bt.prev_ge &&
+            es.far_k[slot] >= job.p + 2) {
+            kmin = es.far_k[slot];
+            carry = Sums3{es.far_b[slot] - bt.q, es.far_c[slot] - bt.c, 0};
+        }
+        bool first_search = true;
         for (;;) {
             const uint64_t need = S - ((ts.xend - sm.x[cur]) & vmask);
             uint64_t fq, fc;
             const uint64_t k = find_tile(e, es, rb, nrec, job.tiles, kmin, carry, need, fq, fc);
+            if (first_search && tid == 0) {  // read by the next tile's search (after barriers)
+                es.far_q[slot] = k < job.tiles ? q : kNone;
+                es.far_ge[slot] = ge;
+                es.far_k[slot] = k;
+                es.far_b[slot] = fq;
+                es.far_c[slot] = fc;
+            }
+            first_search = false;
             if (k >= job.tiles) {  // the run ends with the snapshot, below `need` bytes
                 run_left = fq;
                 break;
@@ -2006,13 +2039,12 @@ __device__ void resolve_entry(const Params& P, Smem& sm, EndSmem& es, uint4 en, 
         // The previous region ended at boundary prev_halo of this tile: with
         // no pinned block between the two region ends, the run goes on and
         // has the bytes between them fewer left.
-        if (run_left != kNone && prev_p + 1 == job.p && ts.packed && prev_halo <= tg.nt) {
+        Between bt{kNone, 0, 0, false};
+        if (prev_p != kNone && prev_p + 1 == job.p && ts.packed && prev_halo <= tg.nt) {
             const uint64_t d = ts.xend - sm.x[prev_halo];
-            const uint64_t between = d & kValMask;
-            run_left = (d >> kValBits) == 0 && run_left >= between ? run_left - between : kNone;
-        } else {
-            run_left = kNone;
+            bt = Between{tg.t0 + prev_halo, d & kValMask, ts.xcend - sm.xc[prev_halo], (d >> kValBits) == 0};
         }
+        run_left = bt.same_run && run_left != kNone && run_left >= bt.q ? run_left - bt.q : kNone;
         prev_p = job.p;
         prev_halo = ts.end - tg.nt;
         if (tg.t0 + ts.end < job.s1 && tg.nt != 0) {  // the region's last run may go on
@@ -2024,7 +2056,7 @@ __device__ void resolve_entry(const Params& P, Smem& sm, EndSmem& es, uint4 en, 
                                                                 __HIP_MEMORY_SCOPE_AGENT));
                 const uint64_t S = ld_const(P.req_size, q);
                 if (!((word >> (bit & 31u)) & 1u) || S == 0) continue;
-                const Key k = far_windows(P, sm, es, job, tg, ts, S, run_left, staged);
+                const Key k = far_windows(P, sm, es, job, tg, ts, q, S, run_left, staged, bt);
                 // the same thread folds the request's key on every tile
                 if (tid == 0 && k.start != kNone) {
                     Key* slot = P.part + q * P.pc + job.g;
@@ -2070,6 +2102,8 @@ __global__ __launch_bounds__(kThreads, 2) void coop_window_long_kernel(Params Pi
     if (n > P.defer_cap) n = P.defer_cap;
     if (n == 0) return;
     Staged staged{kNone, 0, 0};
+    if (threadIdx.x < kFarCache) es.far_q[threadIdx.x] = kNone;
+    __syncthreads();
     for (uint32_t e = blockIdx.x; e < n; e += gridDim.x) {
         const uint4 en = load_entry_device(ex.entries + e);
         // (entries are written by this call's search kernel; the checks keep
