@@ -47,8 +47,10 @@
 //     after the barrier that ends the tile.
 //  3. Starts whose windows end past the staged region (the region's last run
 //     goes on) are a suffix of the tile, found by one search; the request's
-//     wavefront finishes them by walking the rest of the run 64 blocks at a
-//     time.
+//     wavefront walks on through the run 64 blocks at a time, at most
+//     kWalkCap blocks past the region.  Starts still pending there are left
+//     to a second kernel, coop_window_long_kernel, which finds where their
+//     windows end from per-tile records (see the section before it).
 // A tile that holds a block of 2^37 bytes or more keeps plain 64-bit
 // prefixes (P could outgrow the 50-bit field) with the run ids in a separate
 // array, stages no halo, and bisects per start.
@@ -58,7 +60,8 @@
 // A snapshot held by one chunk writes its results directly.  Otherwise every
 // chunk writes one partial key per request into the workspace and takes a
 // ticket on a per-snapshot counter; the chunk holding the last ticket reduces
-// the partials and writes the results.  Counters and the queue carry a
+// the partials and writes the results.  A job with windows left to the
+// second kernel keeps its keys in the partial slots and is finished there.  Counters and the queue carry a
 // per-call tag, so the workspace never needs clearing: eager calls take it
 // from a host counter; calls captured into a graph derive it from a tag word
 // in the workspace, advanced by a one-thread kernel ahead of each replay.
