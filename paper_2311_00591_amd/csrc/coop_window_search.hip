@@ -116,6 +116,11 @@ constexpr uint64_t kNone = ~0ull;
 constexpr uint32_t kNone32 = ~0u;
 constexpr uint32_t kMaxWpr = 8;                  // wavefronts that may share one request
 constexpr uint32_t kWalkCap = 1024;              // blocks a wavefront walks past a staged region
+// A walk is not started when its first pending start needs more bytes past
+// the region than twice the whole region holds (a full region: kStage
+// blocks, so about 8.5 x kWalkCap blocks of its average size): those windows
+// go to the second kernel at once.  Only the speed depends on this guess.
+static_assert(2 * (kTile + kHaloCap) >= 8 * kWalkCap, "a skipped walk is one that would almost surely fail");
 // The fewest blocks of a snapshot whose windows can run past a walk: the
 // walk stops before the snapshot end only if more than kTile + kHaloCap +
 // kWalkCap blocks follow the tile start, which is at most 7 blocks before
@@ -182,6 +187,10 @@ __device__ __forceinline__ uint64_t shfl64(uint64_t v, uint32_t src) {
 
 __device__ __forceinline__ uint32_t uniform(uint32_t v) {
     return static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(v)));
+}
+
+__device__ __forceinline__ uint64_t uniform64(uint64_t v) {
+    return (static_cast<uint64_t>(uniform(static_cast<uint32_t>(v >> 32))) << 32) | uniform(static_cast<uint32_t>(v));
 }
 
 // Prefix-sum element: bytes (or packed key), effective cost, pinned count (or
@@ -335,8 +344,9 @@ struct Params {
 
 // The workspace after the queue word, laid out the same way by the host
 // (make_plan): the tag word, the deferred list's word (queue tag << 32 |
-// entries), the deferred entries {first unit, end unit, g, G} (16-byte
-// aligned), the tile records of tile p >= 1 of every snapshot at index
+// entries), the word coop_window_long_kernel claims entries by (queue tag
+// << 32 | claims), the deferred entries {first unit, end unit, g, G}
+// (16-byte aligned), the tile records of tile p >= 1 of every snapshot at index
 // (seg[b] >> kTileLog2) + p - 1 (bytes of all its blocks, cost of its
 // evictable blocks, its pinned count; written by the search kernel, read by
 // coop_window_long_kernel), and one deferral bit per partial slot (bit q * pc + g: request
@@ -344,6 +354,7 @@ struct Params {
 // where needed rather than passed, to keep the kernels' uniform state small.
 struct Ext {
     uint64_t* defer_word;
+    uint64_t* claim_word;
     uint4* entries;
     uint64_t* rec_p;
     uint64_t* rec_c;
@@ -354,7 +365,8 @@ struct Ext {
 __device__ __forceinline__ Ext ext_of(const Params& P) {
     Ext e;
     e.defer_word = P.queue + 2;
-    e.entries = reinterpret_cast<uint4*>((reinterpret_cast<uintptr_t>(P.queue + 3) + 15) & ~uintptr_t{15});
+    e.claim_word = P.queue + 3;
+    e.entries = reinterpret_cast<uint4*>((reinterpret_cast<uintptr_t>(P.queue + 4) + 15) & ~uintptr_t{15});
     e.rec_p = reinterpret_cast<uint64_t*>(e.entries + P.defer_cap);
     const uint64_t nrec = P.num_blocks >> kTileLog2;
     e.rec_c = e.rec_p + nrec;
@@ -405,7 +417,7 @@ struct Smem {
     Sums hsum[4];       // per-wavefront totals of the halo
     Key slot[kWaves];   // answers of wavefronts that share a request
     uint64_t slot_s[kWaves];
-    uint64_t claim;     // a chunk claimed from the queue, for every wavefront
+    uint64_t claim;     // a chunk claimed from the queue (an entry, in the second kernel)
     uint32_t defer_mark;  // the mark (hi - 1) of the last job a wavefront deferred
 };
 
@@ -1267,6 +1279,13 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
     // on), walked up to the end of the next tile; windows that go further
     // are left to coop_window_long_kernel, which is told by the job's mark
     uint64_t todo = __ballot(lane < held && pend < nt);
+    // bytes past the region beyond which a walk is not started (only where
+    // the snapshot goes on past the walk's limit, as for a walk that fails)
+    uint64_t hopeless = kNone;
+    if (todo && tg.t0 + end + kWalkCap < job.s1) {
+        const uint64_t rb = (ts.xend - sm.x[0]) & vmask;
+        hopeless = rb >> 63 ? kNone : rb << 1;
+    }
     while (todo) {
         const uint32_t n = static_cast<uint32_t>(__builtin_ctzll(todo));
         todo &= todo - 1;
@@ -1274,8 +1293,13 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
         const uint64_t S = readlane64(s_lane, wpr == 1 ? n : static_cast<uint32_t>(vw >> wl2));
         Cand best = cand_none();
         uint64_t best_end = 0;
-        WalkState ws{tg.t0 + end, ts.xend & vmask, ts.xcend, readlane32(pend, n), false};
-        walk_pass(P, sm, lane, nt, lim, job.s0, job.s1, vmask, S, ws, best, best_end);
+        const uint32_t c0 = readlane32(pend, n);
+        WalkState ws{tg.t0 + end, ts.xend & vmask, ts.xcend, c0, false};
+        // (a pending start has fewer than S bytes to the region end; a
+        // walk with its limit at its start loads nothing and leaves the
+        // starts pending)
+        const bool walk = S - ((ts.xend - sm.x[c0]) & vmask) <= hopeless;
+        walk_pass(P, sm, lane, nt, walk ? lim : ws.pos, job.s0, job.s1, vmask, S, ws, best, best_end);
         if (ws.cur < nt && !ws.closed && lane == 0) defer_request(P, sm, job, request(vw));
         const Key k = wave_answer(best, best_end, tl, S);
         if (wpr == 1) {
@@ -1769,16 +1793,27 @@ __device__ uint32_t stage_stretch(const Params& P, EndSmem& es, uint64_t bs, uin
     uint64_t sq[kItems], sc[kItems];
     Sums3 t{0, 0, 0};
     uint32_t fp = kNone32;
+    // every load is issued before any is used: the costs are loaded whatever
+    // the kinds, then masked, so the stretch takes one round trip, not two
+    uint32_t kd[kItems];
 #pragma unroll
     for (uint32_t j = 0; j < kItems; ++j) {
         const uint32_t i = i0 + j;
-        uint64_t s = 0, c = 0;
+        kd[j] = COOP_FREE;
+        sq[j] = 0;
+        sc[j] = 0;
         if (i < n) {
-            const uint32_t k = P.kind[bs + i];
-            s = P.size[bs + i];
-            c = k == COOP_EVICTABLE ? P.cost[bs + i] : 0;
-            if (k >= COOP_PINNED && fp == kNone32) fp = i;
+            kd[j] = P.kind[bs + i];
+            sq[j] = P.size[bs + i];
+            sc[j] = P.cost[bs + i];
         }
+    }
+#pragma unroll
+    for (uint32_t j = 0; j < kItems; ++j) {
+        const uint32_t i = i0 + j;
+        const uint32_t k = kd[j];
+        const uint64_t s = sq[j], c = k == COOP_EVICTABLE ? sc[j] : 0;
+        if (k >= COOP_PINNED && fp == kNone32) fp = i;
         t.q += s;
         t.c += c;
         sq[j] = t.q;
@@ -2033,8 +2068,41 @@ __device__ void resolve_entry(const Params& P, Smem& sm, EndSmem& es, uint4 en, 
     uint64_t run_left = kNone;
     uint32_t prev_halo = 0;
     uint64_t prev_p = kNone;
+    // The bytes from the start of tile prev_p + 1 to the end of the run the
+    // previous region ended in, when that run reaches the tile (kNone if
+    // unknown).  A tile without pinned blocks lies wholly in that run: when
+    // every request that deferred there needs more bytes than this, none of
+    // its starts has a window, and the tile is passed over unstaged (the
+    // count then carries on by the tile's record).
+    uint64_t from_start = kNone;
     for (uint32_t u = en.x; u < en.y; ++u) {
         if (!entry_job(P, en, u, c, job)) continue;  // (not reached: the entry names the job's tiles)
+        if (from_start != kNone && prev_p != kNone && prev_p + 1 == job.p) {
+            const Ext e = ext_of(P);
+            const uint64_t idx = (job.s0 >> kTileLog2) + job.p - 1;  // the record of tile p >= 1
+            bool skip = false;
+            uint64_t tb = 0;
+            if (idx < (P.num_blocks >> kTileLog2) &&
+                uniform64(__hip_atomic_load(e.rec_r + idx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) == 0) {
+                tb = uniform64(__hip_atomic_load(e.rec_p + idx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+                skip = true;
+                for (uint64_t r = 0; r < job.K && skip; ++r) {
+                    const uint64_t q = job.q0 + job.y + (r << P.slices_log2);
+                    const uint64_t bit = q * P.pc + job.g;
+                    const uint32_t word = uniform(__hip_atomic_load(e.bits + (bit >> 5), __ATOMIC_RELAXED,
+                                                                    __HIP_MEMORY_SCOPE_AGENT));
+                    const uint64_t S = ld_const(P.req_size, q);
+                    if (((word >> (bit & 31u)) & 1u) && S != 0 && S <= from_start) skip = false;
+                }
+            }
+            if (skip) {
+                from_start = from_start >= tb ? from_start - tb : kNone;
+                prev_p = job.p;
+                prev_halo = kNone32;  // nothing staged to carry run_left by
+                run_left = kNone;
+                continue;
+            }
+        }
         const TileGeom tg = tile_geom(job);
         TileRegs regs;
         issue_loads(P, tg, tid, regs);
@@ -2048,6 +2116,12 @@ __device__ void resolve_entry(const Params& P, Smem& sm, EndSmem& es, uint4 en, 
             bt = Between{tg.t0 + prev_halo, d & kValMask, ts.xcend - sm.xc[prev_halo], (d >> kValBits) == 0};
         }
         run_left = bt.same_run && run_left != kNone && run_left >= bt.q ? run_left - bt.q : kNone;
+        if (run_left == kNone && from_start != kNone && prev_p != kNone && prev_p + 1 == job.p && ts.packed) {
+            // after tiles passed over: from the tile start when the region
+            // holds no pinned block
+            const uint64_t d = ts.xend - sm.x[0];
+            if ((d >> kValBits) == 0 && from_start >= d) run_left = from_start - d;
+        }
         prev_p = job.p;
         prev_halo = ts.end - tg.nt;
         if (tg.t0 + ts.end < job.s1 && tg.nt != 0) {  // the region's last run may go on
@@ -2066,6 +2140,13 @@ __device__ void resolve_entry(const Params& P, Smem& sm, EndSmem& es, uint4 en, 
                     store_key_device(slot, min_key(load_key_device(slot), k));
                 }
             }
+        }
+        // the next tile starts at boundary nt: in the region's last run when
+        // the halo holds no pinned block
+        from_start = kNone;
+        if (run_left != kNone && ts.packed) {
+            const uint64_t d = ts.end > tg.nt ? ts.xend - sm.x[tg.nt] : 0;
+            if ((d >> kValBits) == 0) from_start = run_left + d;
         }
         __syncthreads();  // LDS is restaged next
     }
@@ -2088,7 +2169,7 @@ __device__ void resolve_entry(const Params& P, Smem& sm, EndSmem& es, uint4 en, 
 // Finishes the jobs the search kernel deferred, after it on the stream.
 // With nothing deferred (the list's word carries an older tag) every
 // workgroup returns at once.  One workgroup per CU (the second LDS buffer);
-// no workgroup waits for another.
+// no workgroup waits for another: each claims entries until none is left.
 __global__ __launch_bounds__(kThreads, 2) void coop_window_long_kernel(Params Pin) {
     __shared__ Smem sm;
     __shared__ EndSmem es;
@@ -2107,7 +2188,15 @@ __global__ __launch_bounds__(kThreads, 2) void coop_window_long_kernel(Params Pi
     Staged staged{kNone, 0, 0};
     if (threadIdx.x < kFarCache) es.far_q[threadIdx.x] = kNone;
     __syncthreads();
-    for (uint32_t e = blockIdx.x; e < n; e += gridDim.x) {
+    // Entries are claimed one at a time (a ticket on the claim word, which
+    // the call's first claim restamps with its tag): their costs differ
+    // widely, and a fixed share per workgroup left some with twice the mean.
+    for (;;) {
+        if (threadIdx.x == 0) sm.claim = take_ticket(ex.claim_word, P.qtag, 32) - 1;
+        __syncthreads();
+        const uint32_t e = uniform(static_cast<uint32_t>(sm.claim));  // claims: below n + grid
+        __syncthreads();  // sm.claim is written again by the next claim
+        if (e >= n) break;
         const uint4 en = load_entry_device(ex.entries + e);
         // (entries are written by this call's search kernel; the checks keep
         // every access in bounds whatever the workspace holds)
@@ -2132,7 +2221,7 @@ struct Plan {
     uint64_t pc;           // partial slots per request
     size_t part_bytes;     // partial keys
     uint64_t defer_cap;    // deferred entries, at most
-    size_t off_defer;      // the deferred list's word, then its entries
+    size_t off_defer;      // the deferred list's word, the claim word, then the entries
     size_t off_entries;
     size_t off_rec;        // tile records: bytes, costs, pinned counts (u64 each)
     uint64_t num_rec;
@@ -2224,7 +2313,7 @@ bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests
     // then the arrival counters, the queue word, the tag word and the
     // deferred list's word
     pl->off_defer = pl->part_bytes + (slices * num_segments + 2) * sizeof(uint64_t);
-    pl->off_entries = (pl->off_defer + sizeof(uint64_t) + 15) & ~static_cast<size_t>(15);
+    pl->off_entries = (pl->off_defer + 2 * sizeof(uint64_t) + 15) & ~static_cast<size_t>(15);
     // (the kernels derive these offsets from the queue word's address: see
     // Ext; the workspace is 256-byte aligned, so aligning offsets aligns
     // addresses)
