@@ -167,7 +167,7 @@ coop_status_t coop_window_search(const uint64_t *size, const uint64_t *cost,
  * arguments, results and status codes as coop_window_search, without the
  * workspace: the cross-workgroup state (partial keys, arrival counters, the
  * chunk queue, the graph tag word, the list of jobs left to the second
- * kernel, per-tile records and deferral bits) lives in a static device array of the
+ * kernel and its claim word, per-tile records and deferral bits) lives in a static device array of the
  * library, 32 MiB on every GPU the library runs on, held until the process
  * ends.  Its address is looked up on the first call on a device (with the
  * stream's device current) and kept; the call then allocates nothing and

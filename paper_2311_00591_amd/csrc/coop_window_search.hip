@@ -817,6 +817,15 @@ __device__ void walk_pass(const Params& P, const Smem& sm, uint32_t lane, uint32
                           Cand& best, uint64_t& best_end) {
     uint32_t cur = ws.cur;
     uint64_t pos = ws.pos, cq = ws.cq, cc = ws.cc;
+    // A walk that would almost surely fail is not started: where the
+    // snapshot goes on past the limit (as for a walk that fails), when the
+    // first pending start needs more bytes past the region than twice the
+    // region holds (cq is the region's byte prefix at its end, sm.x[0] at
+    // its start; a pending start has fewer than S bytes to the region end).
+    if (lim == pos + kWalkCap && lim < s1) {
+        const uint64_t rb = cq - (sm.x[0] & vmask);
+        if (S - (cq - (sm.x[cur] & vmask)) > (rb >> 63 ? kNone : rb << 1)) lim = pos;
+    }
     // the blocks of the chunk at pos; the next chunk's are loaded before
     // this one is processed
     auto load = [&](uint64_t at, uint32_t m, uint32_t& kd, uint64_t& sz, uint64_t& ct) {
@@ -1279,13 +1288,6 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
     // on), walked up to the end of the next tile; windows that go further
     // are left to coop_window_long_kernel, which is told by the job's mark
     uint64_t todo = __ballot(lane < held && pend < nt);
-    // bytes past the region beyond which a walk is not started (only where
-    // the snapshot goes on past the walk's limit, as for a walk that fails)
-    uint64_t hopeless = kNone;
-    if (todo && tg.t0 + end + kWalkCap < job.s1) {
-        const uint64_t rb = (ts.xend - sm.x[0]) & vmask;
-        hopeless = rb >> 63 ? kNone : rb << 1;
-    }
     while (todo) {
         const uint32_t n = static_cast<uint32_t>(__builtin_ctzll(todo));
         todo &= todo - 1;
@@ -1293,13 +1295,8 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
         const uint64_t S = readlane64(s_lane, wpr == 1 ? n : static_cast<uint32_t>(vw >> wl2));
         Cand best = cand_none();
         uint64_t best_end = 0;
-        const uint32_t c0 = readlane32(pend, n);
-        WalkState ws{tg.t0 + end, ts.xend & vmask, ts.xcend, c0, false};
-        // (a pending start has fewer than S bytes to the region end; a
-        // walk with its limit at its start loads nothing and leaves the
-        // starts pending)
-        const bool walk = S - ((ts.xend - sm.x[c0]) & vmask) <= hopeless;
-        walk_pass(P, sm, lane, nt, walk ? lim : ws.pos, job.s0, job.s1, vmask, S, ws, best, best_end);
+        WalkState ws{tg.t0 + end, ts.xend & vmask, ts.xcend, readlane32(pend, n), false};
+        walk_pass(P, sm, lane, nt, lim, job.s0, job.s1, vmask, S, ws, best, best_end);
         if (ws.cur < nt && !ws.closed && lane == 0) defer_request(P, sm, job, request(vw));
         const Key k = wave_answer(best, best_end, tl, S);
         if (wpr == 1) {
