@@ -255,6 +255,50 @@ def test_long_runs_cut_by_pinned_blocks():
     check_results(pools, got)
 
 
+def test_long_runs_measured_from_tile_starts():
+    """Requests of exactly the bytes from a tile's first block to the end of
+    its run, one byte fewer and one more, on runs of 10 to 30 tiles whose
+    ends (pinned blocks) sit mid-tile, at a tile's first block and inside a
+    halo: the second kernel passes over a tile only when every request that
+    deferred there needs more than that count, and a pinned block inside a
+    tile must stop the count.  Half- and whole-run requests make the search
+    kernel leave its walks past the staged region unstarted."""
+    _announce("long runs measured from tile starts")
+    rng = np.random.default_rng(23)
+    snaps, reqs = [], []
+    base = 0  # global index of the snapshot's first block
+    for s in range(6):
+        n = int(rng.integers(10, 31)) * TILE + int(rng.integers(0, TILE))
+        size = (rng.integers(1, 64, size=n) * 512).astype(np.uint64)
+        kind = np.where(rng.random(n) < 0.2, 0, 1).astype(np.uint8)
+        # the snapshot's tiles start at local indices p * TILE - (base & 7)
+        cuts = sorted({int(rng.integers(TILE, n - TILE)) for _ in range(int(rng.integers(1, 3)))})
+        if s % 3 == 0:  # at a tile's first block
+            cuts = [c - (c + (base & 7)) % TILE for c in cuts]
+        elif s % 3 == 1:  # inside a halo (the first 256 blocks of a tile)
+            cuts = [c - (c + (base & 7)) % TILE + 100 for c in cuts]
+        kind[np.array(cuts)] = 2
+        cost = rng.integers(0, 10**6, size=n).astype(np.uint64)
+        ends = cuts + [n]
+        r = []
+        for _ in range(8):
+            # a tile start (batch tiles begin at multiples of 8 before the
+            # snapshot, then every TILE blocks), the end of its run
+            a = TILE * int(rng.integers(1, n // TILE)) - (base & 7)
+            e = min(x for x in ends if x > a)
+            t = int(size[a:e].sum())
+            r += [t - 1, t, t + 1]
+        run0 = int(size[:cuts[0]].sum())
+        r += [run0 // 2, run0, int(size.sum())]
+        snaps.append((size, cost, kind))
+        reqs.append(r)
+        base += n
+    pools = _pools(snaps, reqs)
+    got = gpu_search(pools)
+    assert_parity(pools, got, "long runs measured from tile starts")
+    check_results(pools, got)
+
+
 def test_long_runs_with_more_than_64_requests_per_wavefront():
     """A three-tile run with 20,000 requests among 40 one-request snapshots:
     each wavefront holds more than 64 of the big snapshot's requests, whose
