@@ -73,11 +73,32 @@ def _capture(fn):
     return g
 
 
-@pytest.mark.parametrize("case", ["tickets", "queue"])
+def _long_run_batch():
+    """Two snapshots, each one pinned-free run of 24 tiles between pinned
+    ends, with requests up to the whole run: windows far past the staged
+    regions, left to the second kernel, whose workgroups claim deferred
+    entries through a tagged word that each replay must restart."""
+    rng = np.random.default_rng(31)
+    snaps, reqs = [], []
+    for _ in range(2):
+        n = 24 * 4096 + int(rng.integers(0, 4096))
+        size = (rng.integers(1, 64, size=n) * 512).astype(np.uint64)
+        kind = np.where(rng.random(n) < 0.2, 0, 1).astype(np.uint8)
+        kind[0] = kind[-1] = 2
+        cost = rng.integers(0, 10**6, size=n).astype(np.uint64)
+        run = int(size[1:-1].sum())
+        snaps.append((size, cost, kind))
+        reqs.append([run, run // 2, run // 5, run // 50, 1 << 20, run + 1])
+    return workloads.from_lists(snaps, reqs)
+
+
+@pytest.mark.parametrize("case", ["tickets", "queue", "long"])
 def test_window_search_replays(case):
     import paper_2311_00591_amd as coop
     if case == "tickets":
         a = workloads.make_config(0, 3)
+    elif case == "long":
+        a = _long_run_batch()
     else:
         a = workloads.make_config(3, 5, num_segments=1200)
     info = coop.plan_info(a.num_blocks, a.num_segments, a.num_requests)
