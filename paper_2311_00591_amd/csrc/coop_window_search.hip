@@ -406,12 +406,19 @@ __device__ __forceinline__ void chunk_range(const Params& P, uint64_t c, uint64_
     if (b > e) b = e;
 }
 
+// Staged boundaries in LDS, as 16-byte records: boundary i's key (R << 50 |
+// P, or plain P in a tile with a huge block) at kv[2i] and its cost prefix C
+// at kv[2i + 1], so that one 16-byte read fetches both (a merge step takes
+// two LDS reads); then the records of the end keys a merge may read past the
+// sentinel.
+constexpr uint32_t kKV = kXN + kMaxSteps;
+
 struct Smem {
-    // keys R << 50 | P (or plain P in a tile with a huge block), then the end
-    // keys a merge may read past the sentinel; 16-byte aligned (as is xc,
-    // which follows at a multiple of 16 bytes) for 16-byte staging stores
-    __attribute__((aligned(16))) uint64_t x[kXN + kMaxSteps];
-    uint64_t xc[kXN];   // C
+    __attribute__((aligned(16))) uint64_t kv[2 * kKV];
+    __device__ __forceinline__ uint64_t& K(uint32_t i) { return kv[2 * i]; }
+    __device__ __forceinline__ uint64_t K(uint32_t i) const { return kv[2 * i]; }
+    __device__ __forceinline__ uint64_t& C(uint32_t i) { return kv[2 * i + 1]; }
+    __device__ __forceinline__ uint64_t C(uint32_t i) const { return kv[2 * i + 1]; }
     uint16_t run[kXN];  // R, kept only in a tile with a huge block
     Sums wsum[kWaves];  // per-wavefront totals of the tile
     Sums hsum[4];       // per-wavefront totals of the halo
@@ -646,8 +653,8 @@ __device__ __forceinline__ coop_window_t to_window(const Key& k, uint64_t S) {
     return coop_window_t{k.start, k.end, k.cost};
 }
 
-__device__ __forceinline__ uint64_t lds_u64(const uint64_t* base, uint32_t byte_off) {
-    return *reinterpret_cast<const uint64_t*>(reinterpret_cast<const char*>(base) + byte_off);
+__device__ __forceinline__ ulonglong2 lds_u128(const uint64_t* base, uint32_t byte_off) {
+    return *reinterpret_cast<const ulonglong2*>(reinterpret_cast<const char*>(base) + byte_off);
 }
 
 // Merge steps per lane for `total` merge elements over `lanes` lanes, rounded
@@ -673,7 +680,7 @@ __device__ __forceinline__ uint32_t merge_steps(uint32_t total, uint32_t lanes) 
 // X[nB + 1] must be kEndKey, above every target, and so must the kMaxSteps
 // keys after it: a lane that has taken the start nB + 1 (the sentinel itself)
 // can take nothing more, and its end index runs on through those keys.  Only
-// the start is kept (as a byte offset, pA + pB growing by 8 a step gives the
+// the start is kept (as a byte offset, pA + pB growing by 16 a step gives the
 // end pointer); the caller finds the winner's end again (merged_answer).
 __device__ __forceinline__ void merge_pass(const Smem& sm, uint32_t nA, uint32_t nB, uint32_t d,
                                            uint32_t L, uint64_t Sc, Cand& best) {
@@ -682,21 +689,22 @@ __device__ __forceinline__ void merge_pass(const Smem& sm, uint32_t nA, uint32_t
     while (lo < hi) {
         const uint32_t mid = (lo + hi) >> 1;
         // start `mid` precedes end key X[d - mid] iff its target is at or below it
-        const bool before = sm.x[mid] + Sc <= sm.x[d - mid];
+        const bool before = sm.K(mid) + Sc <= sm.K(d - mid);
         lo = before ? mid + 1 : lo;
         hi = before ? hi : mid;
     }
-    uint32_t pA = lo * 8u;
-    const uint32_t sum0 = (d + 1) * 8u;  // pA + pB before the first step; grows by 8 a step
+    constexpr uint32_t kStep = 16u;  // bytes per boundary record
+    uint32_t pA = lo * kStep;
+    const uint32_t sum0 = (d + 1) * kStep;  // pA + pB before the first step; grows by kStep a step
     const int64_t sc = static_cast<int64_t>(Sc);
     uint64_t bc = kNone, bd = kNone;
     uint32_t bpa = kNone32;
     for (uint32_t k = 0; k < L; k += 2) {
 #pragma unroll
         for (uint32_t u = 0; u < 2; ++u) {
-            const uint32_t pB = sum0 + (k + u) * 8u - pA;
-            const uint64_t xa = lds_u64(sm.x, pA), kb = lds_u64(sm.x, pB);
-            const uint64_t ca = lds_u64(sm.xc, pA), cb = lds_u64(sm.xc, pB);
+            const uint32_t pB = sum0 + (k + u) * kStep - pA;
+            const ulonglong2 ra = lds_u128(sm.kv, pA), rb = lds_u128(sm.kv, pB);
+            const uint64_t xa = ra.x, ca = ra.y, kb = rb.x, cb = rb.y;
             const uint64_t D = kb - xa;
             const bool takeA = static_cast<int64_t>(D) >= sc;
             const bool valid = takeA & (D < (1ull << kValBits));
@@ -705,12 +713,12 @@ __device__ __forceinline__ void merge_pass(const Smem& sm, uint32_t nA, uint32_t
             bc = better ? cost : bc;
             bd = better ? D : bd;
             bpa = better ? pA : bpa;
-            pA += takeA ? 8u : 0u;
+            pA += takeA ? kStep : 0u;
         }
     }
     // Within a lane starts are met in increasing order, so strict comparison
     // kept the lowest start among equal (cost, bytes).
-    const Cand c{bc, bpa == kNone32 ? kNone : bd - Sc, bpa == kNone32 ? kNone32 : bpa / 8u};
+    const Cand c{bc, bpa == kNone32 ? kNone : bd - Sc, bpa == kNone32 ? kNone32 : bpa / kStep};
     if (cand_less(c, best)) best = c;
 }
 
@@ -722,7 +730,7 @@ __device__ __forceinline__ void plain_pass(const Smem& sm, uint32_t nA, uint32_t
                                            uint32_t& best_end) {
     for (uint32_t i = g; i < nA; i += lanes) {
         const uint32_t run = sm.run[i];
-        const uint64_t base = sm.x[i];
+        const uint64_t base = sm.K(i);
         uint32_t lo = i, hi = end;  // first k in [i, end) whose block closes the run
         while (lo < hi) {
             const uint32_t mid = (lo + hi) >> 1;
@@ -733,10 +741,10 @@ __device__ __forceinline__ void plain_pass(const Smem& sm, uint32_t nA, uint32_t
         hi = rend;
         while (lo < hi) {
             const uint32_t mid = (lo + hi) >> 1;
-            if (sm.x[mid + 1] - base >= S) hi = mid; else lo = mid + 1;
+            if (sm.K(mid + 1) - base >= S) hi = mid; else lo = mid + 1;
         }
         if (lo < rend) {
-            const Cand c{sm.xc[lo + 1] - sm.xc[i], sm.x[lo + 1] - base - S, i};
+            const Cand c{sm.C(lo + 1) - sm.C(i), sm.K(lo + 1) - base - S, i};
             if (cand_less(c, best)) {
                 best = c;
                 best_end = lo + 1;
@@ -788,11 +796,11 @@ __device__ __forceinline__ uint32_t pending_start(const Smem& sm, bool packed, u
         const uint64_t by_run = static_cast<uint64_t>(endrun) << kValBits;
         const uint64_t by_bytes = xend >= Sc ? xend - Sc + 1 : 0;
         const uint64_t thr = by_run > by_bytes ? by_run : by_bytes;
-        return wave_lower_bound(0, nA, lane, [&](uint32_t i) { return sm.x[i] >= thr; });
+        return wave_lower_bound(0, nA, lane, [&](uint32_t i) { return sm.K(i) >= thr; });
     }
     const uint32_t i0 =
         wave_lower_bound(0, nA, lane, [&](uint32_t i) { return sm.run[i] == endrun; });
-    return wave_lower_bound(i0, nA, lane, [&](uint32_t i) { return xend - sm.x[i] < S; });
+    return wave_lower_bound(i0, nA, lane, [&](uint32_t i) { return xend - sm.K(i) < S; });
 }
 
 // Where a wavefront's walk through the run past the staged region stands:
@@ -820,11 +828,11 @@ __device__ void walk_pass(const Params& P, const Smem& sm, uint32_t lane, uint32
     // A walk that would almost surely fail is not started: where the
     // snapshot goes on past the limit (as for a walk that fails), when the
     // first pending start needs more bytes past the region than twice the
-    // region holds (cq is the region's byte prefix at its end, sm.x[0] at
+    // region holds (cq is the region's byte prefix at its end, sm.K(0) at
     // its start; a pending start has fewer than S bytes to the region end).
     if (lim == pos + kWalkCap && lim < s1) {
-        const uint64_t rb = cq - (sm.x[0] & vmask);
-        if (S - (cq - (sm.x[cur] & vmask)) > (rb >> 63 ? kNone : rb << 1)) lim = pos;
+        const uint64_t rb = cq - (sm.K(0) & vmask);
+        if (S - (cq - (sm.K(cur) & vmask)) > (rb >> 63 ? kNone : rb << 1)) lim = pos;
     }
     // the blocks of the chunk at pos; the next chunk's are loaded before
     // this one is processed
@@ -859,12 +867,12 @@ __device__ void walk_pass(const Params& P, const Smem& sm, uint32_t lane, uint32
         const uint64_t lastc = fp ? readlane64(c, lastl) : cc;
         // no window from the first pending start ends in this chunk: none
         // from a later one does either (ends are monotone)
-        const bool none = fp == 0 || lastq - (sm.x[cur] & vmask) < S;
+        const bool none = fp == 0 || lastq - (sm.K(cur) & vmask) < S;
         for (; !none;) {
             const uint32_t i = cur + lane;
             const bool act = i < nA;
             const uint32_t ii = act ? i : nA - 1;
-            const uint64_t base = sm.x[ii] & vmask, cbase = sm.xc[ii];
+            const uint64_t base = sm.K(ii) & vmask, cbase = sm.C(ii);
             const bool ok = act && fp > 0 && lastq - base >= S;
             // the first chunk lane k < fp with q_k - base >= S
             uint32_t lo = 0, hi = lastl;
@@ -1034,10 +1042,10 @@ __device__ __forceinline__ TileState stage_tile(Smem& sm, const TileGeom& tg, ui
         ts.xcend = use_halo ? all_tot.c : tile_tot.c;
         ts.endrun = static_cast<uint32_t>(ts.xend >> kValBits);
         if (i0 + kItems <= nt) {
-            // Lanes 64 bytes apart would put the 16-byte stores of a
-            // wavefront on a few LDS banks: lane t stores its four pairs in
-            // the order (q + t) & 3, which spreads the wavefront over all of
-            // them.
+            // Lanes 128 bytes apart would put the 16-byte stores of a
+            // wavefront on a few LDS banks: lane t stores its four pairs of
+            // boundary records in the order (q + t) & 3, which spreads the
+            // wavefront over more of them.
             ulonglong2 px[kItems / 2], pc[kItems / 2];
 #pragma unroll
             for (uint32_t q = 0; q < kItems / 2; ++q) {
@@ -1060,22 +1068,23 @@ __device__ __forceinline__ TileState stage_tile(Smem& sm, const TileGeom& tg, ui
 #pragma unroll
             for (uint32_t q = 0; q < kItems / 2; ++q) {
                 const uint32_t at = i0 + 2 * ((q + rot) & 3u);
-                *reinterpret_cast<ulonglong2*>(&sm.x[at]) = px[q];
-                *reinterpret_cast<ulonglong2*>(&sm.xc[at]) = pc[q];
+                // the two boundaries' (key, cost) records
+                *reinterpret_cast<ulonglong2*>(&sm.kv[2 * at]) = ulonglong2{px[q].x, pc[q].x};
+                *reinterpret_cast<ulonglong2*>(&sm.kv[2 * at + 2]) = ulonglong2{px[q].y, pc[q].y};
             }
         } else {
 #pragma unroll
             for (uint32_t j = 0; j < kItems; ++j) {
                 if (i0 + j < nt) {
-                    sm.x[i0 + j] = base_x + r.sz[j];
-                    sm.xc[i0 + j] = base_c + r.ct[j];
+                    sm.K(i0 + j) = base_x + r.sz[j];
+                    sm.C(i0 + j) = base_c + r.ct[j];
                 }
             }
         }
         if (use_halo && tid < hm) {
             // halo boundary nt + tid: carry + wavefront inclusive - own block
-            sm.x[nt + tid] = hcarry_x + hs.q - hx_own;
-            sm.xc[nt + tid] = hcarry_c + hs.c - hc_own;
+            sm.K(nt + tid) = hcarry_x + hs.q - hx_own;
+            sm.C(nt + tid) = hcarry_c + hs.c - hc_own;
         }
     } else {
         uint32_t rr = carry.r + wi.r - t.r;  // pinned blocks before this thread's first block
@@ -1086,20 +1095,20 @@ __device__ __forceinline__ TileState stage_tile(Smem& sm, const TileGeom& tg, ui
 #pragma unroll
         for (uint32_t j = 0; j < kItems; ++j) {
             if (i0 + j < nt) {
-                sm.x[i0 + j] = base_x + r.sz[j] - (static_cast<uint64_t>(rr) << kValBits);
-                sm.xc[i0 + j] = base_c + r.ct[j];
+                sm.K(i0 + j) = base_x + r.sz[j] - (static_cast<uint64_t>(rr) << kValBits);
+                sm.C(i0 + j) = base_c + r.ct[j];
                 sm.run[i0 + j] = static_cast<uint16_t>(rr);
             }
             rr += kinds[j] >= COOP_PINNED ? 1u : 0u;
         }
     }
     if (tid == kThreads - 1) {
-        sm.x[ts.end] = ts.xend;
-        sm.xc[ts.end] = ts.xcend;
+        sm.K(ts.end) = ts.xend;
+        sm.C(ts.end) = ts.xcend;
         sm.run[ts.end] = static_cast<uint16_t>(ts.endrun);
-        sm.x[ts.end + 1] = kEndKey;  // sentinel end key
+        sm.K(ts.end + 1) = kEndKey;  // sentinel end key
     }
-    if (tid < kMaxSteps) sm.x[ts.end + 2 + tid] = kEndKey;  // what a merge reads past the sentinel
+    if (tid < kMaxSteps) sm.K(ts.end + 2 + tid) = kEndKey;  // what a merge reads past the sentinel
     __syncthreads();
     return ts;
 }
@@ -1202,9 +1211,9 @@ __device__ __forceinline__ Key merged_answer(const Smem& sm, const Cand& best, u
                                              uint64_t Sc, uint32_t end, uint32_t lane) {
     const Cand m = wave_argmin_packed(best);
     if (m.start == kNone32) return key_none();
-    const uint64_t target = sm.x[m.start] + Sc;
+    const uint64_t target = sm.K(m.start) + Sc;
     const uint32_t e = wave_lower_bound(m.start + 1, end + 1, lane,
-                                        [&](uint32_t k) { return sm.x[k] >= target; });
+                                        [&](uint32_t k) { return sm.K(k) >= target; });
     return Key{m.cost, m.excess + S, tl + m.start, tl + e};
 }
 
@@ -1862,7 +1871,7 @@ __device__ void stretch_merge(const Smem& sm, const EndSmem& es, const TileState
     const uint32_t L = merge_steps(total, kThreads);
     const uint32_t d = tid * L < total ? tid * L : total;
     auto target = [&](uint32_t i) -> uint64_t {
-        return i < na ? S - G - ((ts.xend - sm.x[cur + i]) & vmask) : kNone;
+        return i < na ? S - G - ((ts.xend - sm.K(cur + i)) & vmask) : kNone;
     };
     uint32_t lo = d > m ? d - m : 0, hi = d < na ? d : na;
     while (lo < hi) {
@@ -1878,7 +1887,7 @@ __device__ void stretch_merge(const Smem& sm, const EndSmem& es, const TileState
         const uint64_t T = target(ia), key = es.pb[ib];
         const bool take = key >= T;
         const bool valid = take & (ia < na) & (ib <= m);
-        const uint64_t cost = (ts.xcend - sm.xc[cur + (ia < na ? ia : 0)]) + GC + es.cb[ib];
+        const uint64_t cost = (ts.xcend - sm.C(cur + (ia < na ? ia : 0))) + GC + es.cb[ib];
         const uint64_t ex = key - T;
         const bool better = valid & ((cost < bc) | ((cost == bc) & (ex < bx)));
         bc = better ? cost : bc;
@@ -1930,7 +1939,7 @@ __device__ Key far_windows(const Params& P, const Smem& sm, EndSmem& es, const J
     // No pending start, or a window from the first one needs more bytes past
     // the region end than the run has left there (none from a later start
     // either): no window (the same in every thread).
-    if (cur >= nA || (run_left != kNone && S - ((ts.xend - sm.x[cur]) & vmask) > run_left))
+    if (cur >= nA || (run_left != kNone && S - ((ts.xend - sm.K(cur)) & vmask) > run_left))
         return key_none();
     Cand best = cand_none();
     uint64_t best_end = 0;
@@ -1943,10 +1952,10 @@ __device__ Key far_windows(const Params& P, const Smem& sm, EndSmem& es, const J
         // from the region end to the start of tile p + 1 is minus these
         uint64_t hq = 0, hc = 0, hr = 0;
         if (ts.end > nA) {
-            const uint64_t dd = ts.xend - sm.x[nA];
+            const uint64_t dd = ts.xend - sm.K(nA);
             hq = dd & kValMask;
             hr = dd >> kValBits;
-            hc = ts.xcend - sm.xc[nA];
+            hc = ts.xcend - sm.C(nA);
         }
         const uint64_t ge = tg.t0 + ts.end;  // global index of the region end
         uint64_t kmin = job.p + 1;
@@ -1964,7 +1973,7 @@ __device__ Key far_windows(const Params& P, const Smem& sm, EndSmem& es, const J
         }
         bool first_search = true;
         for (;;) {
-            const uint64_t need = S - ((ts.xend - sm.x[cur]) & vmask);
+            const uint64_t need = S - ((ts.xend - sm.K(cur)) & vmask);
             uint64_t fq, fc;
             const uint64_t k = find_tile(e, es, rb, nrec, job.tiles, kmin, carry, need, fq, fc);
             if (first_search && tid == 0) {  // read by the next tile's search (after barriers)
@@ -1997,7 +2006,7 @@ __device__ Key far_windows(const Params& P, const Smem& sm, EndSmem& es, const J
             // the first start whose window ends past this stretch
             const uint64_t last = es.pb[m], es_last_c = es.cb[m];
             const uint32_t nxt = wave_lower_bound(cur, nA, lane, [&](uint32_t i) {
-                return S - G - ((ts.xend - sm.x[i]) & vmask) > last;
+                return S - G - ((ts.xend - sm.K(i)) & vmask) > last;
             });
             __syncthreads();  // the stretch buffer is restaged next
             if (closed) run_left = G + last;  // the run ends in this stretch
@@ -2109,14 +2118,14 @@ __device__ void resolve_entry(const Params& P, Smem& sm, EndSmem& es, uint4 en, 
         // has the bytes between them fewer left.
         Between bt{kNone, 0, 0, false};
         if (prev_p != kNone && prev_p + 1 == job.p && ts.packed && prev_halo <= tg.nt) {
-            const uint64_t d = ts.xend - sm.x[prev_halo];
-            bt = Between{tg.t0 + prev_halo, d & kValMask, ts.xcend - sm.xc[prev_halo], (d >> kValBits) == 0};
+            const uint64_t d = ts.xend - sm.K(prev_halo);
+            bt = Between{tg.t0 + prev_halo, d & kValMask, ts.xcend - sm.C(prev_halo), (d >> kValBits) == 0};
         }
         run_left = bt.same_run && run_left != kNone && run_left >= bt.q ? run_left - bt.q : kNone;
         if (run_left == kNone && from_start != kNone && prev_p != kNone && prev_p + 1 == job.p && ts.packed) {
             // after tiles passed over: from the tile start when the region
             // holds no pinned block
-            const uint64_t d = ts.xend - sm.x[0];
+            const uint64_t d = ts.xend - sm.K(0);
             if ((d >> kValBits) == 0 && from_start >= d) run_left = from_start - d;
         }
         prev_p = job.p;
@@ -2142,7 +2151,7 @@ __device__ void resolve_entry(const Params& P, Smem& sm, EndSmem& es, uint4 en, 
         // the halo holds no pinned block
         from_start = kNone;
         if (run_left != kNone && ts.packed) {
-            const uint64_t d = ts.end > tg.nt ? ts.xend - sm.x[tg.nt] : 0;
+            const uint64_t d = ts.end > tg.nt ? ts.xend - sm.K(tg.nt) : 0;
             if ((d >> kValBits) == 0) from_start = run_left + d;
         }
         __syncthreads();  // LDS is restaged next
