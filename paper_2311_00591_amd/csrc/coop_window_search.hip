@@ -193,6 +193,35 @@ __device__ __forceinline__ uint64_t uniform64(uint64_t v) {
     return (static_cast<uint64_t>(uniform(static_cast<uint32_t>(v >> 32))) << 32) | uniform(static_cast<uint32_t>(v));
 }
 
+// v += v of the lane Ctrl names (0 where that lane is outside the row; rows
+// off in RowMask keep v), as one add and one add-with-carry whose first
+// operand is the moved lane (DPP on the adds themselves).  The compiler
+// moves each half with its own instruction and then adds, three times the
+// instructions; these sums are most of the staging scans.  The s_nop gives
+// the two wait states a DPP read needs after a VALU write of its source.
+#define COOP_ADD_DPP64(lo, hi, ctrl, mask)                                                     \
+    asm volatile("s_nop 1\n\t"                                                                \
+                 "v_add_co_u32_dpp %0, vcc, %0, %0 " ctrl " row_mask:" mask                    \
+                 " bank_mask:0xf bound_ctrl:1\n\t"                                             \
+                 "v_addc_co_u32_dpp %1, vcc, %1, %1, vcc " ctrl " row_mask:" mask              \
+                 " bank_mask:0xf bound_ctrl:1"                                                 \
+                 : "+v"(lo), "+v"(hi)                                                          \
+                 :                                                                             \
+                 : "vcc")
+
+template <int Ctrl, int RowMask>
+__device__ __forceinline__ void add_dpp64(uint64_t& v) {
+    uint32_t lo = static_cast<uint32_t>(v), hi = static_cast<uint32_t>(v >> 32);
+    if constexpr (Ctrl == kRowShr1 && RowMask == 0xf) COOP_ADD_DPP64(lo, hi, "row_shr:1", "0xf");
+    else if constexpr (Ctrl == kRowShr2 && RowMask == 0xf) COOP_ADD_DPP64(lo, hi, "row_shr:2", "0xf");
+    else if constexpr (Ctrl == kRowShr4 && RowMask == 0xf) COOP_ADD_DPP64(lo, hi, "row_shr:4", "0xf");
+    else if constexpr (Ctrl == kRowShr8 && RowMask == 0xf) COOP_ADD_DPP64(lo, hi, "row_shr:8", "0xf");
+    else if constexpr (Ctrl == kRowBcast15 && RowMask == 0xa) COOP_ADD_DPP64(lo, hi, "row_bcast:15", "0xa");
+    else if constexpr (Ctrl == kRowBcast31 && RowMask == 0xc) COOP_ADD_DPP64(lo, hi, "row_bcast:31", "0xc");
+    else static_assert(Ctrl < 0, "a DPP control without an add form");
+    v = (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
 // Prefix-sum element: bytes (or packed key), effective cost, pinned count (or
 // a flag).
 struct Sums {
@@ -202,8 +231,8 @@ struct Sums {
 
 template <int Ctrl, int RowMask>
 __device__ __forceinline__ void sum_step(Sums& s) {
-    s.q += dpp64<Ctrl, RowMask>(s.q, 0);
-    s.c += dpp64<Ctrl, RowMask>(s.c, 0);
+    add_dpp64<Ctrl, RowMask>(s.q);
+    add_dpp64<Ctrl, RowMask>(s.c);
     s.r += dpp32<Ctrl, RowMask>(s.r, 0);
 }
 
@@ -929,8 +958,8 @@ struct TileState {
 
 template <int Ctrl, int RowMask>
 __device__ __forceinline__ void sum2_step(Sums& s) {
-    s.q += dpp64<Ctrl, RowMask>(s.q, 0);
-    s.c += dpp64<Ctrl, RowMask>(s.c, 0);
+    add_dpp64<Ctrl, RowMask>(s.q);
+    add_dpp64<Ctrl, RowMask>(s.c);
 }
 
 // Inclusive sums of q and c (r untouched) over the rows, and over the wavefront.
@@ -1692,9 +1721,9 @@ __device__ __forceinline__ Sums3 add3(const Sums3& a, const Sums3& b) {
 
 template <int Ctrl, int RowMask>
 __device__ __forceinline__ void sum3_step(Sums3& s) {
-    s.q += dpp64<Ctrl, RowMask>(s.q, 0);
-    s.c += dpp64<Ctrl, RowMask>(s.c, 0);
-    s.r += dpp64<Ctrl, RowMask>(s.r, 0);
+    add_dpp64<Ctrl, RowMask>(s.q);
+    add_dpp64<Ctrl, RowMask>(s.c);
+    add_dpp64<Ctrl, RowMask>(s.r);
 }
 
 __device__ __forceinline__ void wave_inclusive_sum3(Sums3& s) {
