@@ -92,11 +92,22 @@ __device__ __forceinline__ U128 add128(U128 a, U128 b) {
     return r;
 }
 
+// a - b as one chain of subtract-with-borrow over the four 32-bit words:
+// four instructions, where the compiler's form (a 64-bit difference of each
+// half, the borrow taken from a compare and a select) took eight in the
+// merge step.
 __device__ __forceinline__ U128 sub128(U128 a, U128 b) {
-    U128 r;
-    r.lo = a.lo - b.lo;
-    r.hi = a.hi - b.hi - (a.lo < b.lo ? 1u : 0u);
-    return r;
+    uint32_t w0 = static_cast<uint32_t>(a.lo), w1 = static_cast<uint32_t>(a.lo >> 32);
+    uint32_t w2 = static_cast<uint32_t>(a.hi), w3 = static_cast<uint32_t>(a.hi >> 32);
+    asm volatile("v_sub_co_u32 %0, vcc, %0, %4\n\t"
+                 "v_subb_co_u32 %1, vcc, %1, %5, vcc\n\t"
+                 "v_subb_co_u32 %2, vcc, %2, %6, vcc\n\t"
+                 "v_subb_co_u32 %3, vcc, %3, %7, vcc"
+                 : "+v"(w0), "+v"(w1), "+v"(w2), "+v"(w3)
+                 : "v"(static_cast<uint32_t>(b.lo)), "v"(static_cast<uint32_t>(b.lo >> 32)),
+                   "v"(static_cast<uint32_t>(b.hi)), "v"(static_cast<uint32_t>(b.hi >> 32))
+                 : "vcc");
+    return U128{(static_cast<uint64_t>(w1) << 32) | w0, (static_cast<uint64_t>(w3) << 32) | w2};
 }
 
 // h (binary64) in units of 2^-64, rounded to nearest, ties to even.  False
