@@ -2324,13 +2324,19 @@ bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests
     uint64_t c1 = chunk, c2 = chunk, u1 = pl->units, nchunks = pl->grid;
     uint64_t pc = (T + chunk - 1) / chunk + 1;
     if (chunk >= kQueueMinChunk && cap >= 4 && num_segments <= kQueueMaxSegments) {
-        const uint64_t q1 = chunk - chunk / 4, q2 = chunk / 16 ? chunk / 16 : 1;
-        const uint64_t qu1 = pl->grid * q1;
-        const uint64_t qn = pl->grid + (pl->units - qu1 + q2 - 1) / q2;
+        // With a queue the first chunks need not cover the units: every
+        // workgroup slot takes one (unless the partial budget grew the
+        // chunks), e.g. 512 workgroups instead of 507 for 20274 units.
+        const uint64_t qg = chunk == (pl->units + grid - 1) / grid ? grid : pl->grid;
+        const uint64_t share = pl->units / qg;
+        const uint64_t q1 = share - share / 4, q2 = chunk / 16 ? chunk / 16 : 1;
+        const uint64_t qu1 = qg * q1;
+        const uint64_t qn = qg + (pl->units - qu1 + q2 - 1) / q2;
         uint64_t qpc = (T + q2 - 1) / q2 + 2;
         if (qpc > cap) qpc = cap;
         if (qpc > qn) qpc = qn;
-        if (qu1 < pl->units && qpc >= 4) {
+        if (q1 >= 1 && qu1 < pl->units && qpc >= 4) {
+            pl->grid = qg;
             c1 = q1;
             c2 = q2;
             u1 = qu1;
