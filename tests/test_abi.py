@@ -137,6 +137,44 @@ def test_plan_queue_and_partial_slots():
     assert lib.coop_window_search_plan(1, 1, 1, None) == -1
 
 
+@pytest.mark.parametrize("n", [1, 4097, 1_000_003, 66_267_909, 1 << 24, 1 << 30])
+@pytest.mark.parametrize("b", [1, 7, 1024, 4096, 1 << 15])
+@pytest.mark.parametrize("per", [1, 4, 16, 600])
+def test_plan_chunks_cover_every_unit(n, b, per):
+    if b > n:
+        pytest.skip("more snapshots than blocks")
+    q = b * per
+    p = coop.plan_info(n, b, q)
+    units, grid = p["units"], p["workgroups"]
+    assert 1 <= grid <= 512 and grid <= units
+    c1, u1, c2 = p["first_chunk_units"], p["first_units"], p["queued_chunk_units"]
+    if p["chunks_max"] > grid:
+        # with a queue: the first chunks tile [0, u1), the queued ones the rest
+        assert u1 == grid * c1 < units and c1 >= 1 and c2 >= 1
+        assert u1 + (p["chunks_max"] - grid) * c2 >= units
+        # every workgroup slot takes a first chunk unless the partial
+        # budget grew the chunks (a snapshot of T tiles must meet at most
+        # cap chunks, cap = the budget's keys per request)
+        g0 = min(units, 512)
+        chunk0 = -(-units // g0)
+        tiles = -(-n // 4096) + 1
+        cap = max((1 << 23) // q, 2)
+        if -(-tiles // chunk0) + 1 <= cap:
+            assert grid == g0
+    else:
+        assert u1 == units and grid * c1 >= units > (grid - 1) * c1
+    assert p["partial_slots"] >= 1 and p["partial_slots"] <= p["chunks_max"]
+    if q <= 1 << 21:
+        assert p["partial_slots"] * q <= 1 << 23
+
+
+def test_plan_takes_every_workgroup_slot_on_the_ragged_batch():
+    # 20274 units over 512 workgroups: 30 first units each, the rest queued
+    p = coop.plan_info(66_267_909, 4096, 16384)
+    assert p["units"] == 20274 and p["workgroups"] == 512
+    assert p["first_units"] == 512 * 30
+
+
 def test_replay_rejects_unknown_policy_and_null_buffers():
     # validation happens before any launch, so no GPU is touched
     lib = coop.load_library()
