@@ -704,11 +704,20 @@ __device__ __forceinline__ uint32_t merge_steps(uint32_t total, uint32_t lanes) 
 // count.  Windows are ranked by (cost, D), which orders them as (cost,
 // bytes - S).  Steps past the lane's slice repeat work of the next lane
 // (harmless: equal windows).  A lane may take starts past nA (boundaries of
-// the halo): their windows are real windows of the snapshot, the shortest
-// from that start within the staged region, so scoring them is harmless too.
-// X[nB + 1] must be kEndKey, above every target, and so must the kMaxSteps
-// keys after it: a lane that has taken the start nB + 1 (the sentinel itself)
-// can take nothing more, and its end index runs on through those keys.  Only
+// the halo): their windows are real windows of the snapshot, though not
+// always the shortest from that start (the diagonal split counts only the
+// starts below nA), so never better than the window the next tile finds
+// for it; scoring them is harmless too.
+// nB is the region end or an end key whose run id is above every target of
+// a start below nA (the one that takes in the first pinned block after the
+// tile): all nA starts are merged within the first nA + nB elements either
+// way.  Past them a lane merges the staged keys that follow, which are
+// real; a lane whose diagonal lies past nA + nB pairs halo starts with end
+// keys past that pinned block, which never gives a valid window.  The
+// region end is followed by kEndKey, above every target, and so are the
+// kMaxSteps keys after it: a lane that has taken the start after the region
+// end (the sentinel itself) can take nothing more, and its end index runs
+// on through those keys.  Only
 // the start is kept (as a byte offset, pA + pB growing by 16 a step gives the
 // end pointer); the caller finds the winner's end again (merged_answer).
 __device__ __forceinline__ void merge_pass(const Smem& sm, uint32_t nA, uint32_t nB, uint32_t d,
@@ -1283,6 +1292,18 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
     const uint64_t mine = tasks > w ? (tasks - w + kWaves - 1) / kWaves : 0;
     const uint32_t held = mine < 64 ? static_cast<uint32_t>(mine) : 64u;
     uint32_t pend = nt;  // lane n: first pending start of task n
+    // No window of a tile start crosses a pinned block, so every tile start
+    // is merged by the end key that takes in the first pinned block after
+    // the tile (its run id is above every tile start's target); the end keys
+    // after it matter to no tile start.  Looked for only where leaving them
+    // out can shorten the lanes' slices.
+    uint32_t mend = end;
+    if (ts.packed && end > nt + 1 &&
+        merge_steps(2 * nt + 1, lanes) < merge_steps(nt + end, lanes)) {
+        const uint64_t thr = ((sm.K(nt) >> kValBits) + 1) << kValBits;
+        mend = wave_lower_bound(nt + 1, end + 1, lane, [&](uint32_t i) { return sm.K(i) >= thr; });
+        mend = mend < end ? mend : end;
+    }
 
     // ---- in-region windows of every held task
     for (uint32_t n = 0; n < held; ++n) {
@@ -1296,10 +1317,10 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
             const uint32_t gl = sl * 64u + lane;
             uint32_t e32 = 0;
             if (ts.packed) {
-                const uint32_t total = nt + end;
+                const uint32_t total = nt + mend;
                 const uint32_t L = merge_steps(total, lanes);
                 const uint32_t d = gl * L < total ? gl * L : total;
-                merge_pass(sm, nt, end, d, L, Sc, best);
+                merge_pass(sm, nt, mend, d, L, Sc, best);
             } else {
                 plain_pass(sm, nt, end, gl, lanes, S, best, e32);
             }
@@ -1357,11 +1378,11 @@ __device__ __forceinline__ void tile_requests(const Params& P, Smem& sm, const J
                 const uint64_t Sc = S < (1ull << kValBits) ? S : (1ull << kValBits);
                 uint32_t e32 = 0;
                 if (ts.packed) {
-                    const uint32_t total = nt + end;
+                    const uint32_t total = nt + mend;
                     const uint32_t L = merge_steps(total, 64u);
                     const uint32_t d = lane * L < total ? lane * L : total;
                     Cand bm = cand_none();
-                    merge_pass(sm, nt, end, d, L, Sc, bm);
+                    merge_pass(sm, nt, mend, d, L, Sc, bm);
                     km = merged_answer(sm, bm, tl, S, Sc, end, lane);
                 } else {
                     plain_pass(sm, nt, end, lane, 64u, S, best, e32);

@@ -99,6 +99,38 @@ def test_tile_edges_and_ragged_tails():
     assert_parity(pools, gpu_search(pools), "tile edges")
 
 
+def test_merge_stops_at_the_halos_first_pinned_block():
+    """Tiles whose halo holds its first pinned block at offsets 0, 1, 5,
+    128, 255 or nowhere; 16 requests per snapshot (one wavefront per
+    request: the merge leaves out the end keys past that block), 4 and 1
+    (wider slices: it keeps them); equal sizes and costs give many equal
+    windows across the tile ends."""
+    _announce("merge end at the halo's first pinned block")
+    rng = np.random.default_rng(23)
+    snaps, reqs = [], []
+    for off in (0, 1, 5, 128, 255, None):
+        for nreq, equal in ((16, False), (16, True), (4, False), (1, False)):
+            n = 2 * TILE + 300
+            if equal:
+                size = np.full(n, 4096, dtype=np.uint64)
+                cost = np.full(n, 7, dtype=np.uint64)
+                kind = np.ones(n, dtype=np.uint8)
+            else:
+                size = (rng.integers(1, 64, size=n) * 512).astype(np.uint64)
+                cost = rng.integers(0, 1000, size=n).astype(np.uint64)
+                kind = rng.choice([0, 1, 1, 1, 1, 1, 1, 1], size=n).astype(np.uint8)
+                kind[rng.random(n) < 0.01] = 2
+            for e in (TILE, 2 * TILE):  # each tile's halo: pinned only from off on
+                kind[e:e + 256][kind[e:e + 256] >= 2] = 1
+                if off is not None and e + off < n:
+                    kind[e + off] = 3
+            snaps.append((size, cost, kind))
+            base = [1, 4096, 3 * 4096 + 1, 40 * 4096, 300 * 4096, 5000 * 4096, 1 << 40]
+            reqs.append([int(base[i % len(base)] + rng.integers(0, 4096)) for i in range(nreq)])
+    pools = _pools(snaps, reqs)
+    assert_parity(pools, gpu_search(pools), "halo's first pinned block")
+
+
 def _clustered_kinds(rng, n, pinned_mean, open_mean):
     """Alternating pinned and open stretches of geometric lengths; inside an
     open stretch a fifth of the blocks are free."""
