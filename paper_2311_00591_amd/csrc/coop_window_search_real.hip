@@ -510,8 +510,11 @@ __device__ void walk_global(const Prefix& pf, uint64_t i, uint64_t i_end, uint64
 // nA + 1 <= 2049) and walks the same number of steps; a
 // start meets, when it is merged, the first end key at or above its target,
 // the end of its shortest window, and is scored on the spot (valid iff the
-// keys differ by less than 2^51: no pinned block between).  mine[r] receives
-// the lane's least window (batch indices).
+// keys differ by less than 2^51: no pinned block between).  nB may be the
+// end key that takes in the first pinned block after the chunk, by which
+// every start is merged; a lane past nA + nB only moves its end index on
+// through the staged keys and the end-key padding, as no start past nA is
+// taken.  mine[r] receives the lane's least window (batch indices).
 template <int NR>
 __device__ __forceinline__ void merge_requests(const uint64_t* Y, const U128* Cr, uint32_t nA,
                                                uint32_t nB, const uint64_t (&S)[NR], uint64_t c0,
@@ -663,6 +666,28 @@ __global__ __launch_bounds__(kSThreads, 4) void real_search_kernel(Prefix pf, Se
                 __syncthreads();
                 const bool packed_chunk = big_flag == 0;
                 const uint64_t span = packed_chunk ? Y[nB] & (kPackOne - 1) : 0;
+                // No window crosses a pinned block, so every start of the
+                // chunk is merged by the end key that takes in the first
+                // pinned block after it (its run field is above every
+                // start's target): the merges stop there.  Found by the
+                // wavefront, 64 keys a round.
+                uint32_t mB = nB;
+                if (packed_chunk && nB > nA + 1) {
+                    const uint64_t thr = ((Y[nA] >> kPackBits) + 1) << kPackBits;
+                    uint32_t lo = nA + 1, hi = nB + 1;  // first k in [lo, hi) with Y[k] >= thr, else hi
+                    while (hi - lo > 64) {
+                        const uint32_t step = (hi - lo + 63) >> 6;
+                        const uint32_t i = lo + lane * step;
+                        const uint64_t mk = __ballot(i >= hi || Y[i] >= thr);
+                        const uint32_t f = mk ? static_cast<uint32_t>(__builtin_ctzll(mk)) : 64u;
+                        const uint32_t nhi = f < 64 ? lo + f * step : hi;
+                        lo = f ? lo + (f - 1) * step + 1 : lo;
+                        hi = nhi < hi ? nhi : hi;
+                    }
+                    const uint64_t mk = __ballot(lo + lane >= hi || Y[lo + lane] >= thr);
+                    const uint32_t k = mk ? lo + static_cast<uint32_t>(__builtin_ctzll(mk)) : hi;
+                    mB = k < nB ? k : nB;
+                }
                 // starts whose target is above every staged end key: their windows
                 // end past hi (or nowhere); a suffix of the chunk, walked globally
                 // by the request's lanes (true when some start was walked)
@@ -699,7 +724,7 @@ __global__ __launch_bounds__(kSThreads, 4) void real_search_kernel(Prefix pf, Se
                     if (pair && fast(S0) && fast(S1)) {
                         const uint64_t SS[2] = {S0, S1};
                         Best m2[2] = {best_none(), best_none()};
-                        merge_requests<2>(Y, Cr, nA, nB, SS, c0, gl, lanes, m2);
+                        merge_requests<2>(Y, Cr, nA, mB, SS, c0, gl, lanes, m2);
 #pragma unroll
                         for (uint32_t u = 0; u < 2; ++u) {
                             const bool walked = pending(SS[u], m2[u]);
@@ -714,7 +739,7 @@ __global__ __launch_bounds__(kSThreads, 4) void real_search_kernel(Prefix pf, Se
                         if (fast(S)) {
                             const uint64_t SS[1] = {S};
                             Best m1[1] = {best_none()};
-                            merge_requests<1>(Y, Cr, nA, nB, SS, c0, gl, lanes, m1);
+                            merge_requests<1>(Y, Cr, nA, mB, SS, c0, gl, lanes, m1);
                             mine = m1[0];
                             pending(S, mine);
                         } else {

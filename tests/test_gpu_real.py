@@ -132,6 +132,38 @@ def test_windows_longer_than_the_staged_prefixes():
     assert_parity(pools, h, "long windows")
 
 
+def test_merges_stop_at_the_first_pinned_block_after_the_chunk():
+    """Pinned blocks from none to dense, so that the first one after a
+    chunk's 2048 starts lies anywhere in the 512 staged blocks that follow
+    (the merges stop at the end key that takes it in), with 1, 4 and 16
+    requests per snapshot (one or two merges a lane)."""
+    rng = np.random.default_rng(29)
+    snaps, reqs, hs = [], [], []
+    for p_pin in (0.0, 0.002, 0.02, 0.2):
+        for nreq in (1, 4, 16):
+            n = 3 * 2048 + 600
+            size = rng.integers(1, 64, n) * 512
+            kind = np.where(rng.random(n) < p_pin, 2, 1)
+            kind[rng.random(n) < 0.1] = 0
+            snaps.append((size, rng.integers(0, 1000, n), kind))
+            base = [1, 4096, 3 * 4096 + 1, 40 * 4096, 300 * 4096, 5000 * 4096, 1 << 40]
+            reqs.append([int(base[i % len(base)] + rng.integers(0, 4096)) for i in range(nreq)])
+            hs.append(rng.integers(1, 10**6, n) / rng.integers(1, 3000, n))
+    # pinned blocks right at and after the first chunk's end
+    n = 2 * 2048 + 600
+    size = np.full(n, 4096)
+    kind = np.ones(n, dtype=np.int64)
+    kind[[2047, 2048, 2049, 2300]] = 2
+    snaps.append((size, np.full(n, 7), kind))
+    reqs.append([1, 4096, 8192, 3 * 4096, 100 * 4096])
+    hs.append(np.full(n, 0.5))
+    pools = workloads.from_lists(snaps, reqs)
+    _announce("merges stop at the first pinned block after the chunk")
+    h = np.concatenate(hs).astype(np.float64)
+    h[pools.kind != 1] = 0.0
+    assert_parity(pools, h, "first pinned block after the chunk")
+
+
 def test_exact_sums_round_to_binary64():
     """Exact sums with more than 53 significant bits: ties to even, both
     ways, and plain rounding, each in a snapshot of its own."""
