@@ -1692,7 +1692,10 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
         // ---- prefetch the next tile
         const TileGeom tn = has_next ? tile_geom(next) : TileGeom{tg.t0, 0u, 0u, 0u};
         issue_loads(P, tn, t, regs);
-        // ---- 2./3. the requests
+        // ---- 2./3. the requests, at a raised wave priority up to the end of
+        // the tile, so that the other workgroup on the CU, when it stages a
+        // tile meanwhile, yields issue slots to them
+        __builtin_amdgcn_s_setprio(1);
         tile_requests(P, sm, job, tg, ts, wpr, t, acc, s_lane);
         __syncthreads();  // LDS is restaged next
         // a job some wavefront deferred keeps its keys in the partial slots
@@ -1706,6 +1709,7 @@ __global__ __launch_bounds__(kThreads, 4) void coop_window_search_kernel(Params 
                 combine_partials(P, job, t, last_flag);
             }
         }
+        __builtin_amdgcn_s_setprio(0);
         if (!has_next) break;
         job = next;
         tg = tn;
