@@ -626,6 +626,7 @@ __global__ __launch_bounds__(kSThreads, 4) void real_search_kernel(Prefix pf, Se
                 const uint32_t nB = static_cast<uint32_t>(hi - c0);
                 const uint64_t pbase = pf.P(c0), rbase = pf.R(c0);
                 const U128 cbase = pf.C(c0);
+                __builtin_amdgcn_s_setprio(0);  // staging at the normal priority
                 if (tid == 0) big_flag = 0;
                 __syncthreads();  // the previous chunk's readers are done; flag cleared
                 // kStageBatch indices per thread at a time, their loads issued
@@ -664,6 +665,9 @@ __global__ __launch_bounds__(kSThreads, 4) void real_search_kernel(Prefix pf, Se
                 }
                 if (big) big_flag = 1;
                 __syncthreads();
+                // the merges at a raised wave priority: the other workgroup on
+                // the CU, when it stages a chunk meanwhile, yields issue slots
+                __builtin_amdgcn_s_setprio(1);
                 const bool packed_chunk = big_flag == 0;
                 const uint64_t span = packed_chunk ? Y[nB] & (kPackOne - 1) : 0;
                 // No window crosses a pinned block, so every start of the
