@@ -2340,9 +2340,10 @@ bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests
         if (need > chunk) chunk = need;
     }
     pl->grid = (pl->units + chunk - 1) / chunk;
-    // A quarter of each workgroup's share goes to the queue, in chunks of at
-    // least a sixteenth of it (and one unit), so that the workgroups finish
-    // together.  The kernel lengthens queued chunks until the largest
+    // An eighth of each workgroup's share goes to the queue, in chunks of
+    // at least a sixteenth of it (and one unit), so that the workgroups
+    // finish together (a quarter or more costs a snapshot lookup per queued
+    // chunk, a sixteenth leaves them apart).  The kernel lengthens queued chunks until the largest
     // snapshot spans at most pc - 2 of them (a span of L units meets at most
     // ceil(L / c2) + 2 chunks); pc, the partial slots per request, stays
     // within the budget.
@@ -2354,7 +2355,7 @@ bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests
         // chunks), e.g. 512 workgroups instead of 507 for 20274 units.
         const uint64_t qg = chunk == (pl->units + grid - 1) / grid ? grid : pl->grid;
         const uint64_t share = pl->units / qg;
-        const uint64_t q1 = share - share / 4, q2 = chunk / 16 ? chunk / 16 : 1;
+        const uint64_t q1 = share - share / 8, q2 = chunk / 16 ? chunk / 16 : 1;
         const uint64_t qu1 = qg * q1;
         const uint64_t qn = qg + (pl->units - qu1 + q2 - 1) / q2;
         uint64_t qpc = (T + q2 - 1) / q2 + 2;

@@ -120,7 +120,7 @@ def test_gpu_path_shares_nothing_with_the_oracle():
 
 
 def test_plan_queue_and_partial_slots():
-    # a quarter of the units go through the queue once each workgroup has at
+    # an eighth of the units go through the queue once each workgroup has at
     # least 8; the first chunks tile [0, first_units) exactly
     p = coop.plan_info(66_267_909, 4096, 16384)
     assert p["chunks_max"] > p["workgroups"] and 256 < p["workgroups"] <= 512
@@ -169,10 +169,10 @@ def test_plan_chunks_cover_every_unit(n, b, per):
 
 
 def test_plan_takes_every_workgroup_slot_on_the_ragged_batch():
-    # 20274 units over 512 workgroups: 30 first units each, the rest queued
+    # 20274 units over 512 workgroups: 35 first units each, the rest queued
     p = coop.plan_info(66_267_909, 4096, 16384)
     assert p["units"] == 20274 and p["workgroups"] == 512
-    assert p["first_units"] == 512 * 30
+    assert p["first_units"] == 512 * 35
 
 
 def test_replay_rejects_unknown_policy_and_null_buffers():
