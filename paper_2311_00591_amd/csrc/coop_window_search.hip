@@ -2340,10 +2340,11 @@ bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests
         if (need > chunk) chunk = need;
     }
     pl->grid = (pl->units + chunk - 1) / chunk;
-    // An eighth of each workgroup's share goes to the queue, in chunks of
-    // at least a sixteenth of it (and one unit), so that the workgroups
-    // finish together (a quarter or more costs a snapshot lookup per queued
-    // chunk, a sixteenth leaves them apart).  The kernel lengthens queued chunks until the largest
+    // An eighth of each workgroup's share goes to the queue (a quarter with
+    // fewer than 64 snapshots, whose units differ more in cost: windows
+    // cluster in parts of a run), in chunks of at least a sixteenth of it
+    // (and one unit), so that the workgroups finish together.  Every queued
+    // chunk looks its snapshot up again; a sixteenth leaves them apart.  The kernel lengthens queued chunks until the largest
     // snapshot spans at most pc - 2 of them (a span of L units meets at most
     // ceil(L / c2) + 2 chunks); pc, the partial slots per request, stays
     // within the budget.
@@ -2355,7 +2356,8 @@ bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests
         // chunks), e.g. 512 workgroups instead of 507 for 20274 units.
         const uint64_t qg = chunk == (pl->units + grid - 1) / grid ? grid : pl->grid;
         const uint64_t share = pl->units / qg;
-        const uint64_t q1 = share - share / 8, q2 = chunk / 16 ? chunk / 16 : 1;
+        const uint64_t q1 = share - share / (num_segments >= 64 ? 8 : 4);
+        const uint64_t q2 = chunk / 16 ? chunk / 16 : 1;
         const uint64_t qu1 = qg * q1;
         const uint64_t qn = qg + (pl->units - qu1 + q2 - 1) / q2;
         uint64_t qpc = (T + q2 - 1) / q2 + 2;

@@ -120,8 +120,9 @@ def test_gpu_path_shares_nothing_with_the_oracle():
 
 
 def test_plan_queue_and_partial_slots():
-    # an eighth of the units go through the queue once each workgroup has at
-    # least 8; the first chunks tile [0, first_units) exactly
+    # an eighth of the units (a quarter with fewer than 64 snapshots) go
+    # through the queue once each workgroup has at least 8; the first chunks
+    # tile [0, first_units) exactly
     p = coop.plan_info(66_267_909, 4096, 16384)
     assert p["chunks_max"] > p["workgroups"] and 256 < p["workgroups"] <= 512
     assert p["first_units"] == p["workgroups"] * p["first_chunk_units"] < p["units"]
@@ -166,6 +167,13 @@ def test_plan_chunks_cover_every_unit(n, b, per):
     assert p["partial_slots"] >= 1 and p["partial_slots"] <= p["chunks_max"]
     if q <= 1 << 21:
         assert p["partial_slots"] * q <= 1 << 23
+
+
+def test_plan_queues_a_quarter_with_few_snapshots():
+    # one snapshot of 2^24 blocks, 16 requests: 4097 units, a share of 8, 6 first units each
+    p = coop.plan_info(1 << 24, 1, 16)
+    assert p["workgroups"] == 512 and p["first_chunk_units"] == 8 - 8 // 4
+    assert p["first_units"] == 512 * p["first_chunk_units"] < p["units"]
 
 
 def test_plan_takes_every_workgroup_slot_on_the_ragged_batch():
