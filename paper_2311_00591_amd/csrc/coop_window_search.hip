@@ -2340,11 +2340,12 @@ bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests
         if (need > chunk) chunk = need;
     }
     pl->grid = (pl->units + chunk - 1) / chunk;
-    // An eighth of each workgroup's share goes to the queue (a quarter with
-    // fewer than 64 snapshots, whose units differ more in cost: windows
-    // cluster in parts of a run), in chunks of at least a sixteenth of it
-    // (and one unit), so that the workgroups finish together.  Every queued
-    // chunk looks its snapshot up again; a sixteenth leaves them apart.  The kernel lengthens queued chunks until the largest
+    // An eighth of each workgroup's share goes to the queue in chunks of one
+    // unit, so that the workgroups finish together; with fewer than 64
+    // snapshots, whose units differ more in cost (windows cluster in parts
+    // of a run), a quarter in chunks of a sixteenth of the share.  Every
+    // queued chunk looks its snapshot up again; a sixteenth of the share in
+    // the queue leaves the workgroups apart.  The kernel lengthens queued chunks until the largest
     // snapshot spans at most pc - 2 of them (a span of L units meets at most
     // ceil(L / c2) + 2 chunks); pc, the partial slots per request, stays
     // within the budget.
@@ -2357,7 +2358,7 @@ bool make_plan(uint64_t num_blocks, uint64_t num_segments, uint64_t num_requests
         const uint64_t qg = chunk == (pl->units + grid - 1) / grid ? grid : pl->grid;
         const uint64_t share = pl->units / qg;
         const uint64_t q1 = share - share / (num_segments >= 64 ? 8 : 4);
-        const uint64_t q2 = chunk / 16 ? chunk / 16 : 1;
+        const uint64_t q2 = num_segments >= 64 || chunk < 16 ? 1 : chunk / 16;
         const uint64_t qu1 = qg * q1;
         const uint64_t qn = qg + (pl->units - qu1 + q2 - 1) / q2;
         uint64_t qpc = (T + q2 - 1) / q2 + 2;
